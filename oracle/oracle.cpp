@@ -1,0 +1,577 @@
+/*
+ * oracle.cpp -- reference oracle for claim-scoped KV materialization checking.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke entry point and
+ * the benchmark's CPU-baseline leg may load this library.  The product path
+ * (the HIP library and its Python binding) never links, loads or calls it,
+ * and it shares no source, header, table or helper with that path.
+ *
+ * It is deliberately plain: single-threaded loops that follow the
+ * definitions one statement at a time, with no blocking, fusion or
+ * reordering, so that a reader can check it against the definitions below
+ * by eye.  Speed is not a goal.
+ *
+ * What is computed, and where it comes from:
+ *
+ *  - Claim semantics (the paper, "Fail-Closed Lowering of Resident KV Claims
+ *    onto LLM Serving Runtimes"):
+ *      * a claim is an accepted future-reuse responsibility with a stable id,
+ *        a footprint and a predicate (section 1, Table 1 claim_identity,
+ *        explicit_acceptance, materialization_predicate);
+ *      * lifecycle order accept -> offloaded -> restore-required -> restored,
+ *        or -> restoration_failed -> active_request_refused with the claim in
+ *        blocking_claim_ids (section 1 running example; section 7 event list
+ *        E0..E14 and witness paths A and B);
+ *      * only failures of the claim's own blocks count (section 7 path C,
+ *        Table 9 last row); a reported load failure is not undone by later
+ *        correct bytes (Table 9, fallback recompute row);
+ *      * ambiguity yields no claim outcome (Table 2, last rule; Table 5, last
+ *        row): missing registry, unstable ids, cache-identity mismatch,
+ *        partial streams and duplicate ownership all give UNKNOWN here.
+ *  - Arithmetic (the paper fixes none: it never defines a digest or hash; this
+ *    checker's definitions, recorded with the rest of the design):
+ *      * mix64 / splitmix64: the SplitMix64 generator of Steele, Lea and Flood
+ *        (OOPSLA 2014), written here from its published description;
+ *      * KV word keys k_i = splitmix64(S, i) | 1 and the block digest
+ *        D = sum_i w_i * k_i mod 2^64 over little-endian 64-bit words of the
+ *        block's canonical bytes;
+ *      * token keys t_m = splitmix64(~S, m) | 1, the per-block token
+ *        multilinear M_j = sum_m tok * t_m, and the chain
+ *        h_{-1} = S, h_j = splitmix64(h_{j-1} xor M_j).
+ *
+ * Parity pins (checked by the CPU tests): the published SplitMix64 outputs
+ * for seed 0; D(0) = 0, D(e_i) = k_i, additivity, the exact single-bit-flip
+ * delta +-2^beta * k_i; exhaustive single flips on a small block; shared
+ * token prefixes give equal chain hashes; outcome enumeration over every
+ * ok/failed/missing assignment of short claims; memcmp brute force of the
+ * failing set on the tiny pool; the paper's event-order templates.
+ */
+
+#include <cstdint>
+#include <cstring>
+#include <unordered_map>
+#include <vector>
+
+namespace {
+
+/* ---------------------------------------------------------------- hashing */
+
+const uint64_t kGamma = 0x9E3779B97F4A7C15ull; /* SplitMix64 increment */
+
+/* SplitMix64 output (finaliser) function. */
+uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+/* One SplitMix64 step from state x: advance by gamma, then finalise. */
+uint64_t splitmix64(uint64_t x) { return mix64(x + kGamma); }
+
+/* The (i+1)-th output of the SplitMix64 stream whose state starts at s. */
+uint64_t splitmix64_at(uint64_t s, uint64_t i) { return mix64(s + (i + 1) * kGamma); }
+
+uint64_t kv_key(uint64_t seed, uint64_t i) { return splitmix64_at(seed, i) | 1ull; }
+
+uint64_t token_key(uint64_t seed, uint64_t m) { return splitmix64_at(~seed, m) | 1ull; }
+
+/* Little-endian 64-bit word from 8 bytes, one byte at a time. */
+uint64_t le_word(const uint8_t* p) {
+  uint64_t w = 0;
+  for (int k = 0; k < 8; ++k) w |= (uint64_t)p[k] << (8 * k);
+  return w;
+}
+
+/* Block digest over canonical bytes: sum over words of w_i * k_i mod 2^64. */
+uint64_t block_digest(const uint8_t* canon, uint64_t nbytes, uint64_t seed) {
+  uint64_t d = 0;
+  for (uint64_t i = 0; i < nbytes / 8; ++i) d += le_word(canon + 8 * i) * kv_key(seed, i);
+  return d;
+}
+
+/* Token multilinear of one token block: sum over present tokens of tok * t_m. */
+uint64_t token_multilinear(const uint32_t* tok, uint64_t n, uint64_t seed) {
+  uint64_t m_sum = 0;
+  for (uint64_t m = 0; m < n; ++m) m_sum += (uint64_t)tok[m] * token_key(seed, m);
+  return m_sum;
+}
+
+uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+
+/* Chain over a claim's tokens: h_{-1} = S, h_j = splitmix64(h_{j-1} ^ M_j).
+ * Writes h_0 .. h_{nt-1} (nt = ceil(ntok / bs)) and returns h_{nt-1}, or S
+ * when there are no tokens. */
+uint64_t chain(const uint32_t* tok, uint64_t ntok, uint32_t bs, uint64_t seed,
+               std::vector<uint64_t>* h_out) {
+  uint64_t h = seed;
+  uint64_t nt = ceil_div(ntok, bs);
+  if (h_out) h_out->assign(nt, 0);
+  for (uint64_t j = 0; j < nt; ++j) {
+    uint64_t first = j * bs;
+    uint64_t count = ntok - first < bs ? ntok - first : bs;
+    uint64_t m_sum = token_multilinear(tok + first, count, seed);
+    h = splitmix64(h ^ m_sum);
+    if (h_out) (*h_out)[j] = h;
+  }
+  return h;
+}
+
+/* ------------------------------------------------------------ vocabulary */
+
+const uint32_t kNone = 0xFFFFFFFFu;
+const uint64_t kReservedId = 0xFFFFFFFFFFFFFFFFull;
+
+enum { ST_ACCEPTED = 1, ST_OFFLOADED = 2, ST_RESTORE_REQUIRED = 4 };
+
+enum {
+  OUT_UNKNOWN = 0,
+  OUT_MATERIALIZED = 1,
+  OUT_RESTORE_FAILED_FAIL_CLOSED = 2,
+};
+
+enum {
+  EV_ACCEPTED = 1,
+  EV_OFFLOADED = 2,
+  EV_RESTORE_REQUIRED = 3,
+  EV_RESTORED = 4,
+  EV_RESTORATION_FAILED = 5,
+  EV_ACTIVE_REQUEST_REFUSED = 6,
+  EV_OUTCOME_UNKNOWN = 7,
+};
+
+enum {
+  R_NOT_ACCEPTED = 0x001,
+  R_NOT_OFFLOADED = 0x002,
+  R_NO_RESTORE = 0x004,
+  R_TOKEN_MISMATCH = 0x008,
+  R_FOOTPRINT_MISMATCH = 0x010,
+  R_MISSING_ENTRY = 0x020,
+  R_NO_OFFLOAD_RECORD = 0x040,
+  R_SHAPE_MISMATCH = 0x080,
+  R_EMPTY = 0x100,
+  R_MALFORMED = 0x200,
+  R_LOAD_FAILED = 0x400,
+  R_DIGEST_MISMATCH = 0x800,
+};
+
+enum { ORC_OK = 0, ORC_EINVAL = -1, ORC_EDUP = -5 };
+
+}  // namespace
+
+extern "C" {
+
+/* Records handed back to the tests (the oracle's own layout). */
+typedef struct orc_outcome {
+  uint64_t claim_id;
+  uint32_t code;
+  uint32_t first_failing_block;
+  uint32_t phys_block;
+  uint32_t num_blocks;
+  uint32_t reasons;
+  uint32_t pad;
+  uint64_t expected_digest;
+  uint64_t observed_digest;
+  uint64_t chain_hash;
+  uint64_t chain_hash_at_fail;
+} orc_outcome;
+
+typedef struct orc_event {
+  uint64_t seq;
+  uint64_t claim_id;
+  uint64_t aux;
+  uint32_t kind;
+  uint32_t block_index;
+  uint32_t phys_block;
+  uint32_t pad;
+} orc_event;
+
+}  // extern "C"
+
+namespace {
+
+struct Claim {
+  uint32_t state;
+  std::vector<uint32_t> footprint;
+  uint64_t n_tokens;
+  uint64_t chain_hash;
+};
+
+struct Pool {
+  uint32_t num_blocks;
+  uint32_t block_size;
+  uint64_t seed;
+  std::vector<uint64_t> d_off, d_res;
+  std::vector<uint8_t> valid_off, load_failed;
+  std::unordered_map<uint64_t, Claim> registry;
+  std::vector<orc_event> log;
+  uint64_t next_seq;
+};
+
+/* A read-only view of one claim batch (compressed rows). */
+struct Batch {
+  uint32_t num_claims;
+  uint64_t num_refs;
+  uint64_t num_tokens;
+  const uint64_t* ids;
+  const uint32_t* blk_off;
+  const uint32_t* blk_ids;
+  const uint64_t* tok_off;
+  const uint32_t* tokens;
+};
+
+/* A claim row is malformed when its offsets run backwards or past the end of
+ * the arrays, or when it uses the reserved id.  Malformed rows are never
+ * accepted and check as UNKNOWN. */
+bool malformed(const Batch& bt, uint32_t c) {
+  if (bt.ids[c] == kReservedId) return true;
+  if (bt.blk_off[c] > bt.blk_off[c + 1] || bt.blk_off[c + 1] > bt.num_refs) return true;
+  if (bt.tok_off[c] > bt.tok_off[c + 1] || bt.tok_off[c + 1] > bt.num_tokens) return true;
+  return false;
+}
+
+void append_event(Pool* p, uint64_t claim_id, uint32_t kind, uint32_t j, uint32_t phys,
+                  uint64_t aux) {
+  orc_event e;
+  e.seq = p->next_seq++;
+  e.claim_id = claim_id;
+  e.aux = aux;
+  e.kind = kind;
+  e.block_index = j;
+  e.phys_block = phys;
+  e.pad = 0;
+  p->log.push_back(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+/* -------------------------------------------------------- pure functions */
+
+uint64_t orc_mix64(uint64_t z) { return mix64(z); }
+uint64_t orc_splitmix64(uint64_t x) { return splitmix64(x); }
+uint64_t orc_splitmix64_at(uint64_t s, uint64_t i) { return splitmix64_at(s, i); }
+uint64_t orc_kv_key(uint64_t seed, uint64_t i) { return kv_key(seed, i); }
+uint64_t orc_token_key(uint64_t seed, uint64_t m) { return token_key(seed, m); }
+
+uint64_t orc_block_digest(const uint8_t* canon, uint64_t nbytes, uint64_t seed) {
+  return block_digest(canon, nbytes, seed);
+}
+
+uint64_t orc_token_multilinear(const uint32_t* tok, uint64_t n, uint64_t seed) {
+  return token_multilinear(tok, n, seed);
+}
+
+/* Chain hashes h_0 .. h_{nt-1} of one claim's tokens; returns h_{nt-1} (S if
+ * there are no tokens).  h_out may be NULL. */
+uint64_t orc_chain(const uint32_t* tok, uint64_t ntok, uint32_t bs, uint64_t seed,
+                   uint64_t* h_out) {
+  std::vector<uint64_t> h;
+  uint64_t last = chain(tok, ntok, bs, seed, &h);
+  if (h_out)
+    for (uint64_t j = 0; j < h.size(); ++j) h_out[j] = h[j];
+  return last;
+}
+
+/* Canonical bytes of block b: the concatenation over planes p = 0..P-1 of
+ * the chunk of plane p, where the pool is laid out [plane][block][chunk]. */
+int orc_canonical_block(const uint8_t* pool, uint32_t planes, uint32_t num_blocks,
+                        uint64_t chunk_bytes, uint32_t b, uint8_t* out) {
+  if (b >= num_blocks) return ORC_EINVAL;
+  for (uint32_t p = 0; p < planes; ++p) {
+    const uint8_t* src = pool + ((uint64_t)p * num_blocks + b) * chunk_bytes;
+    for (uint64_t q = 0; q < chunk_bytes; ++q) out[(uint64_t)p * chunk_bytes + q] = src[q];
+  }
+  return ORC_OK;
+}
+
+/* Flip canonical bit `bit` of block b in place (bit 0 = least significant
+ * bit of canonical byte 0). */
+int orc_apply_flip(uint8_t* pool, uint32_t planes, uint32_t num_blocks, uint64_t chunk_bytes,
+                   uint32_t b, uint64_t bit) {
+  if (b >= num_blocks || bit >= 8 * chunk_bytes * planes) return ORC_EINVAL;
+  uint64_t byte = bit / 8;
+  uint64_t p = byte / chunk_bytes;
+  uint64_t q = byte % chunk_bytes;
+  pool[(p * num_blocks + b) * chunk_bytes + q] ^= (uint8_t)(1u << (bit % 8));
+  return ORC_OK;
+}
+
+/* -------------------------------------------------------------- lifecycle */
+
+void* orc_pool_new(uint32_t num_blocks, uint32_t block_size, uint64_t seed) {
+  if (num_blocks == 0 || block_size == 0) return nullptr;
+  Pool* p = new Pool();
+  p->num_blocks = num_blocks;
+  p->block_size = block_size;
+  p->seed = seed;
+  p->d_off.assign(num_blocks, 0);
+  p->d_res.assign(num_blocks, 0);
+  p->valid_off.assign(num_blocks, 0);
+  p->load_failed.assign(num_blocks, 0);
+  p->next_seq = 0;
+  return p;
+}
+
+void orc_pool_free(void* handle) { delete static_cast<Pool*>(handle); }
+
+/* Accept and offload a batch.  digest_now[b] is the digest of block b's
+ * current bytes (only entries referenced by the batch are read).
+ *
+ * The whole batch is refused (ORC_EDUP, nothing changes, no event) if a
+ * non-reserved id occurs twice in it or is already registered.  Otherwise,
+ * in batch order, each well-formed claim is registered (ACCEPTED), every
+ * in-range block it references gets an offload record, and a claim whose
+ * footprint is non-empty, fully present and consistent with its token count
+ * is marked OFFLOADED. */
+int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num_tokens,
+                const uint64_t* ids, const uint32_t* blk_off, const uint32_t* blk_ids,
+                const uint64_t* tok_off, const uint32_t* tokens, const uint64_t* digest_now) {
+  Pool* p = static_cast<Pool*>(handle);
+  Batch bt = {num_claims, num_refs, num_tokens, ids, blk_off, blk_ids, tok_off, tokens};
+
+  /* duplicate ownership refuses acceptance of the whole batch */
+  std::unordered_map<uint64_t, int> seen;
+  for (uint32_t c = 0; c < num_claims; ++c) {
+    if (ids[c] == kReservedId) continue;
+    if (p->registry.count(ids[c]) || seen.count(ids[c])) return ORC_EDUP;
+    seen[ids[c]] = 1;
+  }
+
+  for (uint32_t c = 0; c < num_claims; ++c) {
+    if (malformed(bt, c)) continue;
+    uint32_t n = blk_off[c + 1] - blk_off[c];
+    const uint32_t* fp = blk_ids + blk_off[c];
+    uint64_t ntok = tok_off[c + 1] - tok_off[c];
+
+    Claim cl;
+    cl.state = ST_ACCEPTED;
+    cl.footprint.assign(fp, fp + n);
+    cl.n_tokens = ntok;
+    cl.chain_hash = chain(tokens + tok_off[c], ntok, p->block_size, p->seed, nullptr);
+    p->registry[ids[c]] = cl;
+    append_event(p, ids[c], EV_ACCEPTED, kNone, kNone, cl.chain_hash);
+
+    bool all_present = n > 0;
+    for (uint32_t j = 0; j < n; ++j) {
+      uint32_t b = fp[j];
+      if (b >= p->num_blocks) {
+        all_present = false;
+        continue;
+      }
+      p->d_off[b] = digest_now[b];
+      p->valid_off[b] = 1;
+      p->load_failed[b] = 0;
+    }
+    if (all_present && n == ceil_div(ntok, p->block_size)) {
+      p->registry[ids[c]].state |= ST_OFFLOADED;
+      append_event(p, ids[c], EV_OFFLOADED, kNone, kNone, n);
+    }
+  }
+  return ORC_OK;
+}
+
+/* Restore: mark the listed blocks as reported load failures, then, in batch
+ * order, move every well-formed, registered and offloaded claim to
+ * RESTORE_REQUIRED.  (Bit flips act on bytes, see orc_apply_flip.) */
+int orc_restore(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num_tokens,
+                const uint64_t* ids, const uint32_t* blk_off, const uint32_t* blk_ids,
+                const uint64_t* tok_off, const uint32_t* tokens, uint32_t num_failed,
+                const uint32_t* failed_blocks) {
+  Pool* p = static_cast<Pool*>(handle);
+  Batch bt = {num_claims, num_refs, num_tokens, ids, blk_off, blk_ids, tok_off, tokens};
+  for (uint32_t f = 0; f < num_failed; ++f)
+    if (failed_blocks[f] >= p->num_blocks) return ORC_EINVAL;
+  for (uint32_t f = 0; f < num_failed; ++f) p->load_failed[failed_blocks[f]] = 1;
+
+  for (uint32_t c = 0; c < num_claims; ++c) {
+    if (malformed(bt, c)) continue;
+    auto it = p->registry.find(ids[c]);
+    if (it == p->registry.end() || !(it->second.state & ST_OFFLOADED)) continue;
+    it->second.state |= ST_RESTORE_REQUIRED;
+    append_event(p, ids[c], EV_RESTORE_REQUIRED, kNone, kNone, it->second.footprint.size());
+  }
+  return ORC_OK;
+}
+
+/* Check: record restored digests, then decide each claim's outcome.
+ *
+ * Every failure or ambiguity is a key (class << 32 | position); class 0 is
+ * an ambiguity (no claim outcome), class 1 a restoration failure, and a
+ * claim-level ambiguity sits at position NONE.  The smallest key decides:
+ * none -> MATERIALIZED, class 0 -> UNKNOWN, class 1 ->
+ * RESTORE_FAILED_FAIL_CLOSED.  Events are appended in batch order. */
+int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num_tokens,
+              const uint64_t* ids, const uint32_t* blk_off, const uint32_t* blk_ids,
+              const uint64_t* tok_off, const uint32_t* tokens, const uint64_t* digest_now,
+              orc_outcome* out) {
+  Pool* p = static_cast<Pool*>(handle);
+  Batch bt = {num_claims, num_refs, num_tokens, ids, blk_off, blk_ids, tok_off, tokens};
+
+  /* restored digests of every block the well-formed claims reference */
+  for (uint32_t c = 0; c < num_claims; ++c) {
+    if (malformed(bt, c)) continue;
+    for (uint32_t j = blk_off[c]; j < blk_off[c + 1]; ++j) {
+      uint32_t b = blk_ids[j];
+      if (b < p->num_blocks && p->valid_off[b]) p->d_res[b] = digest_now[b];
+    }
+  }
+
+  for (uint32_t c = 0; c < num_claims; ++c) {
+    const uint64_t none_key = ((uint64_t)0 << 32) | kNone;
+    uint64_t best = ~0ull; /* no key yet */
+    uint32_t reasons = 0;
+    uint32_t n = 0;
+    uint64_t ntok = 0;
+    const uint32_t* fp = nullptr;
+    const uint32_t* tok = nullptr;
+
+    if (malformed(bt, c)) {
+      reasons |= R_MALFORMED;
+      if (none_key < best) best = none_key;
+    } else {
+      n = blk_off[c + 1] - blk_off[c];
+      fp = blk_ids + blk_off[c];
+      ntok = tok_off[c + 1] - tok_off[c];
+      tok = tokens + tok_off[c];
+    }
+
+    std::vector<uint64_t> h;
+    uint64_t chain_hash = chain(tok, ntok, p->block_size, p->seed, &h);
+    uint64_t nt = h.size();
+
+    if (!(reasons & R_MALFORMED)) {
+      auto it = p->registry.find(ids[c]);
+      if (it == p->registry.end()) {
+        reasons |= R_NOT_ACCEPTED;
+        if (none_key < best) best = none_key;
+      } else {
+        const Claim& cl = it->second;
+        if (!(cl.state & ST_OFFLOADED)) {
+          reasons |= R_NOT_OFFLOADED;
+          if (none_key < best) best = none_key;
+        }
+        if (!(cl.state & ST_RESTORE_REQUIRED)) {
+          reasons |= R_NO_RESTORE;
+          if (none_key < best) best = none_key;
+        }
+        if (cl.n_tokens != ntok || cl.chain_hash != chain_hash) {
+          reasons |= R_TOKEN_MISMATCH;
+          if (none_key < best) best = none_key;
+        }
+        uint32_t na = (uint32_t)cl.footprint.size();
+        uint32_t common = n < na ? n : na;
+        for (uint32_t j = 0; j < common; ++j) {
+          if (fp[j] != cl.footprint[j]) {
+            reasons |= R_FOOTPRINT_MISMATCH;
+            uint64_t k = ((uint64_t)0 << 32) | j;
+            if (k < best) best = k;
+          }
+        }
+        if (n != na) {
+          reasons |= R_FOOTPRINT_MISMATCH;
+          uint64_t k = ((uint64_t)0 << 32) | common;
+          if (k < best) best = k;
+        }
+      }
+      if (n == 0) {
+        reasons |= R_EMPTY;
+        if (none_key < best) best = none_key;
+      }
+      if (n != nt) {
+        reasons |= R_SHAPE_MISMATCH;
+        uint64_t k = ((uint64_t)0 << 32) | (uint32_t)(n < nt ? n : nt);
+        if (k < best) best = k;
+      }
+      for (uint32_t j = 0; j < n; ++j) {
+        uint32_t b = fp[j];
+        if (b >= p->num_blocks) {
+          reasons |= R_MISSING_ENTRY;
+          uint64_t k = ((uint64_t)0 << 32) | j;
+          if (k < best) best = k;
+        } else if (!p->valid_off[b]) {
+          reasons |= R_NO_OFFLOAD_RECORD;
+          uint64_t k = ((uint64_t)0 << 32) | j;
+          if (k < best) best = k;
+        } else {
+          bool lf = p->load_failed[b] != 0;
+          bool mm = p->d_res[b] != p->d_off[b];
+          if (lf) reasons |= R_LOAD_FAILED;
+          if (mm) reasons |= R_DIGEST_MISMATCH;
+          if (lf || mm) {
+            uint64_t k = ((uint64_t)1 << 32) | j;
+            if (k < best) best = k;
+          }
+        }
+      }
+    }
+
+    orc_outcome o;
+    std::memset(&o, 0, sizeof(o));
+    o.claim_id = ids[c];
+    o.num_blocks = n;
+    o.reasons = reasons;
+    o.chain_hash = chain_hash;
+    if (best == ~0ull) {
+      o.code = OUT_MATERIALIZED;
+      o.first_failing_block = kNone;
+      o.phys_block = kNone;
+    } else {
+      uint32_t cls = (uint32_t)(best >> 32);
+      uint32_t j = (uint32_t)(best & 0xFFFFFFFFu);
+      o.code = cls == 0 ? OUT_UNKNOWN : OUT_RESTORE_FAILED_FAIL_CLOSED;
+      o.first_failing_block = j;
+      o.phys_block = j < n ? fp[j] : kNone;
+      if (cls == 1) {
+        o.expected_digest = p->d_off[fp[j]];
+        o.observed_digest = p->d_res[fp[j]];
+      }
+      if (j != kNone && j < nt) o.chain_hash_at_fail = h[j];
+    }
+    out[c] = o;
+
+    if (o.code == OUT_MATERIALIZED) {
+      append_event(p, o.claim_id, EV_RESTORED, kNone, kNone, o.chain_hash);
+    } else if (o.code == OUT_RESTORE_FAILED_FAIL_CLOSED) {
+      append_event(p, o.claim_id, EV_RESTORATION_FAILED, o.first_failing_block, o.phys_block,
+                   o.observed_digest);
+      append_event(p, o.claim_id, EV_ACTIVE_REQUEST_REFUSED, o.first_failing_block,
+                   o.phys_block, o.claim_id);
+    } else {
+      append_event(p, o.claim_id, EV_OUTCOME_UNKNOWN, o.first_failing_block, o.phys_block,
+                   o.reasons);
+    }
+  }
+  return ORC_OK;
+}
+
+uint64_t orc_num_events(void* handle) { return static_cast<Pool*>(handle)->log.size(); }
+
+void orc_events(void* handle, orc_event* out) {
+  Pool* p = static_cast<Pool*>(handle);
+  for (size_t i = 0; i < p->log.size(); ++i) out[i] = p->log[i];
+}
+
+/* Drop the events read so far (sequence numbers keep counting). */
+void orc_events_clear(void* handle) { static_cast<Pool*>(handle)->log.clear(); }
+
+void orc_block_state(void* handle, uint64_t* d_off, uint64_t* d_res, uint8_t* valid_off,
+                     uint8_t* load_failed) {
+  Pool* p = static_cast<Pool*>(handle);
+  for (uint32_t b = 0; b < p->num_blocks; ++b) {
+    if (d_off) d_off[b] = p->d_off[b];
+    if (d_res) d_res[b] = p->d_res[b];
+    if (valid_off) valid_off[b] = p->valid_off[b];
+    if (load_failed) load_failed[b] = p->load_failed[b];
+  }
+}
+
+/* Registry state of one claim id: returns the state bits, or 0 if the id is
+ * not registered. */
+uint32_t orc_claim_state(void* handle, uint64_t id) {
+  Pool* p = static_cast<Pool*>(handle);
+  auto it = p->registry.find(id);
+  return it == p->registry.end() ? 0 : it->second.state;
+}
+
+}  // extern "C"

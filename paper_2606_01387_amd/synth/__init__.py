@@ -1,0 +1,9 @@
+"""Seeded synthetic inputs: workloads, claim batches, faults and pool content.
+
+This subpackage only builds inputs.  It holds none of the checker's
+arithmetic and is shared by the product's tests, the oracle side and the
+benchmark.
+"""
+
+from .claims import MISSING, Batch, FaultSpec, from_claims, make_batch, make_faults  # noqa: F401
+from .workloads import FULL, LLAMA3_8B, LLAMA3_70B, MLA_FP8, STRESS, TINY, Geometry, Workload, scaled  # noqa: F401

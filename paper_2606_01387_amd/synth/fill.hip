@@ -1,0 +1,107 @@
+// fill.hip -- seeded synthetic KV-pool content, generated on the GPU.
+//
+// Part of the input generator (not the checker): it writes the same bytes as
+// content_host.c, from the same definition (Philox4x32-10 counters per
+// 16-byte unit; bf16 Irwin-Hall values or raw bytes), directly into a pool
+// that is too large to build on the host.  A GPU test compares the two.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace {
+
+constexpr uint32_t kTagBf16 = 0x6B760000u;
+constexpr uint32_t kTagBytes = 0x6B760001u;
+
+__device__ inline void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t lo0 = 0xD2511F53u * c[0];
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c[0]);
+    const uint32_t lo1 = 0xCD9E8D57u * c[2];
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c[2]);
+    const uint32_t n0 = hi1 ^ c[1] ^ k0;
+    const uint32_t n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+  }
+}
+
+__device__ inline uint32_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__global__ void __launch_bounds__(256) fill_kernel(uint4* __restrict__ pool, uint64_t units,
+                                                   uint32_t num_blocks, uint32_t vecs_per_chunk,
+                                                   uint32_t k0, uint32_t k1, int raw_bytes) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t u = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; u < units; u += stride) {
+    const uint32_t v = (uint32_t)(u % vecs_per_chunk);
+    const uint64_t pb = u / vecs_per_chunk;
+    const uint32_t b = (uint32_t)(pb % num_blocks);
+    const uint32_t p = (uint32_t)(pb / num_blocks);
+    uint4 out;
+    if (raw_bytes) {
+      uint32_t c[4] = {v, b, p, kTagBytes};
+      philox4x32_10(c, k0, k1);
+      out = make_uint4(c[0], c[1], c[2], c[3]);
+    } else {
+      uint32_t w[12];
+#pragma unroll
+      for (uint32_t r = 0; r < 3; ++r) {
+        uint32_t c[4] = {3u * v + r, b, p, kTagBf16};
+        philox4x32_10(c, k0, k1);
+        w[4 * r + 0] = c[0];
+        w[4 * r + 1] = c[1];
+        w[4 * r + 2] = c[2];
+        w[4 * r + 3] = c[3];
+      }
+      uint32_t h[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        uint32_t s = 0;
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+          const int idx = 3 * t + k;
+          s += (w[idx / 2] >> (16 * (idx % 2))) & 0xFFFFu;
+        }
+        const int32_t n = 2 * (int32_t)s - 196605;
+        h[t] = bf16_rne((float)n * (1.0f / 65536.0f));
+      }
+      out = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                       h[6] | (h[7] << 16));
+    }
+    pool[u] = out;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+// Fill a [plane][block][chunk] pool on `stream` (a hipStream_t, may be null).
+// Returns 0, -1 for bad geometry or a too-small buffer, -3 for a HIP error.
+int synth_fill_pool(void* pool, uint64_t pool_bytes, uint64_t seed, int raw_bytes,
+                    uint32_t planes, uint32_t num_blocks, uint64_t chunk_bytes, void* stream) {
+  if (!pool || planes == 0 || num_blocks == 0 || chunk_bytes == 0 || chunk_bytes % 16) return -1;
+  if (chunk_bytes / 16 > 0xFFFFFFFFull / 3) return -1;
+  const uint64_t total = (uint64_t)planes * num_blocks * chunk_bytes;
+  if (pool_bytes < total || ((uintptr_t)pool & 15)) return -1;
+  const uint64_t units = total / 16;
+  uint64_t blocks = (units + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                     (uint4*)pool, units, num_blocks, (uint32_t)(chunk_bytes / 16),
+                     (uint32_t)seed, (uint32_t)(seed >> 32), raw_bytes);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+}  // extern "C"

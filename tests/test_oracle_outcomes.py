@@ -1,0 +1,373 @@
+"""Pins for the oracle's claim lifecycle: outcomes, attribution, event order.
+
+The expected results come from the paper's semantics (section 1 running
+example, section 7 witness paths and controls, Table 2 ambiguity rule,
+Tables 8 and 9 false-positive controls), stated independently of the
+oracle's min-reduction: sequential scans, enumeration, memcmp brute force.
+"""
+
+import itertools
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2606_01387_amd.synth import MISSING, TINY, FaultSpec, from_claims, make_batch, make_faults
+from tests.conftest import golden_lines
+from tests.helpers import NONE32, apply_flips, digests, expected_by_scan, host_pool, modeled_digests, oracle_lifecycle
+
+KIND = {
+    "ACCEPTED": O.EV_ACCEPTED,
+    "OFFLOADED": O.EV_OFFLOADED,
+    "RESTORE_REQUIRED": O.EV_RESTORE_REQUIRED,
+    "RESTORED": O.EV_RESTORED,
+    "RESTORATION_FAILED": O.EV_RESTORATION_FAILED,
+    "ACTIVE_REQUEST_REFUSED": O.EV_ACTIVE_REQUEST_REFUSED,
+    "OUTCOME_UNKNOWN": O.EV_OUTCOME_UNKNOWN,
+}
+PATHS = {row[0]: [KIND[k] for k in row[1:]] for row in golden_lines("paper_event_paths.txt")
+         if row[0] in ("A", "B", "C_target", "C_nontarget")}
+
+BS = TINY.geometry.block_size
+NB = TINY.geometry.num_blocks
+RNG = np.random.default_rng(2024)
+
+
+def toks(nblocks, tail=BS):
+    return RNG.integers(0, 32000, size=(nblocks - 1) * BS + tail if nblocks else 0, dtype=np.uint32)
+
+
+def kinds_for(events, cid):
+    return [int(e["kind"]) for e in events if int(e["claim_id"]) == cid]
+
+
+@pytest.fixture(scope="module")
+def pool():
+    return host_pool(TINY)
+
+
+@pytest.fixture(scope="module")
+def d0(pool):
+    return digests(pool, TINY)
+
+
+def fresh():
+    return O.OraclePool(NB, BS, TINY.seed)
+
+
+# ------------------------------------------------------- outcome enumeration
+
+
+def test_outcome_enumeration_matches_sequential_scan():
+    """Every assignment of ok / failed / missing to the blocks of a claim of
+    n <= 7 blocks: missing (no outcome) dominates failure, and the smallest
+    position of the dominating kind is reported."""
+    nb = 16
+    base = np.arange(nb, dtype=np.uint64) * np.uint64(1000003) + np.uint64(17)
+    for n in range(0, 8):
+        for state in itertools.product("ofm", repeat=n):
+            blocks = [j if s != "m" else MISSING for j, s in enumerate(state)]
+            tk = np.arange(n * 4, dtype=np.uint32)  # block size 4 -> n token blocks
+            b = from_claims([(42, blocks, tk)])
+            op = O.OraclePool(nb, 4, 77)
+            assert op.offload(b, base) == O.OK
+            assert op.restore(b) == O.OK
+            after = base.copy()
+            for j, s in enumerate(state):
+                if s == "f":
+                    after[j] ^= np.uint64(1)
+            out = op.check(b, after)[0]
+            if n == 0:
+                assert (out["code"], out["first_failing_block"]) == (O.UNKNOWN, NONE32)
+                assert out["reasons"] & O.R_EMPTY
+                continue
+            if "m" in state:
+                want = (O.UNKNOWN, state.index("m"))
+            elif "f" in state:
+                want = (O.RESTORE_FAILED_FAIL_CLOSED, state.index("f"))
+            else:
+                want = (O.MATERIALIZED, NONE32)
+            assert (int(out["code"]), int(out["first_failing_block"])) == want, state
+            assert bool(out["reasons"] & O.R_MISSING_ENTRY) == ("m" in state)
+            assert bool(out["reasons"] & O.R_DIGEST_MISMATCH) == ("f" in state)
+
+
+# ------------------------------------------------------ paper witness paths
+
+
+def test_path_a_success_order(pool, d0):
+    cid = 0xC1A1
+    b = from_claims([(cid, [3, 9, 27], toks(3, 5))])
+    op = fresh()
+    assert op.offload(b, d0) == O.OK
+    assert op.restore(b) == O.OK
+    out = op.check(b, d0)[0]
+    ev = op.events()
+    assert kinds_for(ev, cid) == PATHS["A"]
+    assert out["code"] == O.MATERIALIZED and out["reasons"] == 0
+    assert out["first_failing_block"] == NONE32 and out["phys_block"] == NONE32
+    h = O.chain_hash(b.claim(0)[2], BS, TINY.seed)
+    assert out["chain_hash"] == h
+    assert ev[0]["aux"] == h and ev[-1]["aux"] == h  # accepted identity == restored identity
+    assert list(ev["seq"]) == list(range(len(ev)))
+
+
+def test_path_b_same_claim_reported_load_failure(pool, d0):
+    cid = 0xC1B2
+    b = from_claims([(cid, [5, 6, 7, 8], toks(4))])
+    op = fresh()
+    op.offload(b, d0)
+    op.restore(b, load_failed_blocks=[7])
+    out = op.check(b, d0)[0]
+    ev = op.events()
+    assert kinds_for(ev, cid) == PATHS["B"]
+    assert out["code"] == O.RESTORE_FAILED_FAIL_CLOSED
+    assert out["first_failing_block"] == 2 and out["phys_block"] == 7
+    assert out["reasons"] == O.R_LOAD_FAILED
+    assert out["expected_digest"] == out["observed_digest"] == d0[7]
+    refused = ev[ev["kind"] == O.EV_ACTIVE_REQUEST_REFUSED]
+    assert len(refused) == 1 and refused[0]["aux"] == cid  # blocking_claim_ids = [C]
+    failed = ev[ev["kind"] == O.EV_RESTORATION_FAILED]
+    assert failed[0]["seq"] < refused[0]["seq"]
+    h = O.chain(b.claim(0)[2], BS, TINY.seed)
+    assert out["chain_hash_at_fail"] == h[2]
+
+
+def test_path_b_silent_corruption(pool, d0):
+    cid = 0xC1B3
+    b = from_claims([(cid, [10, 11, 12], toks(3))])
+    f = FaultSpec(np.array([11], np.uint32), np.array([12345], np.uint64), np.zeros(0, np.uint32))
+    op, out, ev, _, d1 = oracle_lifecycle(TINY, b, f, pool)
+    assert kinds_for(ev, cid) == PATHS["B"]
+    o = out[0]
+    assert o["code"] == O.RESTORE_FAILED_FAIL_CLOSED and o["first_failing_block"] == 1
+    assert o["expected_digest"] == d0[11] and o["observed_digest"] == d1[11] != d0[11]
+    assert o["reasons"] == O.R_DIGEST_MISMATCH
+
+
+def test_path_c_target_only_attribution(pool):
+    target, nontarget = 0x7A, 0x7B
+    b = from_claims([(target, [1, 2, 3], toks(3)), (nontarget, [4, 5, 6], toks(3))])
+    f = FaultSpec(np.array([2], np.uint32), np.array([77], np.uint64), np.zeros(0, np.uint32))
+    op, out, ev, _, _ = oracle_lifecycle(TINY, b, f, pool)
+    assert kinds_for(ev, target) == PATHS["C_target"]
+    assert kinds_for(ev, nontarget) == PATHS["C_nontarget"]
+    refused = ev[ev["kind"] == O.EV_ACTIVE_REQUEST_REFUSED]
+    assert set(int(x) for x in refused["aux"]) == {target}
+    assert out["code"].tolist() == [O.RESTORE_FAILED_FAIL_CLOSED, O.MATERIALIZED]
+
+
+# ------------------------------------------- false-positive controls (Table 9)
+
+
+def test_unclaimed_failure_gives_no_claim_outcome(pool):
+    b = from_claims([(1, [0, 1], toks(2)), (2, [2, 3], toks(2))])
+    f = FaultSpec(np.array([40], np.uint32), np.array([5], np.uint64), np.array([41], np.uint32))
+    op, out, ev, _, _ = oracle_lifecycle(TINY, b, f, pool)
+    assert (out["code"] == O.MATERIALIZED).all()
+    assert not (ev["kind"] == O.EV_RESTORATION_FAILED).any()
+
+
+def test_fallback_recompute_does_not_restore_the_claim(pool, d0):
+    """A reported load failure stays a failure even if the bytes are later
+    rewritten correctly (fallback recompute is not restoration)."""
+    b = from_claims([(9, [20, 21], toks(2))])
+    op = fresh()
+    op.offload(b, d0)
+    op.restore(b, load_failed_blocks=[21])
+    out = op.check(b, d0)[0]  # bytes equal to the original
+    assert out["code"] == O.RESTORE_FAILED_FAIL_CLOSED and out["first_failing_block"] == 1
+    # only a fresh offload record clears it
+    op2 = fresh()
+    op2.offload(b, d0)
+    op2.restore(b, load_failed_blocks=[21])
+    b2 = from_claims([(10, [21], toks(1))])
+    op2.offload(b2, d0)
+    op2.restore(b2)
+    assert op2.check(b2, d0)[0]["code"] == O.MATERIALIZED
+
+
+def test_ordinary_offload_without_claim_is_not_an_outcome(d0):
+    """Claim Y was never accepted; its blocks were offloaded by claim X."""
+    tk = toks(2)
+    x = from_claims([(100, [30, 31], tk)])
+    y = from_claims([(200, [30, 31], tk)])
+    op = fresh()
+    op.offload(x, d0)
+    op.restore(x)
+    out = op.check(y, d0)[0]
+    assert out["code"] == O.UNKNOWN and out["first_failing_block"] == NONE32
+    assert out["reasons"] & O.R_NOT_ACCEPTED
+    assert kinds_for(op.events(), 200) == [O.EV_OUTCOME_UNKNOWN]
+
+
+def test_wrong_claim_failure_is_not_attributed(pool):
+    b = from_claims([(1, [12, 13], toks(2)), (2, [14, 15], toks(2))])
+    f = FaultSpec(np.zeros(0, np.uint32), np.zeros(0, np.uint64), np.array([15], np.uint32))
+    op, out, ev, _, _ = oracle_lifecycle(TINY, b, f, pool)
+    assert out["code"].tolist() == [O.MATERIALIZED, O.RESTORE_FAILED_FAIL_CLOSED]
+    assert kinds_for(ev, 1)[-1] == O.EV_RESTORED
+
+
+def test_reuse_without_restore_is_ambiguous(d0):
+    b = from_claims([(5, [1, 2], toks(2))])
+    op = fresh()
+    op.offload(b, d0)
+    out = op.check(b, d0)[0]
+    assert out["code"] == O.UNKNOWN and out["reasons"] == O.R_NO_RESTORE
+
+
+def test_cache_identity_mismatch_is_ambiguous(d0):
+    tk = toks(3)
+    b = from_claims([(5, [1, 2, 3], tk)])
+    op = fresh()
+    op.offload(b, d0)
+    op.restore(b)
+    tk2 = tk.copy()
+    tk2[20] += 1
+    out = op.check(from_claims([(5, [1, 2, 3], tk2)]), d0)[0]
+    assert out["code"] == O.UNKNOWN and out["reasons"] == O.R_TOKEN_MISMATCH
+    assert out["first_failing_block"] == NONE32
+    out = op.check(from_claims([(5, [1, 9, 3], tk)]), d0)[0]
+    assert out["code"] == O.UNKNOWN and out["first_failing_block"] == 1
+    # block 9 differs from the accepted footprint and has no offload record
+    assert out["reasons"] == O.R_FOOTPRINT_MISMATCH | O.R_NO_OFFLOAD_RECORD
+    out = op.check(from_claims([(5, [1, 2], tk[: 2 * BS])]), d0)[0]
+    assert out["code"] == O.UNKNOWN and out["first_failing_block"] == 2
+    assert out["reasons"] & O.R_FOOTPRINT_MISMATCH and out["reasons"] & O.R_TOKEN_MISMATCH
+
+
+def test_missing_entry_blocks_offload_and_outcome(d0):
+    b = from_claims([(6, [4, MISSING, 5], toks(3))])
+    op = fresh()
+    op.offload(b, d0)
+    op.restore(b)
+    out = op.check(b, d0)[0]
+    assert kinds_for(op.events(), 6) == [O.EV_ACCEPTED, O.EV_OUTCOME_UNKNOWN]
+    assert out["code"] == O.UNKNOWN and out["first_failing_block"] == 1
+    assert out["phys_block"] == MISSING
+    assert out["reasons"] & O.R_MISSING_ENTRY and out["reasons"] & O.R_NOT_OFFLOADED
+    assert op.claim_state(6) == O.ST_ACCEPTED
+
+
+def test_unknown_dominates_earlier_failure(pool):
+    b = from_claims([(8, [16, 17, 18, MISSING], toks(4))])
+    f = FaultSpec(np.array([16], np.uint32), np.array([3], np.uint64), np.zeros(0, np.uint32))
+    _, out, _, _, _ = oracle_lifecycle(TINY, b, f, pool)
+    assert out[0]["code"] == O.UNKNOWN and out[0]["first_failing_block"] == 3
+    assert out[0]["reasons"] & O.R_DIGEST_MISMATCH
+
+
+def test_shared_block_corruption_fails_every_referencing_claim(pool):
+    tk = toks(3)
+    b = from_claims([(1, [50, 51, 52], tk), (2, [50, 51, 60], np.concatenate([tk[: 2 * BS], toks(1)])),
+                     (3, [61, 62], toks(2))])
+    f = FaultSpec(np.array([51], np.uint32), np.array([999], np.uint64), np.zeros(0, np.uint32))
+    _, out, _, _, _ = oracle_lifecycle(TINY, b, f, pool)
+    assert out["code"].tolist() == [O.RESTORE_FAILED_FAIL_CLOSED, O.RESTORE_FAILED_FAIL_CLOSED,
+                                    O.MATERIALIZED]
+    assert out["first_failing_block"].tolist()[:2] == [1, 1]
+    assert out[0]["chain_hash_at_fail"] == out[1]["chain_hash_at_fail"]  # shared prefix identity
+
+
+def test_duplicate_ownership_refuses_acceptance(d0):
+    op = fresh()
+    dup = from_claims([(1, [1], toks(1)), (1, [2], toks(1))])
+    assert op.offload(dup, d0) == O.EDUP
+    assert len(op.events()) == 0 and op.claim_state(1) == 0
+    ok = from_claims([(1, [1], toks(1))])
+    assert op.offload(ok, d0) == O.OK
+    assert op.offload(from_claims([(2, [2], toks(1)), (1, [3], toks(1))]), d0) == O.EDUP
+    assert op.claim_state(2) == 0
+
+
+def test_malformed_rows_and_empty_claims(d0):
+    b = from_claims([(1, [1, 2], toks(2)), (2, [], toks(0)), (0xFFFFFFFFFFFFFFFF, [3], toks(1)),
+                     (4, [4, 5], toks(3))])
+    op = fresh()
+    assert op.offload(b, d0) == O.OK
+    op.restore(b)
+    out = op.check(b, d0)
+    assert out["code"].tolist() == [O.MATERIALIZED, O.UNKNOWN, O.UNKNOWN, O.UNKNOWN]
+    assert out[1]["reasons"] & O.R_EMPTY and out[1]["first_failing_block"] == NONE32
+    assert out[2]["reasons"] == O.R_MALFORMED and out[2]["num_blocks"] == 0
+    assert out[3]["reasons"] & O.R_SHAPE_MISMATCH and out[3]["first_failing_block"] == 2
+    assert op.claim_state(0xFFFFFFFFFFFFFFFF) == 0
+    # offsets that run backwards make a row malformed, never an error
+    bad = from_claims([(7, [1, 2], toks(2)), (8, [3], toks(1))])
+    bad.block_offsets[1] = 3  # offsets [0, 3, 2]: row 1 runs backwards
+    bad.block_offsets[2] = 2
+    op2 = fresh()
+    assert op2.offload(bad, d0) == O.OK
+    op2.restore(bad)
+    out = op2.check(bad, d0)
+    assert out[1]["reasons"] == O.R_MALFORMED
+
+
+def test_predicate_prefix_of_running_example(d0):
+    """The running example's predicate covers 448 tokens = 28 full blocks;
+    a failure in the 28th block fails the claim, and the chain hash before
+    it identifies the intact 27-block prefix."""
+    rows = {r[0]: int(r[1]) for r in golden_lines("paper_event_paths.txt") if r[0].startswith("PRED")}
+    nblk = rows["PREDICATE_TOKENS"] // rows["PREDICATE_BLOCK_SIZE"]
+    assert nblk == 28 and rows["PREDICATE_BLOCK_SIZE"] == BS
+    tk = toks(nblk)
+    b = from_claims([(0xC, list(range(nblk)), tk)])
+    op = fresh()
+    op.offload(b, d0)
+    op.restore(b, load_failed_blocks=[27])
+    out = op.check(b, d0)[0]
+    assert out["code"] == O.RESTORE_FAILED_FAIL_CLOSED and out["first_failing_block"] == 27
+    h = O.chain(tk, BS, TINY.seed)
+    assert out["chain_hash_at_fail"] == h[27] and out["chain_hash"] == h[27]
+    assert O.chain_hash(tk[: 27 * BS], BS, TINY.seed) == h[26]
+
+
+# --------------------------------------------------- tiny-pool brute force
+
+
+def test_tiny_workload_matches_memcmp_brute_force():
+    """The tiny workload end to end: the failing set is computed by comparing
+    restored and original bytes block by block, plus the reported failures,
+    with no digest involved; the digest-based outcomes must agree."""
+    w = TINY
+    b = make_batch(w)
+    f = make_faults(w, b)
+    f = FaultSpec(f.flip_blocks, f.flip_bits, np.array([int(b.block_ids[5])], np.uint32))
+    pool = host_pool(w)
+    op, out, ev, d0, d1 = oracle_lifecycle(w, b, f, pool)
+    restored = apply_flips(pool, w, f)
+    g = w.geometry
+    failing = set(int(x) for x in f.load_failed)
+    for blk in range(g.num_blocks):
+        a = O.canonical_block(pool, g.planes, g.num_blocks, g.chunk_bytes, blk)
+        r = O.canonical_block(restored, g.planes, g.num_blocks, g.chunk_bytes, blk)
+        if not np.array_equal(a, r):
+            failing.add(blk)
+    assert failing  # the workload does exercise failures
+    want = expected_by_scan(b, g.num_blocks, g.block_size, failing)
+    got = [(int(o["code"]), int(o["first_failing_block"])) for o in out]
+    assert got == want
+    # events: one terminal event per outcome, two for a failure, claim order
+    term = ev[ev["kind"] >= O.EV_RESTORED]
+    assert len(term) == b.num_claims + int((out["code"] == O.RESTORE_FAILED_FAIL_CLOSED).sum())
+    assert list(ev["seq"]) == list(range(len(ev)))
+
+
+def test_modeled_digests_reproduce_real_digest_outcomes():
+    """Large pools are checked with real digests only for blocks whose bytes
+    change (and a sample); every other block's before/after digests are
+    equal placeholders.  On the tiny workload this gives exactly the
+    outcomes and events of digesting every block."""
+    w = TINY
+    b = make_batch(w)
+    f = make_faults(w, b)
+    f = FaultSpec(f.flip_blocks, f.flip_bits, np.array([int(b.block_ids[7])], np.uint32))
+    _, out_real, ev_real, _, _ = oracle_lifecycle(w, b, f)
+    m0, m1 = modeled_digests(w, f, blocks_needed=[])
+    op = O.OraclePool(w.geometry.num_blocks, w.geometry.block_size, w.seed)
+    op.offload(b, m0)
+    op.restore(b, f.load_failed)
+    out_mod = op.check(b, m1)
+    assert np.array_equal(out_real, out_mod)
+    assert np.array_equal(ev_real, op.events())

@@ -1,0 +1,94 @@
+"""The seeded input generator: Philox known answers, content statistics and
+the structure of the generated claim batches."""
+
+import numpy as np
+import pytest
+
+from paper_2606_01387_amd.synth import FULL, MISSING, TINY, FaultSpec, content, make_batch, make_faults, scaled
+from tests.conftest import golden_lines
+
+
+def test_philox_known_answers():
+    for row in golden_lines("philox4x32_10_kat.txt"):
+        v = [int(x, 16) for x in row]
+        assert content.philox4x32_10(v[0:4], v[4:6]) == v[6:10]
+
+
+def test_bf16_content_is_standard_normal_like():
+    g = TINY.geometry
+    pool = content.pool_host(g, TINY.content_seed).view("<u2")
+    f = (pool.astype(np.uint32) << 16).view(np.float32)
+    assert abs(f.mean()) < 0.01 and abs(f.var() - 1.0) < 0.02
+    assert np.abs(f).max() <= 3.0
+
+
+def test_fp8_content_is_uniform_bytes():
+    g = scaled(FULL["mla-fp8"], 4, 4).geometry
+    pool = content.pool_host(g, 5)
+    hist = np.bincount(pool, minlength=256)
+    assert hist.min() > 0.8 * pool.size / 256 and hist.max() < 1.2 * pool.size / 256
+
+
+def test_canonical_block_matches_pool_layout():
+    g = TINY.geometry
+    pool = content.pool_host(g, TINY.content_seed)
+    for b in (0, 17, 63):
+        canon = content.block_canonical(g, TINY.content_seed, b)
+        for p in range(g.planes):
+            off = (p * g.num_blocks + b) * g.chunk_bytes
+            assert np.array_equal(canon[p * g.chunk_bytes:(p + 1) * g.chunk_bytes],
+                                  pool[off:off + g.chunk_bytes])
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama3-8b", "mla-fp8"])
+def test_batch_structure(name):
+    w = FULL[name]
+    b = make_batch(w)
+    g = w.geometry
+    assert np.array_equal(b.claim_ids, make_batch(w).claim_ids)  # deterministic
+    assert np.unique(b.claim_ids).size == b.num_claims
+    n = np.diff(b.block_offsets.astype(np.int64))
+    t = np.diff(b.token_offsets.astype(np.int64))
+    assert (n >= 1).all() and np.array_equal(n, (t + g.block_size - 1) // g.block_size)
+    ok = b.block_ids[b.block_ids != MISSING]
+    assert (ok < g.num_blocks).all()
+    # over-subscribed: every pool block is referenced
+    assert b.unique_blocks(g.num_blocks).size == g.num_blocks
+
+
+def test_prefix_sharing_copies_tokens_and_blocks():
+    w = FULL["llama3-8b"]
+    b = make_batch(w)
+    bs = w.geometry.block_size
+    seen = {}
+    shared = 0
+    for c in range(b.num_claims):
+        _, blks, toks = b.claim(c)
+        key = tuple(toks[:bs])
+        if key in seen:
+            _, blks0, toks0 = b.claim(seen[key])
+            k = 0
+            while (k + 1) * bs <= min(len(toks), len(toks0)) and np.array_equal(
+                    toks[k * bs:(k + 1) * bs], toks0[k * bs:(k + 1) * bs]):
+                k += 1
+            assert np.array_equal(blks[:k], blks0[:k])
+            shared += 1
+        else:
+            seen[key] = c
+    assert shared > 50
+
+
+def test_missing_entries_and_faults():
+    w = scaled(FULL["llama3-70b"], 2000, 400)
+    b = make_batch(w)
+    assert (b.block_ids == MISSING).sum() == round(0.02 * 400)
+    f = make_faults(w, b)
+    assert f.flip_blocks.size == round(0.001 * 2000)
+    assert np.unique(f.flip_blocks).size == f.flip_blocks.size
+    assert (f.flip_bits < 8 * w.geometry.block_bytes).all()
+
+
+def test_changed_blocks_cancels_repeated_flips():
+    f = FaultSpec(np.array([3, 3, 5, 7, 7], np.uint32), np.array([10, 10, 1, 2, 3], np.uint64),
+                  np.zeros(0, np.uint32))
+    assert f.changed_blocks().tolist() == [5, 7]
