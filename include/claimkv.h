@@ -1,0 +1,295 @@
+/*
+ * claimkv.h -- C ABI of the claim-scoped KV materialization checker for
+ * MI355X (gfx950).
+ *
+ * What it implements.  The paper ("Fail-Closed Lowering of Resident KV
+ * Claims onto LLM Serving Runtimes", arXiv 2606.01387) requires an
+ * offloadable claim to carry a stable identity, explicit acceptance before
+ * offload, a materialization predicate, restoration before reuse and a
+ * claim-scoped restoration-failure outcome, with ordered lifecycle events
+ * (section 1 running example; Table 1; section 3 offloadable bundle;
+ * section 7 event list and witness paths A, B, C).  Ambiguity must fail
+ * closed (Table 2, last rule).  This library supplies those obligations for
+ * paged KV blocks on the GPU:
+ *
+ *   claim_offload  accept a claim batch and record a 64-bit digest of every
+ *                  referenced physical block (optionally staging the bytes);
+ *   claim_restore  move accepted, offloaded claims to restore-required,
+ *                  optionally scattering staged bytes back, and apply the
+ *                  given faults (bit flips = silent corruption, reported load
+ *                  failures = the paper's controlled CPU->GPU load failure);
+ *   claim_check    re-digest the referenced blocks, compare, chain each
+ *                  claim's token prefix hash and reduce every claim to one
+ *                  outcome (MATERIALIZED, RESTORE_FAILED_FAIL_CLOSED or
+ *                  UNKNOWN) with the first failing block, appending the
+ *                  ordered events;
+ *   outcomes_read  copy the last check's outcomes and the new events to the
+ *                  host.
+ *
+ * The digest, keys and chain are this library's definitions (the paper
+ * leaves the byte-level check open; section 7 path B only requires
+ * affected-block evidence for the failure):
+ *   mix64(z)         SplitMix64 finaliser (Steele, Lea, Flood, OOPSLA 2014);
+ *   splitmix64(x)    = mix64(x + 0x9E3779B97F4A7C15);
+ *   splitmix64(s,i)  = mix64(s + (i+1) * 0x9E3779B97F4A7C15);
+ *   k_i = splitmix64(S, i) | 1,  D(b) = sum_i w_i * k_i mod 2^64 over the
+ *         little-endian 64-bit words w_i of block b's canonical bytes (the
+ *         concatenation of its chunks, plane 0 first);
+ *   t_m = splitmix64(~S, m) | 1, M_j = sum_m tok[j*bs+m] * t_m over the
+ *         tokens present in token block j;
+ *   h_{-1} = S,  h_j = splitmix64(h_{j-1} xor M_j).
+ * S is the pool seed: with the block geometry it is the pool's cache
+ * identity (Table 5, fixed cache identity).
+ *
+ * Conventions for every call:
+ *   - all functions return a status (CLAIM_OK or a negative CLAIM_E*) and
+ *     never abort;
+ *   - argument, layout or size errors return CLAIM_EINVAL before any work is
+ *     queued, and leave the pool unchanged;
+ *   - per-claim problems are never errors: they become UNKNOWN outcomes;
+ *   - work is queued on the pool's stream in call order; only
+ *     claim_offload (for its acceptance verdict and to settle its counts),
+ *     claim_restore (to read the host fault lists), outcomes_read,
+ *     claim_block_state_read, claim_timing_read and claim_pool_destroy wait
+ *     for the stream;
+ *   - device arrays passed in a claim_batch must stay valid and unchanged
+ *     until the queued work that reads them has completed;
+ *   - calls on one pool must not overlap from several host threads.
+ */
+#ifndef CLAIMKV_H
+#define CLAIMKV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------- status */
+#define CLAIM_OK 0
+#define CLAIM_EINVAL (-1) /* bad argument, layout or size */
+#define CLAIM_ENOMEM (-2) /* device allocation failed */
+#define CLAIM_EHIP (-3)   /* HIP runtime error */
+#define CLAIM_ENOSPC (-4) /* registry, footprint store, event log, staging or output too small */
+#define CLAIM_EDUP (-5)   /* duplicate claim id: acceptance refused */
+
+/* ----------------------------------------------------------- outcomes */
+#define CLAIM_UNKNOWN 0 /* no claim outcome (ambiguity fails closed); zero-initialised = fail closed */
+#define CLAIM_MATERIALIZED 1
+#define CLAIM_RESTORE_FAILED_FAIL_CLOSED 2
+
+/* ------------------------------------------------------- event kinds
+ * Equivalent names are acceptable to the paper (section 4; section 7).
+ * The section-7 events they stand for are given in brackets. */
+#define CLAIM_EV_ACCEPTED 1               /* claim metadata accepted [E0] */
+#define CLAIM_EV_OFFLOADED 2              /* whole footprint offloaded [E5] */
+#define CLAIM_EV_RESTORE_REQUIRED 3       /* reuse requires restoration [E6] */
+#define CLAIM_EV_RESTORED 4               /* restored and verified [E8] */
+#define CLAIM_EV_RESTORATION_FAILED 5     /* claim-scoped failure [E11, E12] */
+#define CLAIM_EV_ACTIVE_REQUEST_REFUSED 6 /* fail-closed refusal, blocking id [E13] */
+#define CLAIM_EV_OUTCOME_UNKNOWN 7        /* no outcome: ambiguity (Table 3 unknown) */
+
+/* ------------------------------------------- reason bits of an outcome */
+#define CLAIM_R_NOT_ACCEPTED 0x001      /* id not registered */
+#define CLAIM_R_NOT_OFFLOADED 0x002     /* registered, footprint not fully offloaded */
+#define CLAIM_R_NO_RESTORE 0x004        /* no restore ordered before this check */
+#define CLAIM_R_TOKEN_MISMATCH 0x008    /* token count or chain hash differs from acceptance */
+#define CLAIM_R_FOOTPRINT_MISMATCH 0x010 /* block list differs from acceptance */
+#define CLAIM_R_MISSING_ENTRY 0x020     /* entry is CLAIM_NONE or >= num_blocks */
+#define CLAIM_R_NO_OFFLOAD_RECORD 0x040 /* block has no offload digest */
+#define CLAIM_R_SHAPE_MISMATCH 0x080    /* blocks != ceil(tokens / block_size) */
+#define CLAIM_R_EMPTY 0x100             /* claim has no blocks */
+#define CLAIM_R_MALFORMED 0x200         /* offsets inconsistent, or reserved id */
+#define CLAIM_R_LOAD_FAILED 0x400       /* reported load failure */
+#define CLAIM_R_DIGEST_MISMATCH 0x800   /* restored digest != offload digest */
+
+#define CLAIM_NONE 0xFFFFFFFFu                   /* no position; missing block-table entry */
+#define CLAIM_RESERVED_ID 0xFFFFFFFFFFFFFFFFull /* never a valid claim id */
+
+#define CLAIM_POOL_TIMING 0x1u /* desc.flags: record per-stage hipEvents in claim_check */
+
+typedef struct claim_pool claim_pool;
+
+/* Pool description.  The KV memory is caller-owned device memory laid out
+ * [plane][block][chunk]: plane p = 2*layer + (0 for K, 1 for V) when
+ * planes_per_layer = 2, p = layer for an MLA latent (planes_per_layer = 1);
+ * a chunk is block_size x num_kv_heads x head_dim elements of elem_bytes
+ * bytes in [token][head][dim] order, and must be a multiple of 16 bytes.
+ * Element bytes are never interpreted (bf16 and fp8 are hashed as bytes). */
+typedef struct claim_pool_desc {
+  uint32_t num_layers;
+  uint32_t planes_per_layer; /* 1 or 2 */
+  uint32_t block_size;       /* tokens per block, 1..1024 */
+  uint32_t num_kv_heads;
+  uint32_t head_dim;
+  uint32_t elem_bytes;
+  uint32_t num_blocks;       /* < CLAIM_NONE */
+  uint32_t flags;            /* CLAIM_POOL_TIMING */
+  uint64_t seed;             /* cache-identity seed S */
+  void* kv_base;             /* device pointer, 16-byte aligned */
+  uint64_t kv_bytes;         /* >= planes * num_blocks * chunk bytes */
+  void* stream;              /* hipStream_t (NULL = default stream) */
+  uint64_t max_claims;       /* registry capacity (claims ever accepted) */
+  uint64_t max_footprint;    /* block-table entries ever accepted */
+  uint64_t event_capacity;   /* event records held between outcomes_read calls */
+} claim_pool_desc;
+
+/* A claim batch in compressed rows.  All arrays are device memory owned by
+ * the caller.  Claim c has block-table entries block_ids[block_offsets[c] ..
+ * block_offsets[c+1]) (CLAIM_NONE = missing entry) and token ids
+ * tokens[token_offsets[c] .. token_offsets[c+1]).  Rows whose offsets run
+ * backwards or past num_refs / num_tokens, or whose id is
+ * CLAIM_RESERVED_ID, are malformed: never accepted, UNKNOWN at check.
+ * Claim ids are stable and distinct from request ids (Table 5). */
+typedef struct claim_batch {
+  uint32_t num_claims;
+  uint32_t reserved; /* must be 0 */
+  uint64_t num_refs; /* entries in block_ids, < 2^32 */
+  uint64_t num_tokens;
+  const uint64_t* claim_ids;     /* [num_claims] */
+  const uint32_t* block_offsets; /* [num_claims + 1] */
+  const uint32_t* block_ids;     /* [num_refs] */
+  const uint64_t* token_offsets; /* [num_claims + 1] */
+  const uint32_t* tokens;        /* [num_tokens] */
+} claim_batch;
+
+/* Faults applied by claim_restore (host memory, read before it returns).
+ * flip f XORs canonical bit flip_bits[f] (bit 0 = least significant bit of
+ * canonical byte 0) of block flip_blocks[f]; a bit flipped twice is
+ * restored.  load_failed_blocks are reported load failures: they fail
+ * every claim that references them until a later offload of the block. */
+typedef struct claim_fault_spec {
+  uint32_t num_flips;
+  uint32_t num_load_failed;
+  const uint32_t* flip_blocks; /* [num_flips], each < num_blocks */
+  const uint64_t* flip_bits;   /* [num_flips], each < 8 * block bytes */
+  const uint32_t* load_failed_blocks; /* [num_load_failed], each < num_blocks */
+} claim_fault_spec;
+
+/* One claim's outcome (64 bytes). */
+typedef struct claim_outcome {
+  uint64_t claim_id;
+  uint32_t code;                /* CLAIM_UNKNOWN / _MATERIALIZED / _RESTORE_FAILED_FAIL_CLOSED */
+  uint32_t first_failing_block; /* position j* in the claim, CLAIM_NONE if none */
+  uint32_t phys_block;          /* block-table entry at j* (CLAIM_NONE if j* >= blocks) */
+  uint32_t num_blocks;          /* block-table entries presented (0 if malformed) */
+  uint32_t reasons;             /* OR of CLAIM_R_* found anywhere in the claim */
+  uint32_t reserved;
+  uint64_t expected_digest;     /* offload digest at j* (failures only, else 0) */
+  uint64_t observed_digest;     /* restored digest at j* (failures only, else 0) */
+  uint64_t chain_hash;          /* h_{nt-1} of the presented tokens (S if none) */
+  uint64_t chain_hash_at_fail;  /* h_{j*} if j* < nt, else 0 */
+} claim_outcome;
+
+/* One lifecycle event (40 bytes).  aux by kind: ACCEPTED = chain hash;
+ * OFFLOADED = blocks; RESTORE_REQUIRED = accepted blocks; RESTORED = chain
+ * hash; RESTORATION_FAILED = observed digest at the failing block;
+ * ACTIVE_REQUEST_REFUSED = blocking claim id (the claim itself);
+ * OUTCOME_UNKNOWN = reason bits. */
+typedef struct claim_event {
+  uint64_t seq;         /* position in the pool's global event order */
+  uint64_t claim_id;
+  uint64_t aux;
+  uint32_t kind;        /* CLAIM_EV_* */
+  uint32_t block_index; /* j, CLAIM_NONE if none */
+  uint32_t phys_block;  /* CLAIM_NONE if none */
+  uint32_t reserved;
+} claim_event;
+
+/* Stage times of the claim_check calls queued since the last
+ * claim_timing_read (pools created with CLAIM_POOL_TIMING). */
+typedef struct claim_timing {
+  uint32_t calls;          /* checks measured */
+  uint32_t last_unique;    /* unique blocks digested by the last check */
+  double total_ms;         /* sum over calls: whole check */
+  double digest_ms;        /* sum over calls: the gather + digest kernel */
+  double select_ms;        /* sum over calls: unique-block selection */
+  double finalize_ms;      /* sum over calls: per-block digest combine */
+  double claims_ms;        /* sum over calls: chain, compare, min-reduction, outcomes */
+  double events_ms;        /* sum over calls: event scan and append */
+} claim_timing;
+
+/* Create a pool over caller-owned KV memory (section 7: the connector's
+ * accepted-claim state; Table 5: fixed cache identity = seed + geometry).
+ * Allocates the pool's device state: offload and restored digests, offload
+ * records, reported-failure flags, the claim registry (ids, state, token
+ * count, chain hash, footprint), the event log and scratch.  Returns
+ * EINVAL for a bad description, ENOMEM / EHIP on allocation failure. */
+int claim_pool_create(const claim_pool_desc* desc, claim_pool** out);
+
+/* Wait for the pool's stream, then free everything the pool owns (not the
+ * KV memory).  NULL is accepted. */
+int claim_pool_destroy(claim_pool* pool);
+
+/* Accept and offload a batch (section 1: accept, materialized, offloaded;
+ * section 5 storage_restorability: the claim is accepted before offload).
+ * The whole batch is refused with EDUP if a non-reserved id occurs twice or
+ * is already registered (Table 2: duplicate ownership fails closed); nothing
+ * changes then.  Otherwise each well-formed claim is registered (event
+ * ACCEPTED); every in-range block it references gets an offload digest and
+ * its reported-failure flag is cleared; a claim whose footprint is
+ * non-empty, fully present and equal in length to ceil(tokens/block_size)
+ * becomes OFFLOADED (event OFFLOADED).  With staging != NULL the canonical
+ * bytes of every such block are also written to staging (device memory or
+ * host memory from hipHostMalloc, 16-byte aligned, else EINVAL), one block
+ * after another in ascending block-id order; staging_bytes must cover them
+ * (else ENOSPC).  A staged offload replaces the previous one.  Waits twice
+ * for the stream to read the acceptance verdict.  ENOSPC if the registry,
+ * footprint store or event log could overflow. */
+int claim_offload(claim_pool* pool, const claim_batch* batch, void* staging,
+                  uint64_t staging_bytes);
+
+/* Restore (section 7 path A steps 4-5, path B steps 3-5).  If staging is
+ * not NULL it must hold the bytes of the pool's last staged offload
+ * (staging_bytes covering every block it staged, else EINVAL): every staged
+ * block referenced by a well-formed claim of the batch is copied back into
+ * the pool.  Then the faults are applied (faults may be NULL).  Then each
+ * well-formed, registered and OFFLOADED claim of the batch moves to
+ * RESTORE_REQUIRED (event RESTORE_REQUIRED).  EINVAL for an out-of-range
+ * fault or a staging pointer that is not 16-byte aligned. */
+int claim_restore(claim_pool* pool, const claim_batch* batch, const void* staging,
+                  uint64_t staging_bytes, const claim_fault_spec* faults);
+
+/* Check (section 7 path A step 5, path B steps 5-7, path C): digest every
+ * in-range, offloaded block the well-formed claims reference, compare with
+ * the offload digest, chain each claim's tokens and decide its outcome: the
+ * smallest key (class << 32 | position) over the claim's problems wins,
+ * class 0 = ambiguity -> UNKNOWN, class 1 = load failure or digest mismatch
+ * -> RESTORE_FAILED_FAIL_CLOSED, none -> MATERIALIZED.  Appends, in batch
+ * order, RESTORED, or RESTORATION_FAILED then ACTIVE_REQUEST_REFUSED (the
+ * claim is its own blocking id), or OUTCOME_UNKNOWN.  The registry is not
+ * changed.  ENOSPC if the event log could overflow. */
+int claim_check(claim_pool* pool, const claim_batch* batch);
+
+/* Wait for the pool's stream and copy to the host the outcomes of the last
+ * claim_check (into out, capacity out_cap; *num_out = their count) and the
+ * events appended since the previous outcomes_read (into events, capacity
+ * ev_cap; *num_events = their count), which are then dropped from the log
+ * (sequence numbers keep counting).  A NULL out or events skips that part
+ * (events are then kept).  ENOSPC, with nothing copied or dropped, if a
+ * capacity is too small. */
+int outcomes_read(claim_pool* pool, claim_outcome* out, uint32_t out_cap, uint32_t* num_out,
+                  claim_event* events, uint64_t ev_cap, uint64_t* num_events);
+
+/* Wait for the pool's stream and return the summed stage times of the
+ * checks queued since the previous call (EINVAL unless the pool was created
+ * with CLAIM_POOL_TIMING). */
+int claim_timing_read(claim_pool* pool, claim_timing* out);
+
+/* Wait for the pool's stream and copy the per-block state of blocks
+ * [first, first + count) to the host: offload digests D_off, restored
+ * digests D_res (as of the last check that digested the block), offload
+ * records and reported-failure flags (one byte each, 0 or 1).  Any output
+ * pointer may be NULL.  EINVAL if the range exceeds the pool.  This is the
+ * block-level evidence behind a claim outcome (section 7 path B step 5). */
+int claim_block_state_read(claim_pool* pool, uint32_t first, uint32_t count, uint64_t* d_off,
+                           uint64_t* d_res, uint8_t* valid_off, uint8_t* load_failed);
+
+/* Text for a status code (static storage). */
+const char* claim_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CLAIMKV_H */

@@ -1,0 +1,290 @@
+"""Python binding of ``libclaimkv.so`` (the C ABI in ``include/claimkv.h``).
+
+Argument marshalling only: every step of offload, restore and check runs in
+the library's HIP kernels.  PyTorch provides device memory and the stream.
+There is no fallback: if the library is missing, loading it raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(_HERE)
+SOURCE = os.path.join(_HERE, "csrc", "claimkv.hip")
+LIBRARY = os.path.join(_HERE, "libclaimkv.so")
+INCLUDE = os.path.join(ROOT, "include")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-shared", "-std=c++17",
+             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+
+# ------------------------------------------------------------ vocabulary
+OK, EINVAL, ENOMEM, EHIP, ENOSPC, EDUP = 0, -1, -2, -3, -4, -5
+UNKNOWN, MATERIALIZED, RESTORE_FAILED_FAIL_CLOSED = 0, 1, 2
+EV_ACCEPTED, EV_OFFLOADED, EV_RESTORE_REQUIRED, EV_RESTORED = 1, 2, 3, 4
+EV_RESTORATION_FAILED, EV_ACTIVE_REQUEST_REFUSED, EV_OUTCOME_UNKNOWN = 5, 6, 7
+NONE = 0xFFFFFFFF
+RESERVED_ID = 0xFFFFFFFFFFFFFFFF
+POOL_TIMING = 0x1
+
+OUTCOME_DTYPE = np.dtype(
+    [("claim_id", "<u8"), ("code", "<u4"), ("first_failing_block", "<u4"), ("phys_block", "<u4"),
+     ("num_blocks", "<u4"), ("reasons", "<u4"), ("reserved", "<u4"), ("expected_digest", "<u8"),
+     ("observed_digest", "<u8"), ("chain_hash", "<u8"), ("chain_hash_at_fail", "<u8")])
+EVENT_DTYPE = np.dtype(
+    [("seq", "<u8"), ("claim_id", "<u8"), ("aux", "<u8"), ("kind", "<u4"), ("block_index", "<u4"),
+     ("phys_block", "<u4"), ("reserved", "<u4")])
+
+EXPORTS = ("claim_pool_create", "claim_pool_destroy", "claim_offload", "claim_restore",
+           "claim_check", "outcomes_read", "claim_timing_read", "claim_block_state_read",
+           "claim_strerror")
+
+
+class PoolDesc(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_uint32), ("planes_per_layer", ctypes.c_uint32),
+                ("block_size", ctypes.c_uint32), ("num_kv_heads", ctypes.c_uint32),
+                ("head_dim", ctypes.c_uint32), ("elem_bytes", ctypes.c_uint32),
+                ("num_blocks", ctypes.c_uint32), ("flags", ctypes.c_uint32),
+                ("seed", ctypes.c_uint64), ("kv_base", ctypes.c_void_p),
+                ("kv_bytes", ctypes.c_uint64), ("stream", ctypes.c_void_p),
+                ("max_claims", ctypes.c_uint64), ("max_footprint", ctypes.c_uint64),
+                ("event_capacity", ctypes.c_uint64)]
+
+
+class CBatch(ctypes.Structure):
+    _fields_ = [("num_claims", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("num_refs", ctypes.c_uint64), ("num_tokens", ctypes.c_uint64),
+                ("claim_ids", ctypes.c_void_p), ("block_offsets", ctypes.c_void_p),
+                ("block_ids", ctypes.c_void_p), ("token_offsets", ctypes.c_void_p),
+                ("tokens", ctypes.c_void_p)]
+
+
+class CFaults(ctypes.Structure):
+    _fields_ = [("num_flips", ctypes.c_uint32), ("num_load_failed", ctypes.c_uint32),
+                ("flip_blocks", ctypes.c_void_p), ("flip_bits", ctypes.c_void_p),
+                ("load_failed_blocks", ctypes.c_void_p)]
+
+
+class CTiming(ctypes.Structure):
+    _fields_ = [("calls", ctypes.c_uint32), ("last_unique", ctypes.c_uint32),
+                ("total_ms", ctypes.c_double), ("digest_ms", ctypes.c_double),
+                ("select_ms", ctypes.c_double), ("finalize_ms", ctypes.c_double),
+                ("claims_ms", ctypes.c_double), ("events_ms", ctypes.c_double)]
+
+
+assert ctypes.sizeof(PoolDesc) == 88 and ctypes.sizeof(CBatch) == 64
+assert OUTCOME_DTYPE.itemsize == 64 and EVENT_DTYPE.itemsize == 40
+
+
+class ClaimError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {strerror(status)} ({status})")
+
+
+def build() -> str:
+    """Compile libclaimkv.so for gfx950 in-tree."""
+    tmp = LIBRARY + ".tmp"
+    subprocess.run([HIPCC, *HIP_FLAGS, f"-I{INCLUDE}", SOURCE, "-o", tmp], check=True)
+    os.replace(tmp, LIBRARY)
+    return LIBRARY
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library.  Raises if it has not been built: there is no
+    fallback path."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIBRARY):
+            raise RuntimeError(f"{LIBRARY} is missing: build it (__graft_entry__.build())")
+        L = ctypes.CDLL(LIBRARY)
+        vp, i32, u32, u64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint32, ctypes.c_uint64
+        sig = {
+            "claim_pool_create": ([ctypes.POINTER(PoolDesc), ctypes.POINTER(vp)], i32),
+            "claim_pool_destroy": ([vp], i32),
+            "claim_offload": ([vp, ctypes.POINTER(CBatch), vp, u64], i32),
+            "claim_restore": ([vp, ctypes.POINTER(CBatch), vp, u64, ctypes.POINTER(CFaults)], i32),
+            "claim_check": ([vp, ctypes.POINTER(CBatch)], i32),
+            "outcomes_read": ([vp, vp, u32, ctypes.POINTER(u32), vp, u64, ctypes.POINTER(u64)], i32),
+            "claim_timing_read": ([vp, ctypes.POINTER(CTiming)], i32),
+            "claim_block_state_read": ([vp, u32, u32, vp, vp, vp, vp], i32),
+            "claim_strerror": ([i32], ctypes.c_char_p),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def strerror(status: int) -> str:
+    return lib().claim_strerror(status).decode()
+
+
+def _check(status: int, what: str) -> None:
+    if status != OK:
+        raise ClaimError(status, what)
+
+
+def _torch():
+    import torch
+
+    return torch
+
+
+class DeviceBatch:
+    """A claim batch in device memory (torch tensors) plus its C struct.
+
+    ``batch`` is any object with numpy arrays ``claim_ids`` (u64),
+    ``block_offsets`` (u32), ``block_ids`` (u32), ``token_offsets`` (u64)
+    and ``tokens`` (u32)."""
+
+    def __init__(self, batch, device="cuda"):
+        torch = _torch()
+
+        def up(a, np_dtype, t_dtype):
+            a = np.ascontiguousarray(np.asarray(a, dtype=np_dtype))
+            t = torch.from_numpy(a.view(t_dtype_np[t_dtype])).to(device)
+            return t
+
+        t_dtype_np = {torch.int64: np.int64, torch.int32: np.int32}
+        self.ids = up(batch.claim_ids, np.uint64, torch.int64)
+        self.bo = up(batch.block_offsets, np.uint32, torch.int32)
+        self.bi = up(batch.block_ids, np.uint32, torch.int32)
+        self.to = up(batch.token_offsets, np.uint64, torch.int64)
+        self.tok = up(batch.tokens, np.uint32, torch.int32)
+        n_claims = int(self.ids.numel())
+        self.struct = CBatch(
+            num_claims=n_claims, reserved=0, num_refs=int(self.bi.numel()),
+            num_tokens=int(self.tok.numel()),
+            claim_ids=self.ids.data_ptr() or None, block_offsets=self.bo.data_ptr() or None,
+            block_ids=self.bi.data_ptr() or None, token_offsets=self.to.data_ptr() or None,
+            tokens=self.tok.data_ptr() or None)
+
+    @property
+    def num_claims(self) -> int:
+        return int(self.struct.num_claims)
+
+
+class Pool:
+    """A claim pool over a caller-owned KV tensor on the current GPU.
+
+    ``geometry`` has num_layers, planes_per_layer, block_size, num_kv_heads,
+    head_dim, elem_bytes and num_blocks (e.g. ``synth.Geometry``); ``kv`` is a
+    contiguous CUDA tensor of at least planes x num_blocks x chunk bytes laid
+    out [plane][block][chunk]."""
+
+    def __init__(self, geometry, seed: int, kv, *, stream=None, max_claims: int = 1 << 16,
+                 max_footprint: int = 1 << 22, event_capacity: int = 1 << 20, timing: bool = False):
+        torch = _torch()
+        if not kv.is_cuda or not kv.is_contiguous():
+            raise ValueError("kv must be a contiguous device tensor")
+        if stream is None:
+            stream = torch.cuda.current_stream(kv.device)
+        self.kv = kv
+        self.stream = stream
+        self.geometry = geometry
+        self.seed = seed
+        d = PoolDesc(
+            num_layers=geometry.num_layers, planes_per_layer=geometry.planes_per_layer,
+            block_size=geometry.block_size, num_kv_heads=geometry.num_kv_heads,
+            head_dim=geometry.head_dim, elem_bytes=geometry.elem_bytes,
+            num_blocks=geometry.num_blocks, flags=POOL_TIMING if timing else 0, seed=seed,
+            kv_base=kv.data_ptr(), kv_bytes=kv.numel() * kv.element_size(),
+            stream=stream.cuda_stream, max_claims=max_claims, max_footprint=max_footprint,
+            event_capacity=event_capacity)
+        h = ctypes.c_void_p()
+        with torch.cuda.device(kv.device):
+            _check(lib().claim_pool_create(ctypes.byref(d), ctypes.byref(h)), "claim_pool_create")
+        self._h = h
+        self.event_capacity = event_capacity
+
+    def close(self) -> None:
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            _check(lib().claim_pool_destroy(h), "claim_pool_destroy")
+        self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    # --------------------------------------------------------------- calls
+    def offload(self, batch: DeviceBatch, staging=None, staging_bytes: int | None = None) -> None:
+        ptr, nbytes = _staging_args(staging, staging_bytes)
+        _check(lib().claim_offload(self._h, ctypes.byref(batch.struct), ptr, nbytes), "claim_offload")
+
+    def restore(self, batch: DeviceBatch, staging=None, faults=None,
+                staging_bytes: int | None = None) -> None:
+        ptr, nbytes = _staging_args(staging, staging_bytes)
+        keep = []
+        fs = None
+        if faults is not None:
+            fb = np.ascontiguousarray(faults.flip_blocks, dtype=np.uint32)
+            fbits = np.ascontiguousarray(faults.flip_bits, dtype=np.uint64)
+            lf = np.ascontiguousarray(faults.load_failed, dtype=np.uint32)
+            keep = [fb, fbits, lf]
+            fs = CFaults(num_flips=fb.size, num_load_failed=lf.size,
+                         flip_blocks=fb.ctypes.data if fb.size else None,
+                         flip_bits=fbits.ctypes.data if fbits.size else None,
+                         load_failed_blocks=lf.ctypes.data if lf.size else None)
+        _check(lib().claim_restore(self._h, ctypes.byref(batch.struct), ptr, nbytes,
+                                   ctypes.byref(fs) if fs is not None else None), "claim_restore")
+        del keep
+
+    def check(self, batch: DeviceBatch) -> None:
+        _check(lib().claim_check(self._h, ctypes.byref(batch.struct)), "claim_check")
+
+    def read(self, max_outcomes: int = 1 << 22, max_events: int | None = None):
+        """(outcomes of the last check, events since the last read)."""
+        if max_events is None:
+            max_events = self.event_capacity
+        out = np.zeros(max_outcomes, dtype=OUTCOME_DTYPE)
+        ev = np.zeros(max_events, dtype=EVENT_DTYPE)
+        n_out = ctypes.c_uint32()
+        n_ev = ctypes.c_uint64()
+        _check(lib().outcomes_read(self._h, out.ctypes.data, out.size, ctypes.byref(n_out),
+                                   ev.ctypes.data, ev.size, ctypes.byref(n_ev)), "outcomes_read")
+        return out[: n_out.value].copy(), ev[: n_ev.value].copy()
+
+    def block_state(self, first: int = 0, count: int | None = None) -> dict:
+        """Per-block digests and flags of blocks [first, first + count)."""
+        if count is None:
+            count = self.geometry.num_blocks - first
+        d_off = np.zeros(count, np.uint64)
+        d_res = np.zeros(count, np.uint64)
+        valid = np.zeros(count, np.uint8)
+        failed = np.zeros(count, np.uint8)
+        _check(lib().claim_block_state_read(self._h, first, count, d_off.ctypes.data,
+                                            d_res.ctypes.data, valid.ctypes.data,
+                                            failed.ctypes.data), "claim_block_state_read")
+        return {"d_off": d_off, "d_res": d_res, "valid_off": valid, "load_failed": failed}
+
+    def timing(self) -> dict:
+        t = CTiming()
+        _check(lib().claim_timing_read(self._h, ctypes.byref(t)), "claim_timing_read")
+        return {name: getattr(t, name) for name, _ in CTiming._fields_}
+
+
+def _staging_args(staging, nbytes):
+    if staging is None:
+        return None, 0
+    if hasattr(staging, "data_ptr"):
+        return staging.data_ptr(), nbytes if nbytes is not None else staging.numel() * staging.element_size()
+    return int(staging), int(nbytes or 0)

@@ -1,0 +1,1528 @@
+// claimkv.hip -- claim-scoped KV materialization checking for MI355X (gfx950).
+//
+// HIP kernels and the host side of the C ABI declared in include/claimkv.h.
+// The header states what each call computes and which passage of the paper
+// ("Fail-Closed Lowering of Resident KV Claims onto LLM Serving Runtimes")
+// it follows; this file is the implementation.
+//
+// Design (one GPU, one stream per pool, all work integer, no MFMA: nothing
+// on this path is a dense contraction):
+//
+//  * Block digest (the HBM-bound stage).  The pool is plane-major
+//    [plane][block][chunk].  D(b) = sum_i w_i k_i is linear in the words, so
+//    it splits into partial sums over (plane, segment) pieces of the
+//    canonical block: the key k_i depends only on the word's canonical
+//    position, so a wave pinned to one (plane, segment) keeps that piece's
+//    keys in VGPRs for its whole life and streams the same piece of many
+//    blocks.  A piece is 64 lanes x LPT 16-byte vectors (LPT = 8: 8 KiB);
+//    each load instruction moves 1 KiB of contiguous, coalesced bytes.
+//    Each 64-bit word costs one 32x32->64 multiply-add for lo(w) lo(k) and
+//    two 32-bit multiply-adds for the cross terms (only their low 32 bits
+//    reach the result mod 2^64).  The wave sum is written as one partial per
+//    (block, piece); a second small kernel adds a block's partials.  No
+//    atomics, so results are bitwise deterministic.
+//  * Unique blocks.  Blocks referenced by a batch are marked, then compacted
+//    in ascending order, so each physical block is read once however many
+//    claims alias it.
+//  * Claims.  A group of W lanes (W = 2..64, picked from the batch's mean
+//    claim length) owns one claim: lanes take block positions j = j0 + lane,
+//    test their block (footprint, missing entry, offload record, reported
+//    failure, digest mismatch) and compute the token multilinear M_j; the
+//    serial chain h_j = splitmix64(h_{j-1} ^ M_j) then walks the W
+//    positions of the round through lane shuffles.  The outcome is the
+//    minimum of packed keys (class << 32 | position).
+//  * Events.  Per-claim event counts (0..2) are scanned in three small
+//    kernels (tile sums, one-workgroup scan of the tile sums, write) so the
+//    log stays in batch order with no spin waits.
+
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+#include <string.h>
+
+#include <new>
+
+#include "claimkv.h"
+
+namespace {
+
+// ------------------------------------------------------------------ constants
+
+constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kEmptyId = CLAIM_RESERVED_ID;  // registry empty slot
+constexpr uint32_t kNone = CLAIM_NONE;
+constexpr uint64_t kNoKey = ~0ull;
+constexpr uint64_t kClaimLevelKey = (uint64_t)kNone;  // class 0, position NONE
+constexpr uint32_t kMaxBlockSize = 1024;
+constexpr int kThreads = 256;
+constexpr int kTile = 1024;  // claims per event-scan tile
+
+constexpr uint32_t kStAccepted = 1, kStOffloaded = 2, kStRestoreRequired = 4;
+
+enum MarkMode : int { kMarkAny = 0, kMarkOffloaded = 1, kMarkStaged = 2 };
+
+// --------------------------------------------------------------- hash helpers
+
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ uint64_t splitmix_step(uint64_t x) { return mix64(x + kGamma); }
+
+__device__ __forceinline__ uint64_t stream_output(uint64_t s, uint64_t i) {
+  return mix64(s + (i + 1) * kGamma);
+}
+
+// Slot hash of the claim registry (a data-structure detail, unrelated to the
+// digest): the 64-bit finaliser of MurmurHash3.
+__device__ __forceinline__ uint64_t slot_of_id(uint64_t id, uint64_t mask) {
+  id ^= id >> 33;
+  id *= 0xFF51AFD7ED558CCDull;
+  id ^= id >> 33;
+  id *= 0xC4CEB9FE1A85EC53ull;
+  id ^= id >> 33;
+  return id & mask;
+}
+
+// ----------------------------------------------------------- lane exchange
+
+__device__ __forceinline__ uint32_t lane_read(uint32_t v, uint32_t src_lane) {
+  return (uint32_t)__builtin_amdgcn_ds_bpermute((int)(src_lane << 2), (int)v);
+}
+
+__device__ __forceinline__ uint64_t lane_read64(uint64_t v, uint32_t src_lane) {
+  const uint32_t lo = lane_read((uint32_t)v, src_lane);
+  const uint32_t hi = lane_read((uint32_t)(v >> 32), src_lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t wave_sum64(uint64_t v) {
+  const uint32_t lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += lane_read64(v, lane ^ o);
+  return v;
+}
+
+template <int W>
+__device__ __forceinline__ uint64_t group_min64(uint64_t v) {
+  const uint32_t lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = W / 2; o >= 1; o >>= 1) {
+    const uint64_t w = lane_read64(v, lane ^ o);
+    v = w < v ? w : v;
+  }
+  return v;
+}
+
+template <int W>
+__device__ __forceinline__ uint32_t group_or(uint32_t v) {
+  const uint32_t lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = W / 2; o >= 1; o >>= 1) v |= lane_read(v, lane ^ o);
+  return v;
+}
+
+// ---------------------------------------------------------- kernel argument
+
+struct BatchDev {
+  uint64_t C, N, T;
+  const uint64_t* ids;
+  const uint32_t* bo;
+  const uint32_t* bi;
+  const uint64_t* to;
+  const uint32_t* tok;
+};
+
+struct RegDev {
+  uint64_t mask;
+  uint64_t* key;
+  uint32_t* state;
+  uint32_t* nblk;
+  uint64_t* ntok;
+  uint64_t* chain;
+  uint64_t* fpoff;
+  const uint32_t* fp;
+};
+
+struct Pend {  // events a claim will append (0..2), written before the scan
+  uint64_t aux0, aux1;
+  uint32_t kinds;  // kind0 | kind1 << 8
+  uint32_t j;
+  uint32_t phys;
+  uint32_t pad;
+};
+
+struct Counters {  // device-resident counters of one pool (48 bytes)
+  uint32_t uniq_count;
+  uint32_t dup_flag;
+  uint64_t log_count;  // events held in the log
+  uint64_t seq_next;   // next global sequence number
+  uint64_t call_pos;   // log position of the current call's first event
+  uint64_t call_seq;   // its sequence number
+  uint64_t reg_count;  // claims registered
+};
+
+static_assert(sizeof(Counters) == 48, "Counters layout");
+static_assert(sizeof(claim_outcome) == 64, "claim_outcome layout");
+static_assert(sizeof(claim_event) == 40, "claim_event layout");
+static_assert(sizeof(Pend) == 32, "Pend layout");
+
+struct Row {
+  uint64_t id;
+  uint64_t to0, ntok;
+  uint32_t bo0, n;
+  bool malformed;
+};
+
+__device__ __forceinline__ Row read_row(const BatchDev& b, uint64_t c) {
+  Row r;
+  r.id = b.ids[c];
+  const uint32_t bo0 = b.bo[c], bo1 = b.bo[c + 1];
+  const uint64_t to0 = b.to[c], to1 = b.to[c + 1];
+  r.malformed = r.id == kEmptyId || bo0 > bo1 || (uint64_t)bo1 > b.N || to0 > to1 || to1 > b.T;
+  r.bo0 = bo0;
+  r.n = r.malformed ? 0 : bo1 - bo0;
+  r.to0 = to0;
+  r.ntok = r.malformed ? 0 : to1 - to0;
+  return r;
+}
+
+__device__ __forceinline__ int64_t reg_find(const RegDev& r, uint64_t id) {
+  if (id == kEmptyId) return -1;
+  uint64_t s = slot_of_id(id, r.mask);
+  for (uint64_t probe = 0; probe <= r.mask; ++probe) {
+    const uint64_t k = r.key[s];
+    if (k == id) return (int64_t)s;
+    if (k == kEmptyId) return -1;
+    s = (s + 1) & r.mask;
+  }
+  return -1;
+}
+
+__device__ __forceinline__ uint64_t token_multilinear(const uint32_t* __restrict__ tok,
+                                                      uint64_t first, uint64_t count,
+                                                      const uint64_t* tkey) {
+  uint64_t m_sum = 0;
+  for (uint64_t m = 0; m < count; ++m) m_sum += (uint64_t)tok[first + m] * tkey[m];
+  return m_sum;
+}
+
+__device__ __forceinline__ void load_token_keys(uint64_t* tkey, uint32_t bs, uint64_t seed) {
+  for (uint32_t m = threadIdx.x; m < bs; m += blockDim.x) tkey[m] = stream_output(~seed, m) | 1ull;
+  __syncthreads();
+}
+
+// ------------------------------------------------------------ small kernels
+
+template <typename T>
+__global__ void __launch_bounds__(kThreads) k_fill(T* p, uint64_t n, T v) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
+}
+
+__global__ void __launch_bounds__(kThreads) k_copy_u32(uint32_t* dst, const uint32_t* src,
+                                                       uint64_t n) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    dst[i] = src[i];
+}
+
+// Mark the in-range blocks referenced by well-formed claims (filtered by
+// mode).  A group of W lanes walks one claim's row.
+template <int W>
+__global__ void __launch_bounds__(kThreads) k_mark(BatchDev b, uint32_t nb, int mode,
+                                                   const uint8_t* __restrict__ valid_off,
+                                                   const uint32_t* __restrict__ slot_of,
+                                                   uint8_t* __restrict__ mark) {
+  const uint64_t c = ((uint64_t)blockIdx.x * kThreads + threadIdx.x) / W;
+  if (c >= b.C) return;
+  const uint32_t gl = threadIdx.x & (W - 1);
+  const Row r = read_row(b, c);
+  for (uint32_t j = gl; j < r.n; j += W) {
+    const uint32_t blk = b.bi[(uint64_t)r.bo0 + j];
+    if (blk >= nb) continue;
+    if (mode == kMarkOffloaded && !valid_off[blk]) continue;
+    if (mode == kMarkStaged && slot_of[blk] == kNone) continue;
+    mark[blk] = 1;
+  }
+}
+
+// Exclusive scan over a 1024-thread workgroup; returns the prefix and
+// writes the total to *total.
+__device__ uint32_t block_exclusive_scan_1024(uint32_t v, uint32_t* total, uint32_t* lds16) {
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t incl = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t up = lane_read(incl, lane >= (uint32_t)o ? lane - o : lane);
+    if (lane >= (uint32_t)o) incl += up;
+  }
+  if (lane == 63) lds16[wave] = incl;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t run = 0;
+    for (int w = 0; w < 16; ++w) {
+      const uint32_t t = lds16[w];
+      lds16[w] = run;
+      run += t;
+    }
+    lds16[16] = run;
+  }
+  __syncthreads();
+  const uint32_t out = lds16[wave] + incl - v;
+  *total = lds16[16];
+  __syncthreads();
+  return out;
+}
+
+// Ordered compaction of the marks into the unique-block list (ascending
+// block id).  One workgroup of 1024 threads; clears the marks it reads.
+__global__ void __launch_bounds__(1024) k_compact(uint8_t* __restrict__ mark, uint32_t nb,
+                                                  uint32_t* __restrict__ uniq,
+                                                  Counters* __restrict__ ctr) {
+  __shared__ uint32_t lds[17];
+  uint32_t base = 0;
+  constexpr uint32_t kPer = 16;
+  for (uint64_t t0 = 0; t0 < nb; t0 += 1024ull * kPer) {
+    const uint64_t first = t0 + (uint64_t)threadIdx.x * kPer;
+    uint32_t bits = 0;
+    for (uint32_t k = 0; k < kPer; ++k) {
+      const uint64_t i = first + k;
+      if (i < nb && mark[i]) bits |= 1u << k;
+    }
+    uint32_t total;
+    uint32_t pos = base + block_exclusive_scan_1024(__builtin_popcount(bits), &total, lds);
+    for (uint32_t k = 0; k < kPer; ++k) {
+      if (bits & (1u << k)) {
+        uniq[pos++] = (uint32_t)(first + k);
+        mark[first + k] = 0;
+      }
+    }
+    base += total;
+  }
+  if (threadIdx.x == 0) ctr->uniq_count = base;
+}
+
+// ----------------------------------------------------------- digest kernel
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Partial digests of the unique blocks.  Wave w serves piece ps = w % PS
+// (plane p = ps / segs, segment s = ps % segs) and blocks u = w / PS,
+// w / PS + groups, ...  Lane l, slot k covers 16-byte vector
+// v = s*64*LPT + 64k + l of the plane's chunk, i.e. canonical words
+// i = p*2V + 2v and 2v + 1.  Optionally copies the vectors to staging
+// ([slot][plane][chunk], slot = unique index).
+template <int LPT>
+__global__ void __launch_bounds__(kThreads) k_digest(const u32x4* __restrict__ pool, uint32_t nb,
+                                                     uint32_t chunk_vecs, uint32_t planes,
+                                                     uint32_t segs, uint32_t groups,
+                                                     const uint32_t* __restrict__ uniq,
+                                                     const Counters* __restrict__ ctr,
+                                                     uint64_t seed, uint64_t* __restrict__ partial,
+                                                     u32x4* __restrict__ staging) {
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t wave = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const uint32_t ps_total = planes * segs;
+  const uint32_t ps = wave % ps_total;
+  const uint32_t g = wave / ps_total;
+  if (g >= groups) return;
+  const uint32_t p = ps / segs, s = ps % segs;
+
+  uint32_t klo[LPT][2], khi[LPT][2];
+  bool valid[LPT];
+#pragma unroll
+  for (int k = 0; k < LPT; ++k) {
+    const uint32_t v = s * 64u * LPT + 64u * k + lane;
+    valid[k] = v < chunk_vecs;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const uint64_t key = stream_output(seed, (uint64_t)p * chunk_vecs * 2 + 2ull * v + h) | 1ull;
+      klo[k][h] = valid[k] ? (uint32_t)key : 0u;
+      khi[k][h] = valid[k] ? (uint32_t)(key >> 32) : 0u;
+    }
+  }
+
+  const uint32_t U = ctr->uniq_count;
+  const uint64_t piece = (uint64_t)s * 64u * LPT + lane;
+  for (uint32_t u = g; u < U; u += groups) {
+    const uint32_t b = uniq[u];
+    const u32x4* chunk = pool + ((uint64_t)p * nb + b) * chunk_vecs;
+    u32x4 x[LPT];
+#pragma unroll
+    for (int k = 0; k < LPT; ++k) {
+      // a masked slot (past the end of a ragged chunk) reads the chunk's
+      // first vector instead and discards it: no address outside the chunk
+      // is ever formed
+      const u32x4 t = __builtin_nontemporal_load(chunk + (valid[k] ? piece + 64 * k : 0));
+      x[k] = valid[k] ? t : u32x4{0u, 0u, 0u, 0u};
+    }
+    uint64_t acc = 0;
+    uint32_t cross = 0;
+#pragma unroll
+    for (int k = 0; k < LPT; ++k) {
+      // word 0 = (x.y:x.x), word 1 = (x.w:x.z)
+      acc += (uint64_t)x[k].x * klo[k][0];
+      cross += x[k].x * khi[k][0] + x[k].y * klo[k][0];
+      acc += (uint64_t)x[k].z * klo[k][1];
+      cross += x[k].z * khi[k][1] + x[k].w * klo[k][1];
+    }
+    const uint64_t sum = wave_sum64(acc + ((uint64_t)cross << 32));
+    if (lane == 0) partial[(uint64_t)u * ps_total + ps] = sum;
+    if (staging) {
+      u32x4* dst = staging + ((uint64_t)u * planes + p) * chunk_vecs + piece;
+#pragma unroll
+      for (int k = 0; k < LPT; ++k)
+        if (valid[k]) dst[64 * k] = x[k];
+    }
+  }
+}
+
+// Add each unique block's partials.  One wave per block.
+//   mode 0 (offload): d_off, valid_off = 1, load_failed = 0, slot_of
+//   mode 1 (check):   d_res
+__global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restrict__ uniq,
+                                                       const Counters* __restrict__ ctr,
+                                                       const uint64_t* __restrict__ partial,
+                                                       uint32_t ps_total, int mode, int staged,
+                                                       uint64_t* __restrict__ d_out,
+                                                       uint8_t* __restrict__ valid_off,
+                                                       uint8_t* __restrict__ load_failed,
+                                                       uint32_t* __restrict__ slot_of) {
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t waves = gridDim.x * (kThreads / 64);
+  const uint32_t U = ctr->uniq_count;
+  for (uint32_t u = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6); u < U; u += waves) {
+    uint64_t sum = 0;
+    for (uint32_t q = lane; q < ps_total; q += 64) sum += partial[(uint64_t)u * ps_total + q];
+    sum = wave_sum64(sum);
+    if (lane == 0) {
+      const uint32_t b = uniq[u];
+      d_out[b] = sum;
+      if (mode == 0) {
+        valid_off[b] = 1;
+        load_failed[b] = 0;
+        slot_of[b] = staged ? u : kNone;
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------------- offload
+
+// Duplicate ownership: a non-reserved id occurring twice in the batch or
+// already registered sets dup_flag.  table is a cleared scratch hash set.
+__global__ void __launch_bounds__(kThreads) k_dupcheck(BatchDev b, RegDev reg,
+                                                       unsigned long long* table, uint64_t tmask,
+                                                       Counters* ctr) {
+  const uint64_t c = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (c >= b.C) return;
+  const uint64_t id = b.ids[c];
+  if (id == kEmptyId) return;
+  if (reg_find(reg, id) >= 0) {
+    atomicOr(&ctr->dup_flag, 1u);
+    return;
+  }
+  uint64_t s = slot_of_id(id, tmask);
+  for (uint64_t probe = 0; probe <= tmask; ++probe) {
+    const unsigned long long old = atomicCAS(table + s, (unsigned long long)kEmptyId,
+                                             (unsigned long long)id);
+    if (old == kEmptyId) return;
+    if (old == id) {
+      atomicOr(&ctr->dup_flag, 1u);
+      return;
+    }
+    s = (s + 1) & tmask;
+  }
+}
+
+// Acceptance: chain hash of the claim's tokens, presence of its footprint,
+// registration, and the ACCEPTED (+ OFFLOADED) events.
+template <int W>
+__global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, uint32_t nb,
+                                                     uint32_t bs, uint64_t seed, uint64_t fp_base,
+                                                     Counters* __restrict__ ctr,
+                                                     uint32_t* __restrict__ cnt,
+                                                     Pend* __restrict__ pend) {
+  __shared__ uint64_t tkey[kMaxBlockSize];
+  load_token_keys(tkey, bs, seed);
+  const uint64_t c = ((uint64_t)blockIdx.x * kThreads + threadIdx.x) / W;
+  if (c >= b.C) return;
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t gl = lane & (W - 1), gbase = lane & ~(uint32_t)(W - 1);
+  const Row r = read_row(b, c);
+  const uint64_t nt = (r.ntok + bs - 1) / bs;
+  const uint64_t L = (uint64_t)r.n > nt ? (uint64_t)r.n : nt;
+
+  uint64_t h = seed;
+  uint32_t missing = 0;
+  for (uint64_t j0 = 0; j0 < L; j0 += W) {
+    const uint64_t j = j0 + gl;
+    if (j < r.n && b.bi[(uint64_t)r.bo0 + j] >= nb) missing = 1;
+    uint64_t m_sum = 0;
+    if (j < nt) {
+      const uint64_t first = j * bs;
+      const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
+      m_sum = token_multilinear(b.tok, r.to0 + first, count, tkey);
+    }
+    const uint64_t steps = j0 < nt ? (nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W) : 0;
+    for (uint32_t t = 0; t < steps; ++t) h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
+  }
+  missing = group_or<W>(missing);
+  if (gl != 0) return;
+  if (r.malformed) {
+    cnt[c] = 0;
+    return;
+  }
+  const bool offloaded = r.n > 0 && !missing && (uint64_t)r.n == nt;
+  uint64_t s = slot_of_id(r.id, reg.mask);
+  bool inserted = false;
+  for (uint64_t probe = 0; probe <= reg.mask && !inserted; ++probe) {
+    const unsigned long long old = atomicCAS((unsigned long long*)reg.key + s,
+                                             (unsigned long long)kEmptyId,
+                                             (unsigned long long)r.id);
+    if (old == kEmptyId)
+      inserted = true;
+    else
+      s = (s + 1) & reg.mask;
+  }
+  if (!inserted) {  // unreachable: the host keeps the table at most half full
+    cnt[c] = 0;
+    return;
+  }
+  reg.state[s] = kStAccepted | (offloaded ? kStOffloaded : 0u);
+  reg.nblk[s] = r.n;
+  reg.ntok[s] = r.ntok;
+  reg.chain[s] = h;
+  reg.fpoff[s] = fp_base + r.bo0;
+  atomicAdd((unsigned long long*)&ctr->reg_count, 1ull);
+  Pend pe;
+  pe.aux0 = h;
+  pe.aux1 = r.n;
+  pe.kinds = CLAIM_EV_ACCEPTED | (offloaded ? (CLAIM_EV_OFFLOADED << 8) : 0u);
+  pe.j = kNone;
+  pe.phys = kNone;
+  pe.pad = 0;
+  pend[c] = pe;
+  cnt[c] = offloaded ? 2 : 1;
+}
+
+// ----------------------------------------------------------------- restore
+
+__global__ void __launch_bounds__(kThreads) k_flips(uint32_t* __restrict__ pool32, uint32_t nb,
+                                                    uint64_t chunk_bytes, uint32_t n,
+                                                    const uint32_t* __restrict__ blocks,
+                                                    const uint64_t* __restrict__ bits) {
+  const uint32_t f = blockIdx.x * kThreads + threadIdx.x;
+  if (f >= n) return;
+  const uint64_t byte = bits[f] >> 3;
+  const uint64_t p = byte / chunk_bytes, q = byte % chunk_bytes;
+  const uint64_t addr = (p * nb + blocks[f]) * chunk_bytes + q;
+  atomicXor(pool32 + (addr >> 2), 1u << ((addr & 3) * 8 + (bits[f] & 7)));
+}
+
+__global__ void __launch_bounds__(kThreads) k_set_failed(uint8_t* __restrict__ load_failed,
+                                                         uint32_t n,
+                                                         const uint32_t* __restrict__ blocks) {
+  const uint32_t f = blockIdx.x * kThreads + threadIdx.x;
+  if (f < n) load_failed[blocks[f]] = 1;
+}
+
+// Copy staged blocks (those in the unique list) back into the pool.
+__global__ void __launch_bounds__(kThreads) k_unstage(u32x4* __restrict__ pool, uint32_t nb,
+                                                      uint32_t chunk_vecs, uint32_t planes,
+                                                      const uint32_t* __restrict__ uniq,
+                                                      const Counters* __restrict__ ctr,
+                                                      const uint32_t* __restrict__ slot_of,
+                                                      const u32x4* __restrict__ staging) {
+  const uint64_t per_block = (uint64_t)planes * chunk_vecs;
+  const uint64_t total = (uint64_t)ctr->uniq_count * per_block;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+    const uint64_t u = i / per_block, r = i % per_block;
+    const uint32_t b = uniq[u];
+    const uint64_t p = r / chunk_vecs, v = r % chunk_vecs;
+    pool[(p * nb + b) * chunk_vecs + v] = staging[(uint64_t)slot_of[b] * per_block + r];
+  }
+}
+
+__global__ void __launch_bounds__(kThreads) k_restore_claims(BatchDev b, RegDev reg,
+                                                             uint32_t* __restrict__ cnt,
+                                                             Pend* __restrict__ pend) {
+  const uint64_t c = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (c >= b.C) return;
+  const Row r = read_row(b, c);
+  cnt[c] = 0;
+  if (r.malformed) return;
+  const int64_t s = reg_find(reg, r.id);
+  if (s < 0 || !(reg.state[s] & kStOffloaded)) return;
+  atomicOr(reg.state + s, kStRestoreRequired);
+  Pend pe;
+  pe.aux0 = reg.nblk[s];
+  pe.aux1 = 0;
+  pe.kinds = CLAIM_EV_RESTORE_REQUIRED;
+  pe.j = kNone;
+  pe.phys = kNone;
+  pe.pad = 0;
+  pend[c] = pe;
+  cnt[c] = 1;
+}
+
+// ------------------------------------------------------------------- check
+
+struct CheckState {
+  const uint64_t* d_off;
+  const uint64_t* d_res;
+  const uint8_t* valid_off;
+  const uint8_t* load_failed;
+};
+
+template <int W>
+__global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, CheckState st,
+                                                    uint32_t nb, uint32_t bs, uint64_t seed,
+                                                    claim_outcome* __restrict__ out,
+                                                    uint32_t* __restrict__ cnt,
+                                                    Pend* __restrict__ pend) {
+  __shared__ uint64_t tkey[kMaxBlockSize];
+  load_token_keys(tkey, bs, seed);
+  const uint64_t c = ((uint64_t)blockIdx.x * kThreads + threadIdx.x) / W;
+  if (c >= b.C) return;
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t gl = lane & (W - 1), gbase = lane & ~(uint32_t)(W - 1);
+  const Row r = read_row(b, c);
+  const uint64_t nt = (r.ntok + bs - 1) / bs;
+  const uint64_t n = r.n;
+
+  uint32_t reasons = 0;
+  uint64_t special = kNoKey;  // claim-level and length keys
+  int64_t slot = -1;
+  uint32_t na = 0, state = 0;
+  uint64_t acc_ntok = 0, acc_chain = 0, fpo = 0;
+  if (r.malformed) {
+    reasons |= CLAIM_R_MALFORMED;
+    special = kClaimLevelKey;
+  } else {
+    slot = reg_find(reg, r.id);
+    if (slot < 0) {
+      reasons |= CLAIM_R_NOT_ACCEPTED;
+      special = kClaimLevelKey;
+    } else {
+      state = reg.state[slot];
+      na = reg.nblk[slot];
+      acc_ntok = reg.ntok[slot];
+      acc_chain = reg.chain[slot];
+      fpo = reg.fpoff[slot];
+      if (!(state & kStOffloaded)) {
+        reasons |= CLAIM_R_NOT_OFFLOADED;
+        special = kClaimLevelKey;
+      }
+      if (!(state & kStRestoreRequired)) {
+        reasons |= CLAIM_R_NO_RESTORE;
+        special = kClaimLevelKey;
+      }
+      if (n != na) {
+        reasons |= CLAIM_R_FOOTPRINT_MISMATCH;
+        const uint64_t k = n < na ? n : na;
+        special = k < special ? k : special;
+      }
+    }
+    if (n == 0) {
+      reasons |= CLAIM_R_EMPTY;
+      special = kClaimLevelKey < special ? kClaimLevelKey : special;
+    }
+    if (n != nt) {
+      reasons |= CLAIM_R_SHAPE_MISMATCH;
+      const uint64_t k = n < nt ? n : nt;
+      special = k < special ? k : special;
+    }
+  }
+  const bool found = slot >= 0;
+  const uint64_t common = n < na ? n : na;
+  const uint64_t q1 = (found && n != na) ? common : kNoKey;  // positions whose
+  const uint64_t q2 = (n != nt) ? (n < nt ? n : nt) : kNoKey;  // h may be needed
+
+  uint64_t h = seed, best_pos = kNoKey, h_best = 0, h_q1 = 0, h_q2 = 0;
+  const uint64_t L = n > nt ? n : nt;
+  for (uint64_t j0 = 0; j0 < L; j0 += W) {
+    const uint64_t j = j0 + gl;
+    uint64_t my_key = kNoKey;
+    if (j < n) {
+      const uint32_t blk = b.bi[(uint64_t)r.bo0 + j];
+      if (found && j < common && blk != reg.fp[fpo + j]) {
+        reasons |= CLAIM_R_FOOTPRINT_MISMATCH;
+        my_key = j;
+      }
+      if (blk >= nb) {
+        reasons |= CLAIM_R_MISSING_ENTRY;
+        my_key = j < my_key ? j : my_key;
+      } else if (!st.valid_off[blk]) {
+        reasons |= CLAIM_R_NO_OFFLOAD_RECORD;
+        my_key = j < my_key ? j : my_key;
+      } else {
+        const bool lf = st.load_failed[blk] != 0;
+        const bool mm = st.d_res[blk] != st.d_off[blk];
+        if (lf) reasons |= CLAIM_R_LOAD_FAILED;
+        if (mm) reasons |= CLAIM_R_DIGEST_MISMATCH;
+        const uint64_t k = (1ull << 32) | j;
+        if ((lf || mm) && k < my_key) my_key = k;
+      }
+    }
+    uint64_t m_sum = 0;
+    if (j < nt) {
+      const uint64_t first = j * bs;
+      const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
+      m_sum = token_multilinear(b.tok, r.to0 + first, count, tkey);
+    }
+    const uint64_t steps = j0 < nt ? (nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W) : 0;
+    uint64_t my_h = 0;
+    for (uint32_t t = 0; t < steps; ++t) {
+      h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
+      if (gl == t) my_h = h;
+    }
+    const uint64_t rk = group_min64<W>(my_key);
+    if (rk < best_pos) {
+      best_pos = rk;
+      h_best = lane_read64(my_h, gbase + (uint32_t)((rk & 0xFFFFFFFFull) - j0));
+    }
+    if (q1 >= j0 && q1 < j0 + W) h_q1 = lane_read64(my_h, gbase + (uint32_t)(q1 - j0));
+    if (q2 >= j0 && q2 < j0 + W) h_q2 = lane_read64(my_h, gbase + (uint32_t)(q2 - j0));
+  }
+  if (found && (acc_ntok != r.ntok || acc_chain != h)) {
+    reasons |= CLAIM_R_TOKEN_MISMATCH;
+    special = kClaimLevelKey < special ? kClaimLevelKey : special;
+  }
+  reasons = group_or<W>(reasons);
+  if (gl != 0) return;
+
+  const uint64_t best = best_pos < special ? best_pos : special;
+  claim_outcome o;
+  o.claim_id = r.id;
+  o.num_blocks = r.n;
+  o.reasons = reasons;
+  o.reserved = 0;
+  o.expected_digest = 0;
+  o.observed_digest = 0;
+  o.chain_hash = h;
+  o.chain_hash_at_fail = 0;
+  Pend pe;
+  pe.pad = 0;
+  pe.aux1 = 0;
+  if (best == kNoKey) {
+    o.code = CLAIM_MATERIALIZED;
+    o.first_failing_block = kNone;
+    o.phys_block = kNone;
+    pe.kinds = CLAIM_EV_RESTORED;
+    pe.aux0 = h;
+    cnt[c] = 1;
+  } else {
+    const uint32_t cls = (uint32_t)(best >> 32);
+    const uint32_t js = (uint32_t)(best & 0xFFFFFFFFull);
+    o.code = cls == 0 ? CLAIM_UNKNOWN : CLAIM_RESTORE_FAILED_FAIL_CLOSED;
+    o.first_failing_block = js;
+    o.phys_block = (uint64_t)js < n ? b.bi[(uint64_t)r.bo0 + js] : kNone;
+    if (cls == 1) {
+      o.expected_digest = st.d_off[o.phys_block];
+      o.observed_digest = st.d_res[o.phys_block];
+    }
+    if (js != kNone && (uint64_t)js < nt)
+      o.chain_hash_at_fail = best == best_pos ? h_best : (js == q1 ? h_q1 : h_q2);
+    if (cls == 1) {
+      pe.kinds = CLAIM_EV_RESTORATION_FAILED | (CLAIM_EV_ACTIVE_REQUEST_REFUSED << 8);
+      pe.aux0 = o.observed_digest;
+      pe.aux1 = r.id;
+      cnt[c] = 2;
+    } else {
+      pe.kinds = CLAIM_EV_OUTCOME_UNKNOWN;
+      pe.aux0 = reasons;
+      cnt[c] = 1;
+    }
+  }
+  pe.j = o.first_failing_block;
+  pe.phys = o.phys_block;
+  out[c] = o;
+  pend[c] = pe;
+}
+
+// ------------------------------------------------------------ event append
+
+__global__ void __launch_bounds__(kThreads) k_tile_sums(const uint32_t* __restrict__ cnt,
+                                                        uint64_t C, uint32_t* __restrict__ tsum) {
+  __shared__ uint32_t lds[kThreads / 64];
+  const uint64_t first = (uint64_t)blockIdx.x * kTile + threadIdx.x * (kTile / kThreads);
+  uint32_t v = 0;
+  for (int k = 0; k < kTile / kThreads; ++k)
+    if (first + k < C) v += cnt[first + k];
+  const uint32_t lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += lane_read(v, lane ^ o);
+  if (lane == 0) lds[threadIdx.x >> 6] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) tsum[blockIdx.x] = lds[0] + lds[1] + lds[2] + lds[3];
+}
+
+// One workgroup: exclusive scan of the tile sums; reserves the call's range
+// of the log.
+__global__ void __launch_bounds__(1024) k_scan_tiles(uint32_t* __restrict__ tsum, uint64_t ntiles,
+                                                     Counters* __restrict__ ctr) {
+  __shared__ uint32_t lds[17];
+  __shared__ uint64_t run;
+  if (threadIdx.x == 0) run = 0;
+  __syncthreads();
+  for (uint64_t t0 = 0; t0 < ntiles; t0 += 1024) {
+    const uint64_t t = t0 + threadIdx.x;
+    const uint32_t v = t < ntiles ? tsum[t] : 0;
+    uint32_t total;
+    const uint32_t ex = block_exclusive_scan_1024(v, &total, lds);
+    // tile prefixes can exceed 32 bits only for > 2^31 claims; kept 32-bit
+    if (t < ntiles) tsum[t] = (uint32_t)(run + ex);
+    __syncthreads();
+    if (threadIdx.x == 0) run += total;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    ctr->call_pos = ctr->log_count;
+    ctr->call_seq = ctr->seq_next;
+    ctr->log_count += run;
+    ctr->seq_next += run;
+  }
+}
+
+__global__ void __launch_bounds__(kThreads) k_write_events(const uint32_t* __restrict__ cnt,
+                                                           const Pend* __restrict__ pend,
+                                                           const uint64_t* __restrict__ ids,
+                                                           uint64_t C,
+                                                           const uint32_t* __restrict__ tprefix,
+                                                           const Counters* __restrict__ ctr,
+                                                           claim_event* __restrict__ log) {
+  __shared__ uint32_t lds[kThreads / 64 + 1];
+  constexpr int kPer = kTile / kThreads;
+  const uint64_t first = (uint64_t)blockIdx.x * kTile + threadIdx.x * kPer;
+  uint32_t v[kPer];
+  uint32_t sum = 0;
+  for (int k = 0; k < kPer; ++k) {
+    v[k] = first + k < C ? cnt[first + k] : 0;
+    sum += v[k];
+  }
+  // exclusive scan over the 256 threads
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t incl = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t up = lane_read(incl, lane >= (uint32_t)o ? lane - o : lane);
+    if (lane >= (uint32_t)o) incl += up;
+  }
+  if (lane == 63) lds[wave] = incl;
+  __syncthreads();
+  uint32_t wbase = 0;
+  for (uint32_t w = 0; w < wave; ++w) wbase += lds[w];
+  uint64_t pos = (uint64_t)tprefix[blockIdx.x] + wbase + incl - sum;
+  const uint64_t base_pos = ctr->call_pos, base_seq = ctr->call_seq;
+  for (int k = 0; k < kPer; ++k) {
+    const uint64_t c = first + k;
+    if (v[k] == 0) continue;
+    const Pend pe = pend[c];
+    for (uint32_t e = 0; e < v[k]; ++e) {
+      claim_event ev;
+      ev.seq = base_seq + pos;
+      ev.claim_id = ids[c];
+      ev.aux = e == 0 ? pe.aux0 : pe.aux1;
+      ev.kind = (pe.kinds >> (8 * e)) & 0xFFu;
+      ev.block_index = pe.j;
+      ev.phys_block = pe.phys;
+      ev.reserved = 0;
+      log[base_pos + pos] = ev;
+      ++pos;
+    }
+  }
+}
+
+// --------------------------------------------------------------- host side
+
+const int kTimingSlots = 64;
+const int kStages = 6;  // start, selected, digested, finalized, claims, events
+
+}  // namespace
+
+struct claim_pool {
+  int device = 0;
+  hipStream_t stream = nullptr;
+  uint32_t flags = 0;
+  uint32_t cus = 256;
+
+  uint32_t planes = 0, bs = 0, nb = 0;
+  uint64_t chunk_bytes = 0, chunk_vecs = 0, block_bytes = 0, seed = 0;
+  void* kv = nullptr;
+
+  int lpt = 8;
+  uint32_t segs = 1, ps_total = 1, groups = 1;
+
+  uint64_t *d_off = nullptr, *d_res = nullptr, *partial = nullptr;
+  uint8_t *valid_off = nullptr, *load_failed = nullptr, *mark = nullptr;
+  uint32_t *uniq = nullptr, *slot_of = nullptr;
+
+  uint64_t reg_mask = 0, max_claims = 0;
+  uint64_t *r_key = nullptr, *r_ntok = nullptr, *r_chain = nullptr, *r_fpoff = nullptr;
+  uint32_t *r_state = nullptr, *r_nblk = nullptr;
+  uint32_t* fp_store = nullptr;
+  uint64_t max_fp = 0, fp_used = 0;
+  uint64_t staged_blocks = 0;  // blocks written by the last staged offload
+  uint64_t reg_used_ub = 0;  // upper bound on registered claims
+
+  claim_event* log = nullptr;
+  uint64_t ev_cap = 0, log_ub = 0;
+
+  Counters* ctr = nullptr;
+  Counters* host_ctr = nullptr;  // pinned
+
+  uint64_t scratch_claims = 0, outcome_cap = 0;
+  claim_outcome* outcomes = nullptr;
+  uint32_t* cnt = nullptr;
+  Pend* pend = nullptr;
+  uint32_t* tsum = nullptr;
+  unsigned long long* dup_table = nullptr;
+  uint64_t dup_cap = 0;
+  uint64_t last_check_claims = 0;
+  bool have_outcomes = false;
+
+  uint32_t* f_blocks = nullptr;
+  uint64_t* f_bits = nullptr;
+  uint64_t f_cap = 0;
+
+  hipEvent_t tev[kTimingSlots][kStages];
+  bool tev_made = false;
+  int t_head = 0, t_count = 0;  // ring of recorded checks not yet read
+  claim_timing t_acc;
+};
+
+namespace {
+
+int hip_status(hipError_t e) { return e == hipSuccess ? CLAIM_OK : CLAIM_EHIP; }
+
+#define HIP_TRY(expr)                         \
+  do {                                        \
+    hipError_t e_ = (expr);                   \
+    if (e_ != hipSuccess) return CLAIM_EHIP;  \
+  } while (0)
+
+#define TRY(expr)                \
+  do {                           \
+    int s_ = (expr);             \
+    if (s_ != CLAIM_OK) return s_; \
+  } while (0)
+
+void dfree(void* p) {
+  if (p) (void)hipFree(p);
+}
+
+template <typename T>
+int dalloc(T** p, uint64_t count) {
+  *p = nullptr;
+  if (count == 0) count = 1;
+  hipError_t e = hipMalloc((void**)p, count * sizeof(T));
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return CLAIM_ENOMEM;
+  }
+  return CLAIM_OK;
+}
+
+uint32_t grid_for(uint64_t threads, uint32_t cap = 1u << 20) {
+  uint64_t g = (threads + kThreads - 1) / kThreads;
+  if (g == 0) g = 1;
+  return (uint32_t)(g < cap ? g : cap);
+}
+
+template <typename T>
+int fill(claim_pool* P, T* p, uint64_t n, T v) {
+  if (n == 0) return CLAIM_OK;
+  hipLaunchKernelGGL(k_fill<T>, dim3(grid_for(n, 4096)), dim3(kThreads), 0, P->stream, p, n, v);
+  return hip_status(hipGetLastError());
+}
+
+uint64_t next_pow2(uint64_t x) {
+  uint64_t p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+// Group width for one claim per group: the mean row length, rounded up to a
+// power of two in [2, 64].
+int group_width(const claim_batch* b) {
+  const uint64_t mean = b->num_claims ? (b->num_refs + b->num_claims - 1) / b->num_claims : 1;
+  int w = 2;
+  while (w < 64 && (uint64_t)w < mean) w <<= 1;
+  return w;
+}
+
+BatchDev batch_dev(const claim_batch* b) {
+  BatchDev d;
+  d.C = b->num_claims;
+  d.N = b->num_refs;
+  d.T = b->num_tokens;
+  d.ids = b->claim_ids;
+  d.bo = b->block_offsets;
+  d.bi = b->block_ids;
+  d.to = b->token_offsets;
+  d.tok = b->tokens;
+  return d;
+}
+
+RegDev reg_dev(claim_pool* P) {
+  RegDev r;
+  r.mask = P->reg_mask;
+  r.key = P->r_key;
+  r.state = P->r_state;
+  r.nblk = P->r_nblk;
+  r.ntok = P->r_ntok;
+  r.chain = P->r_chain;
+  r.fpoff = P->r_fpoff;
+  r.fp = P->fp_store;
+  return r;
+}
+
+int check_batch(const claim_pool* P, const claim_batch* b) {
+  if (!b || b->reserved != 0) return CLAIM_EINVAL;
+  if (b->num_refs >= (uint64_t)kNone || b->num_claims > 0x7FFFFFFFu) return CLAIM_EINVAL;
+  if (b->num_claims > 0 && (!b->claim_ids || !b->block_offsets || !b->token_offsets))
+    return CLAIM_EINVAL;
+  if (b->num_refs > 0 && !b->block_ids) return CLAIM_EINVAL;
+  if (b->num_tokens > 0 && !b->tokens) return CLAIM_EINVAL;
+  (void)P;
+  return CLAIM_OK;
+}
+
+int ensure_claim_scratch(claim_pool* P, uint64_t C, bool for_check) {
+  if (for_check && C > P->outcome_cap) {
+    HIP_TRY(hipStreamSynchronize(P->stream));
+    dfree(P->outcomes);
+    P->outcomes = nullptr;
+    P->outcome_cap = 0;
+    P->have_outcomes = false;
+    const uint64_t cap = C < 1024 ? 1024 : C;
+    TRY(dalloc(&P->outcomes, cap));
+    P->outcome_cap = cap;
+  }
+  if (C <= P->scratch_claims) return CLAIM_OK;
+  HIP_TRY(hipStreamSynchronize(P->stream));
+  dfree(P->cnt);
+  dfree(P->pend);
+  dfree(P->tsum);
+  dfree(P->dup_table);
+  P->cnt = nullptr;
+  P->pend = nullptr;
+  P->tsum = nullptr;
+  P->dup_table = nullptr;
+  P->scratch_claims = 0;
+  const uint64_t cap = C < 1024 ? 1024 : C;
+  TRY(dalloc(&P->cnt, cap));
+  TRY(dalloc(&P->pend, cap));
+  TRY(dalloc(&P->tsum, (cap + kTile - 1) / kTile));
+  P->dup_cap = next_pow2(2 * cap);
+  TRY(dalloc(&P->dup_table, P->dup_cap));
+  P->scratch_claims = cap;
+  return CLAIM_OK;
+}
+
+// Mark + compact the blocks referenced by the batch into P->uniq.
+int select_blocks(claim_pool* P, const claim_batch* b, int mode) {
+  if (b->num_claims) {
+    const BatchDev bd = batch_dev(b);
+    const int W = group_width(b);
+    const uint32_t grid = grid_for((uint64_t)b->num_claims * W, 0x7FFFFFFFu);
+    switch (W) {
+#define MARK_CASE(w)                                                                          \
+  case w:                                                                                     \
+    hipLaunchKernelGGL(k_mark<w>, dim3(grid), dim3(kThreads), 0, P->stream, bd, P->nb, mode, \
+                       P->valid_off, P->slot_of, P->mark);                                    \
+    break;
+      MARK_CASE(2)
+      MARK_CASE(4)
+      MARK_CASE(8)
+      MARK_CASE(16)
+      MARK_CASE(32)
+      MARK_CASE(64)
+#undef MARK_CASE
+      default:
+        return CLAIM_EINVAL;
+    }
+    HIP_TRY(hipGetLastError());
+  }
+  hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, P->stream, P->mark, P->nb, P->uniq, P->ctr);
+  return hip_status(hipGetLastError());
+}
+
+int launch_digest(claim_pool* P, uint64_t* partial, void* staging) {
+  const uint64_t waves = (uint64_t)P->ps_total * P->groups;
+  const uint32_t grid = (uint32_t)((waves + kThreads / 64 - 1) / (kThreads / 64));
+  const u32x4* pool = (const u32x4*)P->kv;
+  u32x4* st = (u32x4*)staging;
+  switch (P->lpt) {
+#define DIGEST_CASE(l)                                                                           \
+  case l:                                                                                        \
+    hipLaunchKernelGGL(k_digest<l>, dim3(grid), dim3(kThreads), 0, P->stream, pool, P->nb,       \
+                       (uint32_t)P->chunk_vecs, P->planes, P->segs, P->groups, P->uniq, P->ctr, \
+                       P->seed, partial, st);                                                    \
+    break;
+    DIGEST_CASE(1)
+    DIGEST_CASE(2)
+    DIGEST_CASE(3)
+    DIGEST_CASE(4)
+    DIGEST_CASE(5)
+    DIGEST_CASE(6)
+    DIGEST_CASE(7)
+    DIGEST_CASE(8)
+    DIGEST_CASE(9)
+    DIGEST_CASE(10)
+    DIGEST_CASE(11)
+    DIGEST_CASE(12)
+#undef DIGEST_CASE
+    default:
+      return CLAIM_EINVAL;
+  }
+  return hip_status(hipGetLastError());
+}
+
+int launch_finalize(claim_pool* P, int mode, int staged) {
+  const uint32_t grid = P->nb / (kThreads / 64) + 1 < 8192 ? P->nb / (kThreads / 64) + 1 : 8192;
+  hipLaunchKernelGGL(k_finalize, dim3(grid), dim3(kThreads), 0, P->stream, P->uniq, P->ctr,
+                     P->partial, P->ps_total, mode, staged, mode == 0 ? P->d_off : P->d_res,
+                     P->valid_off, P->load_failed, P->slot_of);
+  return hip_status(hipGetLastError());
+}
+
+// Scan the per-claim event counts and append the events.
+int append_events(claim_pool* P, const claim_batch* b) {
+  const uint64_t C = b->num_claims;
+  if (C == 0) return CLAIM_OK;
+  const uint64_t ntiles = (C + kTile - 1) / kTile;
+  hipLaunchKernelGGL(k_tile_sums, dim3((uint32_t)ntiles), dim3(kThreads), 0, P->stream, P->cnt, C,
+                     P->tsum);
+  HIP_TRY(hipGetLastError());
+  hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, P->stream, P->tsum, ntiles, P->ctr);
+  HIP_TRY(hipGetLastError());
+  hipLaunchKernelGGL(k_write_events, dim3((uint32_t)ntiles), dim3(kThreads), 0, P->stream, P->cnt,
+                     P->pend, b->claim_ids, C, P->tsum, P->ctr, P->log);
+  return hip_status(hipGetLastError());
+}
+
+// Launch a claim-group kernel for the batch's group width.
+#define LAUNCH_GROUPED(KERNEL, P, b, ...)                                                       \
+  do {                                                                                          \
+    const int W_ = group_width(b);                                                              \
+    const uint32_t grid_ = grid_for((uint64_t)(b)->num_claims * W_, 0x7FFFFFFFu);               \
+    switch (W_) {                                                                               \
+      case 2:                                                                                   \
+        hipLaunchKernelGGL(KERNEL<2>, dim3(grid_), dim3(kThreads), 0, (P)->stream, __VA_ARGS__); \
+        break;                                                                                  \
+      case 4:                                                                                   \
+        hipLaunchKernelGGL(KERNEL<4>, dim3(grid_), dim3(kThreads), 0, (P)->stream, __VA_ARGS__); \
+        break;                                                                                  \
+      case 8:                                                                                   \
+        hipLaunchKernelGGL(KERNEL<8>, dim3(grid_), dim3(kThreads), 0, (P)->stream, __VA_ARGS__); \
+        break;                                                                                  \
+      case 16:                                                                                  \
+        hipLaunchKernelGGL(KERNEL<16>, dim3(grid_), dim3(kThreads), 0, (P)->stream, __VA_ARGS__); \
+        break;                                                                                  \
+      case 32:                                                                                  \
+        hipLaunchKernelGGL(KERNEL<32>, dim3(grid_), dim3(kThreads), 0, (P)->stream, __VA_ARGS__); \
+        break;                                                                                  \
+      default:                                                                                  \
+        hipLaunchKernelGGL(KERNEL<64>, dim3(grid_), dim3(kThreads), 0, (P)->stream, __VA_ARGS__); \
+        break;                                                                                  \
+    }                                                                                           \
+    HIP_TRY(hipGetLastError());                                                                 \
+  } while (0)
+
+// Choose vectors per lane (LPT) and segments per chunk for the digest.
+void choose_digest_shape(claim_pool* P) {
+  const uint64_t V = P->chunk_vecs;
+  const uint64_t Q = (V + 63) / 64;  // vectors per lane to cover one chunk
+  // Prefer a divisor of Q in [4, 12] closest to 8 (ties: the larger), so
+  // every segment is full; otherwise 8 per lane with a ragged last segment.
+  int best = 0, best_dist = 1 << 30;
+  if (V % 64 == 0) {
+    for (int d = 4; d <= 12; ++d) {
+      const int dist = d > 8 ? d - 8 : 8 - d;
+      if (Q % d == 0 && (dist < best_dist || (dist == best_dist && d > best))) {
+        best = d;
+        best_dist = dist;
+      }
+    }
+  }
+  if (best == 0) best = Q < 8 ? (int)Q : 8;
+  P->lpt = best;
+  P->segs = (uint32_t)((Q + best - 1) / best);
+  P->ps_total = P->planes * P->segs;
+  // enough waves to keep every CU's SIMDs busy (about 24 waves per CU)
+  const uint64_t target = (uint64_t)P->cus * 24;
+  uint64_t g = target / P->ps_total;
+  if (g < 1) g = 1;
+  if (g > P->nb) g = P->nb;
+  P->groups = (uint32_t)g;
+}
+
+void free_pool(claim_pool* P) {
+  if (!P) return;
+  void* ptrs[] = {P->d_off,    P->d_res,     P->partial,  P->valid_off, P->load_failed,
+                  P->mark,     P->uniq,      P->slot_of,  P->r_key,     P->r_ntok,
+                  P->r_chain,  P->r_fpoff,   P->r_state,  P->r_nblk,    P->fp_store,
+                  P->log,      P->ctr,       P->outcomes, P->cnt,       P->pend,
+                  P->tsum,     P->dup_table, P->f_blocks, P->f_bits};
+  for (void* p : ptrs)
+    if (p) dfree(p);
+  if (P->host_ctr) (void)hipHostFree(P->host_ctr);
+  if (P->tev_made)
+    for (int i = 0; i < kTimingSlots; ++i)
+      for (int s = 0; s < kStages; ++s) (void)hipEventDestroy(P->tev[i][s]);
+  delete P;
+}
+
+int read_counters(claim_pool* P) {
+  HIP_TRY(hipMemcpyAsync(P->host_ctr, P->ctr, sizeof(Counters), hipMemcpyDeviceToHost, P->stream));
+  HIP_TRY(hipStreamSynchronize(P->stream));
+  return CLAIM_OK;
+}
+
+// Fold the oldest recorded check's stage times into the accumulator.
+int fold_timing_slot(claim_pool* P) {
+  const int i = (P->t_head - P->t_count + kTimingSlots) % kTimingSlots;
+  HIP_TRY(hipEventSynchronize(P->tev[i][kStages - 1]));
+  float ms[kStages - 1];
+  for (int s = 0; s + 1 < kStages; ++s) HIP_TRY(hipEventElapsedTime(&ms[s], P->tev[i][s], P->tev[i][s + 1]));
+  P->t_acc.calls += 1;
+  P->t_acc.select_ms += ms[0];
+  P->t_acc.digest_ms += ms[1];
+  P->t_acc.finalize_ms += ms[2];
+  P->t_acc.claims_ms += ms[3];
+  P->t_acc.events_ms += ms[4];
+  P->t_acc.total_ms += ms[0] + ms[1] + ms[2] + ms[3] + ms[4];
+  P->t_count -= 1;
+  return CLAIM_OK;
+}
+
+int record_stage(claim_pool* P, int slot, int stage) {
+  if (!(P->flags & CLAIM_POOL_TIMING)) return CLAIM_OK;
+  return hip_status(hipEventRecord(P->tev[slot][stage], P->stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* claim_strerror(int status) {
+  switch (status) {
+    case CLAIM_OK: return "ok";
+    case CLAIM_EINVAL: return "invalid argument, layout or size";
+    case CLAIM_ENOMEM: return "device allocation failed";
+    case CLAIM_EHIP: return "HIP runtime error";
+    case CLAIM_ENOSPC: return "capacity exceeded (registry, footprint, event log, staging or output)";
+    case CLAIM_EDUP: return "duplicate claim id: acceptance refused";
+    default: return "unknown status";
+  }
+}
+
+int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
+  if (!d || !out) return CLAIM_EINVAL;
+  *out = nullptr;
+  if (d->num_layers == 0 || (d->planes_per_layer != 1 && d->planes_per_layer != 2) ||
+      d->block_size == 0 || d->block_size > kMaxBlockSize || d->num_kv_heads == 0 ||
+      d->head_dim == 0 || d->elem_bytes == 0 || d->num_blocks == 0 || d->num_blocks >= kNone ||
+      !d->kv_base || ((uintptr_t)d->kv_base & 15) || d->max_claims == 0 ||
+      d->event_capacity == 0 || (d->flags & ~CLAIM_POOL_TIMING))
+    return CLAIM_EINVAL;
+  const uint64_t planes = (uint64_t)d->num_layers * d->planes_per_layer;
+  const uint64_t chunk = (uint64_t)d->block_size * d->num_kv_heads * d->head_dim * d->elem_bytes;
+  if (chunk % 16 || planes > 0xFFFFFFFFull || chunk / 16 > 0xFFFFFFFFull) return CLAIM_EINVAL;
+  if (d->max_claims > (1ull << 40) || d->max_footprint > (1ull << 40)) return CLAIM_EINVAL;
+  const long double need = (long double)planes * d->num_blocks * chunk;
+  if (need > (long double)d->kv_bytes) return CLAIM_EINVAL;
+
+  claim_pool* P = new (std::nothrow) claim_pool();
+  if (!P) return CLAIM_ENOMEM;
+  memset(&P->t_acc, 0, sizeof(P->t_acc));
+  int rc = CLAIM_OK;
+  do {
+    if (hipGetDevice(&P->device) != hipSuccess) { rc = CLAIM_EHIP; break; }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, P->device) != hipSuccess) {
+      rc = CLAIM_EHIP;
+      break;
+    }
+    P->cus = cus > 0 ? (uint32_t)cus : 256;
+    P->stream = (hipStream_t)d->stream;
+    P->flags = d->flags;
+    P->planes = (uint32_t)planes;
+    P->bs = d->block_size;
+    P->nb = d->num_blocks;
+    P->chunk_bytes = chunk;
+    P->chunk_vecs = chunk / 16;
+    P->block_bytes = planes * chunk;
+    P->seed = d->seed;
+    P->kv = d->kv_base;
+    choose_digest_shape(P);
+
+    const uint64_t nb = d->num_blocks;
+    if ((rc = dalloc(&P->d_off, nb)) || (rc = dalloc(&P->d_res, nb)) ||
+        (rc = dalloc(&P->partial, nb * P->ps_total)) || (rc = dalloc(&P->valid_off, nb)) ||
+        (rc = dalloc(&P->load_failed, nb)) || (rc = dalloc(&P->mark, nb)) ||
+        (rc = dalloc(&P->uniq, nb)) || (rc = dalloc(&P->slot_of, nb)))
+      break;
+    P->max_claims = d->max_claims;
+    const uint64_t cap = next_pow2(2 * d->max_claims);
+    P->reg_mask = cap - 1;
+    if ((rc = dalloc(&P->r_key, cap)) || (rc = dalloc(&P->r_ntok, cap)) ||
+        (rc = dalloc(&P->r_chain, cap)) || (rc = dalloc(&P->r_fpoff, cap)) ||
+        (rc = dalloc(&P->r_state, cap)) || (rc = dalloc(&P->r_nblk, cap)))
+      break;
+    P->max_fp = d->max_footprint;
+    if ((rc = dalloc(&P->fp_store, d->max_footprint))) break;
+    P->ev_cap = d->event_capacity;
+    if ((rc = dalloc(&P->log, d->event_capacity))) break;
+    if ((rc = dalloc(&P->ctr, 1))) break;
+    if (hipHostMalloc((void**)&P->host_ctr, sizeof(Counters), hipHostMallocDefault) != hipSuccess) {
+      P->host_ctr = nullptr;
+      rc = CLAIM_ENOMEM;
+      break;
+    }
+    if (P->flags & CLAIM_POOL_TIMING) {
+      bool ok = true;
+      for (int i = 0; i < kTimingSlots && ok; ++i)
+        for (int s = 0; s < kStages && ok; ++s) ok = hipEventCreate(&P->tev[i][s]) == hipSuccess;
+      if (!ok) { rc = CLAIM_EHIP; break; }
+      P->tev_made = true;
+    }
+    if ((rc = fill<uint64_t>(P, P->d_off, nb, 0)) || (rc = fill<uint64_t>(P, P->d_res, nb, 0)) ||
+        (rc = fill<uint8_t>(P, P->valid_off, nb, 0)) || (rc = fill<uint8_t>(P, P->load_failed, nb, 0)) ||
+        (rc = fill<uint8_t>(P, P->mark, nb, 0)) || (rc = fill<uint32_t>(P, P->slot_of, nb, kNone)) ||
+        (rc = fill<uint64_t>(P, P->r_key, cap, kEmptyId)) || (rc = fill<uint32_t>(P, P->r_state, cap, 0)))
+      break;
+    if ((rc = fill<uint64_t>(P, (uint64_t*)P->ctr, sizeof(Counters) / 8, 0))) break;
+    if (hipStreamSynchronize(P->stream) != hipSuccess) { rc = CLAIM_EHIP; break; }
+  } while (0);
+  if (rc != CLAIM_OK) {
+    free_pool(P);
+    return rc;
+  }
+  *out = P;
+  return CLAIM_OK;
+}
+
+int claim_pool_destroy(claim_pool* P) {
+  if (!P) return CLAIM_OK;
+  (void)hipSetDevice(P->device);
+  hipError_t e = hipStreamSynchronize(P->stream);
+  free_pool(P);
+  return hip_status(e);
+}
+
+int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t staging_bytes) {
+  if (!P || ((uintptr_t)staging & 15)) return CLAIM_EINVAL;
+  TRY(check_batch(P, b));
+  HIP_TRY(hipSetDevice(P->device));
+  const uint64_t C = b->num_claims;
+  if (P->reg_used_ub + C > P->max_claims || P->fp_used + b->num_refs > P->max_fp ||
+      P->log_ub + 2 * C > P->ev_cap)
+    return CLAIM_ENOSPC;
+  TRY(ensure_claim_scratch(P, C, false));
+
+  // verdict: duplicates and the staged size, before any state changes
+  TRY(fill<uint32_t>(P, &P->ctr->dup_flag, 1, 0u));
+  const BatchDev bd = batch_dev(b);
+  const RegDev rd = reg_dev(P);
+  if (C) {
+    TRY(fill<unsigned long long>(P, P->dup_table, P->dup_cap, (unsigned long long)kEmptyId));
+    hipLaunchKernelGGL(k_dupcheck, dim3(grid_for(C, 0x7FFFFFFFu)), dim3(kThreads), 0, P->stream, bd,
+                       rd, P->dup_table, P->dup_cap - 1, P->ctr);
+    HIP_TRY(hipGetLastError());
+  }
+  TRY(select_blocks(P, b, kMarkAny));
+  TRY(read_counters(P));
+  if (P->host_ctr->dup_flag) return CLAIM_EDUP;
+  const uint64_t U = P->host_ctr->uniq_count;
+  if (staging && staging_bytes < U * P->block_bytes) return CLAIM_ENOSPC;  // nothing changed
+
+  // acceptance
+  if (C) {
+    hipLaunchKernelGGL(k_copy_u32, dim3(grid_for(b->num_refs, 4096)), dim3(kThreads), 0, P->stream,
+                       P->fp_store + P->fp_used, b->block_ids, b->num_refs);
+    HIP_TRY(hipGetLastError());
+    LAUNCH_GROUPED(k_accept, P, b, bd, rd, P->nb, P->bs, P->seed, P->fp_used, P->ctr, P->cnt, P->pend);
+    TRY(append_events(P, b));
+  }
+  // offload record; a staged offload replaces every earlier staging slot
+  if (staging) TRY(fill<uint32_t>(P, P->slot_of, P->nb, kNone));
+  TRY(launch_digest(P, P->partial, staging));
+  TRY(launch_finalize(P, 0, staging != nullptr));
+  TRY(read_counters(P));
+  P->fp_used += b->num_refs;
+  if (staging) P->staged_blocks = U;
+  P->reg_used_ub = P->host_ctr->reg_count;
+  P->log_ub = P->host_ctr->log_count;
+  return CLAIM_OK;
+}
+
+int claim_restore(claim_pool* P, const claim_batch* b, const void* staging,
+                  uint64_t staging_bytes, const claim_fault_spec* f) {
+  if (!P || ((uintptr_t)staging & 15)) return CLAIM_EINVAL;
+  if (staging && staging_bytes < P->staged_blocks * P->block_bytes) return CLAIM_EINVAL;
+  TRY(check_batch(P, b));
+  HIP_TRY(hipSetDevice(P->device));
+  const uint64_t C = b->num_claims;
+  uint32_t nflip = 0, nfail = 0;
+  if (f) {
+    nflip = f->num_flips;
+    nfail = f->num_load_failed;
+    if ((nflip && (!f->flip_blocks || !f->flip_bits)) || (nfail && !f->load_failed_blocks))
+      return CLAIM_EINVAL;
+    for (uint32_t i = 0; i < nflip; ++i)
+      if (f->flip_blocks[i] >= P->nb || f->flip_bits[i] >= 8 * P->block_bytes) return CLAIM_EINVAL;
+    for (uint32_t i = 0; i < nfail; ++i)
+      if (f->load_failed_blocks[i] >= P->nb) return CLAIM_EINVAL;
+  }
+  if (P->log_ub + C > P->ev_cap) return CLAIM_ENOSPC;
+  TRY(ensure_claim_scratch(P, C, false));
+
+  if (staging) {
+    TRY(select_blocks(P, b, kMarkStaged));
+    hipLaunchKernelGGL(k_unstage, dim3(grid_for((uint64_t)P->nb * P->planes * P->chunk_vecs, 65536)),
+                       dim3(kThreads), 0, P->stream, (u32x4*)P->kv, P->nb, (uint32_t)P->chunk_vecs,
+                       P->planes, P->uniq, P->ctr, P->slot_of, (const u32x4*)staging);
+    HIP_TRY(hipGetLastError());
+  }
+  const uint64_t need = nflip > nfail ? nflip : nfail;
+  if (need > P->f_cap) {
+    HIP_TRY(hipStreamSynchronize(P->stream));
+    dfree(P->f_blocks);
+    dfree(P->f_bits);
+    P->f_blocks = nullptr;
+    P->f_bits = nullptr;
+    P->f_cap = 0;
+    TRY(dalloc(&P->f_blocks, need));
+    TRY(dalloc(&P->f_bits, need));
+    P->f_cap = need;
+  }
+  if (nflip) {
+    HIP_TRY(hipMemcpyAsync(P->f_blocks, f->flip_blocks, nflip * sizeof(uint32_t),
+                           hipMemcpyHostToDevice, P->stream));
+    HIP_TRY(hipMemcpyAsync(P->f_bits, f->flip_bits, nflip * sizeof(uint64_t), hipMemcpyHostToDevice,
+                           P->stream));
+    hipLaunchKernelGGL(k_flips, dim3(grid_for(nflip)), dim3(kThreads), 0, P->stream,
+                       (uint32_t*)P->kv, P->nb, P->chunk_bytes, nflip, P->f_blocks, P->f_bits);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipStreamSynchronize(P->stream));  // the fault lists may be reused next
+  }
+  if (nfail) {
+    HIP_TRY(hipMemcpyAsync(P->f_blocks, f->load_failed_blocks, nfail * sizeof(uint32_t),
+                           hipMemcpyHostToDevice, P->stream));
+    hipLaunchKernelGGL(k_set_failed, dim3(grid_for(nfail)), dim3(kThreads), 0, P->stream,
+                       P->load_failed, nfail, P->f_blocks);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipStreamSynchronize(P->stream));
+  }
+  if (C) {
+    hipLaunchKernelGGL(k_restore_claims, dim3(grid_for(C, 0x7FFFFFFFu)), dim3(kThreads), 0,
+                       P->stream, batch_dev(b), reg_dev(P), P->cnt, P->pend);
+    HIP_TRY(hipGetLastError());
+    TRY(append_events(P, b));
+  }
+  P->log_ub += C;
+  return CLAIM_OK;
+}
+
+int claim_check(claim_pool* P, const claim_batch* b) {
+  if (!P) return CLAIM_EINVAL;
+  TRY(check_batch(P, b));
+  HIP_TRY(hipSetDevice(P->device));
+  const uint64_t C = b->num_claims;
+  if (P->log_ub + 2 * C > P->ev_cap) return CLAIM_ENOSPC;
+  TRY(ensure_claim_scratch(P, C, true));
+
+  int slot = 0;
+  if (P->flags & CLAIM_POOL_TIMING) {
+    if (P->t_count == kTimingSlots) TRY(fold_timing_slot(P));
+    slot = P->t_head;
+  }
+  TRY(record_stage(P, slot, 0));
+  TRY(select_blocks(P, b, kMarkOffloaded));
+  TRY(record_stage(P, slot, 1));
+  TRY(launch_digest(P, P->partial, nullptr));
+  TRY(record_stage(P, slot, 2));
+  TRY(launch_finalize(P, 1, 0));
+  TRY(record_stage(P, slot, 3));
+  if (C) {
+    CheckState st;
+    st.d_off = P->d_off;
+    st.d_res = P->d_res;
+    st.valid_off = P->valid_off;
+    st.load_failed = P->load_failed;
+    LAUNCH_GROUPED(k_check, P, b, batch_dev(b), reg_dev(P), st, P->nb, P->bs, P->seed, P->outcomes,
+                   P->cnt, P->pend);
+  }
+  TRY(record_stage(P, slot, 4));
+  TRY(append_events(P, b));
+  TRY(record_stage(P, slot, 5));
+  if (P->flags & CLAIM_POOL_TIMING) {
+    P->t_head = (P->t_head + 1) % kTimingSlots;
+    P->t_count += 1;
+  }
+  P->last_check_claims = C;
+  P->have_outcomes = true;
+  P->log_ub += 2 * C;
+  return CLAIM_OK;
+}
+
+int outcomes_read(claim_pool* P, claim_outcome* out, uint32_t out_cap, uint32_t* num_out,
+                  claim_event* events, uint64_t ev_cap, uint64_t* num_events) {
+  if (!P) return CLAIM_EINVAL;
+  HIP_TRY(hipSetDevice(P->device));
+  TRY(read_counters(P));
+  const uint64_t nev = P->host_ctr->log_count;
+  const uint64_t nout = P->have_outcomes ? P->last_check_claims : 0;
+  if ((out && nout > out_cap) || (events && nev > ev_cap)) return CLAIM_ENOSPC;
+  if (out) {
+    if (nout) HIP_TRY(hipMemcpy(out, P->outcomes, nout * sizeof(claim_outcome), hipMemcpyDeviceToHost));
+    if (num_out) *num_out = (uint32_t)nout;
+  }
+  if (events) {
+    if (nev) HIP_TRY(hipMemcpy(events, P->log, nev * sizeof(claim_event), hipMemcpyDeviceToHost));
+    if (num_events) *num_events = nev;
+    P->host_ctr->log_count = 0;
+    HIP_TRY(hipMemcpyAsync(&P->ctr->log_count, &P->host_ctr->log_count, sizeof(uint64_t),
+                           hipMemcpyHostToDevice, P->stream));
+    HIP_TRY(hipStreamSynchronize(P->stream));
+    P->log_ub = 0;
+  } else {
+    P->log_ub = nev;
+  }
+  return CLAIM_OK;
+}
+
+int claim_block_state_read(claim_pool* P, uint32_t first, uint32_t count, uint64_t* d_off,
+                           uint64_t* d_res, uint8_t* valid_off, uint8_t* load_failed) {
+  if (!P || (uint64_t)first + count > P->nb) return CLAIM_EINVAL;
+  HIP_TRY(hipSetDevice(P->device));
+  HIP_TRY(hipStreamSynchronize(P->stream));
+  if (count == 0) return CLAIM_OK;
+  if (d_off) HIP_TRY(hipMemcpy(d_off, P->d_off + first, count * 8ull, hipMemcpyDeviceToHost));
+  if (d_res) HIP_TRY(hipMemcpy(d_res, P->d_res + first, count * 8ull, hipMemcpyDeviceToHost));
+  if (valid_off) HIP_TRY(hipMemcpy(valid_off, P->valid_off + first, count, hipMemcpyDeviceToHost));
+  if (load_failed)
+    HIP_TRY(hipMemcpy(load_failed, P->load_failed + first, count, hipMemcpyDeviceToHost));
+  return CLAIM_OK;
+}
+
+int claim_timing_read(claim_pool* P, claim_timing* out) {
+  if (!P || !out || !(P->flags & CLAIM_POOL_TIMING)) return CLAIM_EINVAL;
+  HIP_TRY(hipSetDevice(P->device));
+  while (P->t_count > 0) TRY(fold_timing_slot(P));
+  TRY(read_counters(P));
+  *out = P->t_acc;
+  out->last_unique = P->host_ctr->uniq_count;
+  memset(&P->t_acc, 0, sizeof(P->t_acc));
+  return CLAIM_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,466 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle.
+
+Every comparison is exact: outcomes, events, offload / restored digests and
+first-failing-block indices are integers and must match bit for bit.
+
+* scaled workloads (real digests of every block on both sides, several
+  digest tiles, ragged chunks and ragged claim tails);
+* the paper's lifecycle controls, replayed step by step on both sides;
+* the staged offload / restore round trip (device and pinned host staging);
+* the full-size workloads in the benchmark's launch configuration: all
+  outcomes and events, with real oracle digests for every block whose
+  bytes change, every reported failure and a random sample of blocks (the
+  other blocks keep their bytes, so their two digests are equal; the test
+  checks that on the GPU for every referenced block).
+"""
+
+from __future__ import annotations
+
+import gc
+import sys
+from dataclasses import replace
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2606_01387_amd.synth import (FULL, MISSING, TINY, FaultSpec, Geometry, Workload, content,
+                                        from_claims, make_batch, make_faults, scaled)
+from tests.helpers import apply_flips, digests, modeled_digests
+
+pytestmark = pytest.mark.gpu
+
+OUT_FIELDS = [n for n in O.OUTCOME_DTYPE.names if n != "pad"]
+EV_FIELDS = [n for n in O.EVENT_DTYPE.names if n != "pad"]
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    return t
+
+
+@pytest.fixture(scope="module")
+def ck():
+    from paper_2606_01387_amd import claimkv
+
+    claimkv.lib()
+    return claimkv
+
+
+def note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def free_gpu(torch):
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def gpu_pool_tensor(torch, w: Workload):
+    g = w.geometry
+    kv = torch.empty(g.pool_bytes, dtype=torch.uint8, device="cuda")
+    content.fill_pool_gpu(kv.data_ptr(), kv.numel(), g, w.content_seed,
+                          torch.cuda.current_stream().cuda_stream)
+    return kv
+
+
+def same_outcomes(got, want):
+    assert len(got) == len(want)
+    for f in OUT_FIELDS:
+        if f == "reserved":
+            continue
+        if not np.array_equal(got[f], want[f]):
+            bad = np.flatnonzero(got[f] != want[f])[:5]
+            raise AssertionError(f"outcome field {f} differs at claims {bad.tolist()}: "
+                                 f"gpu {got[f][bad].tolist()} oracle {want[f][bad].tolist()}")
+
+
+def same_events(got, want):
+    assert len(got) == len(want), (len(got), len(want))
+    for f in EV_FIELDS:
+        if f == "reserved":
+            continue
+        if not np.array_equal(got[f], want[f]):
+            bad = np.flatnonzero(got[f] != want[f])[:5]
+            raise AssertionError(f"event field {f} differs at {bad.tolist()}: "
+                                 f"gpu {got[f][bad].tolist()} oracle {want[f][bad].tolist()}")
+
+
+def capacities(batch):
+    return dict(max_claims=max(64, 2 * batch.num_claims), max_footprint=max(256, 4 * batch.num_refs),
+                event_capacity=max(256, 8 * batch.num_claims))
+
+
+# --------------------------------------------------------------- fill parity
+
+
+@pytest.mark.parametrize("w", [TINY, scaled(FULL["llama3-8b"], 6, 4), scaled(FULL["mla-fp8"], 5, 4)],
+                         ids=lambda w: w.name)
+def test_gpu_fill_matches_host_generator(torch, w):
+    note(f"fill parity {w.name}")
+    kv = gpu_pool_tensor(torch, w)
+    got = kv.cpu().numpy()
+    want = content.pool_host(w.geometry, w.content_seed)
+    assert np.array_equal(got, want)
+
+
+# ------------------------------------------------- scaled workloads, real bytes
+
+RAGGED = Workload(
+    name="ragged-chunk", geometry=Geometry(3, 2, 16, 3, 40, 2, 37), seed=77, num_claims=300,
+    length=("blocks", 1, 3, True), sharing=("zipf", 1.2, 8), corrupt_rate=0.2, num_load_failed=2,
+    gen_seed=11, content_seed=12)  # 3840-byte chunks: not a multiple of 1 KiB
+TINY_CHUNK = Workload(
+    name="48-byte-chunk", geometry=Geometry(2, 1, 3, 1, 8, 2, 19), seed=5, num_claims=50,
+    length=("blocks", 1, 12, True), sharing=("fraction", 0.3), corrupt_rate=0.3, num_load_failed=1,
+    gen_seed=3, content_seed=4)
+LONG_CLAIMS = Workload(
+    name="long-claims", geometry=Geometry(4, 2, 16, 2, 64, 2, 50), seed=99, num_claims=12,
+    length=("blocks", 100, 300, True), sharing=("fraction", 0.5), corrupt_rate=0.1,
+    missing_claim_rate=0.25, num_load_failed=1, gen_seed=21, content_seed=22)
+
+SCALED = [
+    replace(TINY, num_load_failed=1),
+    scaled(FULL["llama3-8b"], 48, 60, corrupt_rate=0.1, num_load_failed=2),
+    scaled(FULL["llama3-70b"], 24, 40, corrupt_rate=0.1, missing_claim_rate=0.1, num_load_failed=1),
+    scaled(FULL["small-claim-stress"], 256, 30000, corrupt_rate=0.02, num_load_failed=3),
+    scaled(FULL["mla-fp8"], 40, 60, corrupt_rate=0.1, num_load_failed=1),
+    RAGGED,
+    TINY_CHUNK,
+    LONG_CLAIMS,
+]
+
+
+def run_both_real(torch, ck, w, batch, faults):
+    """Whole lifecycle on both sides with real digests of every block."""
+    g = w.geometry
+    kv = gpu_pool_tensor(torch, w)
+    db = ck.DeviceBatch(batch)
+    with ck.Pool(g, w.seed, kv, **capacities(batch)) as pool:
+        pool.offload(db)
+        pool.restore(db, faults=faults)
+        pool.check(db)
+        out, ev = pool.read()
+        st = pool.block_state()
+    host = content.pool_host(g, w.content_seed)
+    d0 = digests(host, w)
+    restored = apply_flips(host, w, faults)
+    d1 = digests(restored, w)
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    assert op.offload(batch, d0) == O.OK
+    assert op.restore(batch, faults.load_failed) == O.OK
+    want = op.check(batch, d1)
+    return out, ev, st, want, op.events(), op.block_state(), kv
+
+
+@pytest.mark.parametrize("w", SCALED, ids=lambda w: w.name)
+def test_parity_scaled_real_digests(torch, ck, w):
+    batch = make_batch(w)
+    faults = make_faults(w, batch)
+    note(f"scaled parity {w.name}: {batch.num_claims} claims, {batch.num_refs} refs, "
+         f"{w.geometry.num_blocks} blocks of {w.geometry.block_bytes} B, "
+         f"{faults.flip_blocks.size} flips, {faults.load_failed.size} load failures")
+    out, ev, st, want, want_ev, want_st, kv = run_both_real(torch, ck, w, batch, faults)
+    same_outcomes(out, want)
+    same_events(ev, want_ev)
+    for f in ("d_off", "d_res", "valid_off", "load_failed"):
+        assert np.array_equal(st[f], want_st[f]), f
+    # the restored pool holds exactly the flipped bytes
+    host = apply_flips(content.pool_host(w.geometry, w.content_seed), w, faults)
+    assert np.array_equal(kv.cpu().numpy(), host)
+    codes = np.bincount(out["code"], minlength=3)
+    note(f"  outcomes unknown/materialized/failed = {codes.tolist()}")
+    del kv
+    free_gpu(torch)
+
+
+# ------------------------------------------------------ paper controls, mirrored
+
+
+class Mirror:
+    """The same lifecycle steps on the GPU library and on the oracle (tiny
+    pool, real bytes on both sides)."""
+
+    def __init__(self, torch, ck, event_capacity=4096):
+        self.w = TINY
+        g = self.w.geometry
+        self.torch, self.ck = torch, ck
+        self.kv = gpu_pool_tensor(torch, self.w)
+        self.host = content.pool_host(g, self.w.content_seed)
+        self.pool = ck.Pool(g, self.w.seed, self.kv, max_claims=256, max_footprint=8192,
+                            event_capacity=event_capacity)
+        self.op = O.OraclePool(g.num_blocks, g.block_size, self.w.seed)
+
+    def offload(self, batch):
+        try:
+            self.pool.offload(self.ck.DeviceBatch(batch))
+            rc = self.ck.OK
+        except self.ck.ClaimError as e:
+            rc = e.status
+        want = self.op.offload(batch, digests(self.host, self.w))
+        assert rc == want, (rc, want)
+        return rc
+
+    def restore(self, batch, flips=(), load_failed=()):
+        f = FaultSpec(np.array([b for b, _ in flips], np.uint32),
+                      np.array([bit for _, bit in flips], np.uint64),
+                      np.array(load_failed, np.uint32))
+        self.pool.restore(self.ck.DeviceBatch(batch), faults=f)
+        self.host = apply_flips(self.host, self.w, f)
+        assert self.op.restore(batch, f.load_failed) == O.OK
+
+    def check(self, batch):
+        db = self.ck.DeviceBatch(batch)
+        self.pool.check(db)
+        want = self.op.check(batch, digests(self.host, self.w))
+        got, ev = self.pool.read()
+        same_outcomes(got, want)
+        same_events(ev, self.op.events(clear=True))
+        return got
+
+    def finish(self):
+        st = self.pool.block_state()
+        want = self.op.block_state()
+        for f in st:
+            assert np.array_equal(st[f], want[f]), f
+        self.pool.close()
+
+
+RNG = np.random.default_rng(77)
+
+
+def toks(nblocks, tail=16):
+    return RNG.integers(0, 32000, size=(nblocks - 1) * 16 + tail if nblocks else 0, dtype=np.uint32)
+
+
+def test_controls_mirrored(torch, ck):
+    note("controls mirrored on gpu and oracle")
+    m = Mirror(torch, ck)
+    ck_ = ck
+    # path A and B and C in one pool
+    tA, tB, tN = toks(3, 5), toks(4), toks(3)
+    a = from_claims([(0xA, [3, 9, 27], tA)])
+    b = from_claims([(0xB, [5, 6, 7, 8], tB), (0xD, [40, 41, 42], tN)])
+    m.offload(a)
+    m.offload(b)
+    m.restore(a)
+    m.restore(b, flips=[(41, 1234)], load_failed=[7])
+    out = m.check(from_claims([(0xA, [3, 9, 27], tA), (0xB, [5, 6, 7, 8], tB),
+                               (0xD, [40, 41, 42], tN)]))
+    assert out["code"].tolist() == [ck_.MATERIALIZED, ck_.RESTORE_FAILED_FAIL_CLOSED,
+                                    ck_.RESTORE_FAILED_FAIL_CLOSED]
+    # unclaimed failure, not accepted, reuse without restore, identity mismatch
+    m.restore(from_claims([]), flips=[(60, 7)], load_failed=[61])
+    c = from_claims([(0xC, [10, 11], toks(2))])
+    m.offload(c)
+    tk = toks(3)
+    e = from_claims([(0xE, [12, 13, 14], tk)])
+    m.offload(e)
+    m.restore(e)
+    m.check(from_claims([(0xF, [10, 11], c.claim(0)[2]),  # never accepted
+                         (0xC, [10, 11], c.claim(0)[2]),  # no restore
+                         (0xE, [12, 13, 14], np.where(np.arange(tk.size) == 20, tk + 1, tk)),
+                         (0xE, [12, 99 % 64, 14], tk),  # footprint mismatch
+                         (0xE, [12, 13], tk[:32]),
+                         (0xE, [12, 13, 14], tk)]))
+    # missing entries, empty and malformed rows, shared block
+    f = from_claims([(0x10, [20, MISSING, 21], toks(3)), (0x11, [], toks(0)),
+                     (0xFFFFFFFFFFFFFFFF, [22], toks(1)), (0x12, [23, 24], toks(3)),
+                     (0x13, [30, 31, 32], toks(3)), (0x14, [30, 31, 33], toks(3))])
+    m.offload(f)
+    m.restore(f, flips=[(31, 999)])
+    m.check(f)
+    # duplicates refuse acceptance on both sides
+    assert m.offload(from_claims([(0x20, [1], toks(1)), (0x20, [2], toks(1))])) == ck_.EDUP
+    assert m.offload(from_claims([(0x21, [1], toks(1)), (0xA, [2], toks(1))])) == ck_.EDUP
+    # the running example: 448 tokens = 28 blocks, failure in the 28th block
+    p = from_claims([(0x448, list(range(28, 56)), toks(28))])
+    m.offload(p)
+    m.restore(p, load_failed=[55])
+    out = m.check(p)
+    assert out[0]["first_failing_block"] == 27
+    # a later offload of a block clears its reported failure (fresh record)
+    q = from_claims([(0x449, [55], toks(1))])
+    m.offload(q)
+    m.restore(q)
+    assert m.check(q)[0]["code"] == ck_.MATERIALIZED
+    # malformed offsets in a device batch never fault and give UNKNOWN
+    bad = from_claims([(0x30, [1, 2], toks(2)), (0x31, [3], toks(1))])
+    bad.block_offsets[1] = 3
+    bad.block_offsets[2] = 2
+    m.offload(bad)
+    m.restore(bad)
+    m.check(bad)
+    # an empty batch on every call
+    empty = from_claims([])
+    m.offload(empty)
+    m.restore(empty)
+    m.check(empty)
+    m.finish()
+    del m
+    free_gpu(torch)
+
+
+def test_repeated_checks_append_events_in_order(torch, ck):
+    note("repeated checks")
+    m = Mirror(torch, ck)
+    w = TINY
+    batch = make_batch(w)
+    faults = make_faults(w, batch)
+    m.offload(batch)
+    m.restore(batch, flips=list(zip(faults.flip_blocks.tolist(), faults.flip_bits.tolist())))
+    first = m.check(batch)
+    for _ in range(3):
+        again = m.check(batch)
+        assert np.array_equal(first, again)  # deterministic
+    m.finish()
+    free_gpu(torch)
+
+
+def test_capacity_errors(torch, ck):
+    note("capacity errors")
+    w = TINY
+    g = w.geometry
+    kv = gpu_pool_tensor(torch, w)
+    batch = make_batch(w)
+    db = ck.DeviceBatch(batch)
+    with ck.Pool(g, w.seed, kv, max_claims=8, event_capacity=4096) as pool:
+        with pytest.raises(ck.ClaimError) as ei:
+            pool.offload(db)  # 16 claims > 8
+        assert ei.value.status == ck.ENOSPC
+    with ck.Pool(g, w.seed, kv, max_claims=64, event_capacity=40) as pool:
+        pool.offload(db)  # 16..32 events
+        with pytest.raises(ck.ClaimError) as ei:
+            pool.check(db)  # could need 32 more
+        assert ei.value.status == ck.ENOSPC
+        pool.read()  # drains the log
+        pool.restore(db)
+        pool.read()
+        pool.check(db)
+        out, ev = pool.read()
+        assert len(out) == 16 and len(ev) >= 16
+    with ck.Pool(g, w.seed, kv, max_claims=64, event_capacity=4096) as pool:
+        small = torch.empty(g.block_bytes, dtype=torch.uint8, device="cuda")
+        with pytest.raises(ck.ClaimError) as ei:
+            pool.offload(db, staging=small)
+        assert ei.value.status == ck.ENOSPC
+        pool.offload(db)  # the refused call changed nothing
+        with pytest.raises(ck.ClaimError) as ei:
+            pool.offload(db)
+        assert ei.value.status == ck.EDUP
+        bad = FaultSpec(np.array([g.num_blocks], np.uint32), np.array([0], np.uint64),
+                        np.zeros(0, np.uint32))
+        with pytest.raises(ck.ClaimError) as ei:
+            pool.restore(db, faults=bad)
+        assert ei.value.status == ck.EINVAL
+        bad = FaultSpec(np.array([0], np.uint32), np.array([8 * g.block_bytes], np.uint64),
+                        np.zeros(0, np.uint32))
+        with pytest.raises(ck.ClaimError) as ei:
+            pool.restore(db, faults=bad)
+        assert ei.value.status == ck.EINVAL
+        # restoring from staging needs the whole staged size
+        U = batch.unique_blocks(g.num_blocks).size
+        big = torch.empty(U * g.block_bytes, dtype=torch.uint8, device="cuda")
+        pool2 = ck.Pool(g, w.seed, kv, max_claims=64, event_capacity=4096)
+        pool2.offload(db, staging=big)
+        with pytest.raises(ck.ClaimError) as ei:
+            pool2.restore(db, staging=big, staging_bytes=big.numel() - 16)
+        assert ei.value.status == ck.EINVAL
+        pool2.restore(db, staging=big)
+        pool2.close()
+    del kv
+    free_gpu(torch)
+
+
+# ------------------------------------------------------------- staged round trip
+
+
+@pytest.mark.parametrize("where", ["device", "pinned-host"])
+def test_staged_round_trip(torch, ck, where):
+    w = scaled(FULL["mla-fp8"], 30, 40, corrupt_rate=0.1, num_load_failed=1)
+    g = w.geometry
+    batch = make_batch(w)
+    faults = make_faults(w, batch)
+    U = batch.unique_blocks(g.num_blocks).size
+    note(f"staged round trip via {where}: {U} blocks of {g.block_bytes} B")
+    kv = gpu_pool_tensor(torch, w)
+    if where == "device":
+        staging = torch.empty(U * g.block_bytes, dtype=torch.uint8, device="cuda")
+    else:
+        staging = torch.empty(U * g.block_bytes, dtype=torch.uint8, pin_memory=True)
+    db = ck.DeviceBatch(batch)
+    host = content.pool_host(g, w.content_seed)
+    with ck.Pool(g, w.seed, kv, **capacities(batch)) as pool:
+        pool.offload(db, staging=staging)
+        torch.cuda.synchronize()
+        # staging holds the canonical bytes, ascending block order
+        st_bytes = staging.cpu().numpy()
+        uniq = batch.unique_blocks(g.num_blocks)
+        for k in (0, U // 2, U - 1):
+            want = O.canonical_block(host, g.planes, g.num_blocks, g.chunk_bytes, int(uniq[k]))
+            assert np.array_equal(st_bytes[k * g.block_bytes:(k + 1) * g.block_bytes], want)
+        kv.zero_()  # the device copy is gone
+        pool.restore(db, staging=staging, faults=faults)
+        pool.check(db)
+        out, ev = pool.read()
+    restored = apply_flips(host, w, faults)
+    assert np.array_equal(kv.cpu().numpy(), restored)
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    op.offload(batch, digests(host, w))
+    op.restore(batch, faults.load_failed)
+    same_outcomes(out, op.check(batch, digests(restored, w)))
+    same_events(ev, op.events())
+    del kv, staging
+    free_gpu(torch)
+
+
+# ----------------------------------------------------------- full-size workloads
+
+
+@pytest.mark.parametrize("name", ["llama3-8b", "llama3-70b", "small-claim-stress", "mla-fp8"])
+def test_full_size_parity(torch, ck, name):
+    w = FULL[name]
+    g = w.geometry
+    batch = make_batch(w)
+    faults = make_faults(w, batch)
+    note(f"full size {name}: {batch.num_claims} claims, {batch.num_refs} refs, "
+         f"{batch.num_tokens} tokens, pool {g.pool_bytes / 1e9:.2f} GB")
+    kv = gpu_pool_tensor(torch, w)
+    db = ck.DeviceBatch(batch)
+    rng = np.random.default_rng(w.gen_seed + 1)
+    ref = batch.unique_blocks(g.num_blocks)
+    sample = rng.choice(ref, size=min(16, ref.size), replace=False)
+    with ck.Pool(g, w.seed, kv, **capacities(batch)) as pool:
+        pool.offload(db)
+        pool.restore(db, faults=faults)
+        _, ev_pre = pool.read(max_outcomes=1)
+        pool.check(db)
+        out, ev = pool.read()
+        st = pool.block_state()
+    note("  gpu done; oracle")
+    d0, d1 = modeled_digests(w, faults, sample)
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    assert op.offload(batch, d0) == O.OK
+    assert op.restore(batch, faults.load_failed) == O.OK
+    want_pre = op.events(clear=True)
+    want = op.check(batch, d1)
+    same_events(ev_pre, want_pre)
+    same_outcomes(out, want)
+    same_events(ev, op.events())
+    changed = faults.changed_blocks()
+    real = np.union1d(np.union1d(changed, faults.load_failed), sample).astype(np.int64)
+    real = real[np.isin(real, ref)]
+    assert np.array_equal(st["d_off"][real], d0[real])
+    assert np.array_equal(st["d_res"][real], d1[real])
+    unchanged = np.setdiff1d(ref, changed)
+    assert np.array_equal(st["d_res"][unchanged], st["d_off"][unchanged])
+    assert st["valid_off"][ref].all()
+    codes = np.bincount(out["code"], minlength=3)
+    note(f"  outcomes unknown/materialized/failed = {codes.tolist()}")
+    del kv, db
+    free_gpu(torch)
