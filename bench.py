@@ -1,0 +1,204 @@
+"""Benchmark: verified claim-KV bandwidth of claim_check on one MI355X.
+
+One step = one claim_check call over the whole batch: select the unique
+referenced blocks, gather + digest them (the HBM-bound kernel), combine the
+block digests, then per claim chain the token hash, compare, min-reduce to
+the outcome and append the ordered events.  The pool, the batch and the
+offload record are resident in HBM before the timed region starts.
+
+Prints one JSON line.  ``value`` is the physical verified bandwidth: unique
+physical block bytes digested and checked per second (each physical block
+is read once however many claims alias it).
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verified claim-KV GB/s (gather+digest+compare) and claims/s; % of HBM peak"
+HBM_PEAK_GBPS = 8000.0  # MI355X published HBM3E bandwidth
+
+
+def cpu_baseline(w, batch, faults, sample_blocks: int):
+    """The oracle as it stands, single-threaded, on a bounded sample: the
+    digest of `sample_blocks` distinct unique blocks (content generated
+    untimed) gives the per-byte rate; the claim stage (chain, compare,
+    min-reduction, events) runs on the whole batch with modeled digests."""
+    import numpy as np
+
+    from oracle import oracle as O
+    from paper_2606_01387_amd.synth import content
+    from tests.helpers import modeled_digests
+
+    g = w.geometry
+    uniq = batch.unique_blocks(g.num_blocks)
+    blocks = uniq[:sample_blocks]
+    canon = [content.block_canonical(g, w.content_seed, int(b)) for b in blocks]
+    t0 = time.perf_counter()
+    for c in canon:
+        O.block_digest(c, w.seed)
+    t_digest = time.perf_counter() - t0
+    d0, d1 = modeled_digests(w, faults, blocks_needed=[])
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    op.offload(batch, d0)
+    op.restore(batch, faults.load_failed)
+    op.events(clear=True)
+    t0 = time.perf_counter()
+    out = op.check(batch, d1)
+    t_claims = time.perf_counter() - t0
+    per_byte = t_digest / (len(blocks) * g.block_bytes)
+    t_check = per_byte * uniq.size * g.block_bytes + t_claims
+    gbps = uniq.size * g.block_bytes / t_check / 1e9
+    return {
+        "value": round(gbps, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"single-threaded oracle: digest of {len(blocks)} of {uniq.size} unique blocks "
+                   f"({len(blocks) * g.block_bytes / 1e9:.2f} GB) timed in {t_digest:.2f} s and "
+                   f"extrapolated per byte to all {uniq.size}; claim stage on all "
+                   f"{batch.num_claims} claims timed in {t_claims:.2f} s"),
+        "claims_per_s": round(batch.num_claims / t_check, 2),
+        "host_cpus": os.cpu_count(),
+    }, out
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama3-8b")
+    ap.add_argument("--cpu-sample-blocks", type=int, default=512)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-gib", type=float, default=0.0,
+                    help="run one plain device copy of this size first (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this checker runs one pool per GPU and has no "
+              "multi-GPU path; run it with --gpus 1", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2606_01387_amd import claimkv as ck
+    from paper_2606_01387_amd.synth import FULL, content, make_batch, make_faults
+
+    w = FULL[args.workload]
+    g = w.geometry
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    batch = make_batch(w)
+    faults = make_faults(w, batch)
+    uniq = batch.unique_blocks(g.num_blocks)
+    U, C = int(uniq.size), batch.num_claims
+    present_refs = int((batch.block_ids < g.num_blocks).sum())
+
+    if args.copy_probe_gib > 0:
+        n = int(args.copy_probe_gib * (1 << 30))
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    kv = torch.empty(g.pool_bytes, dtype=torch.uint8, device=dev)
+    content.fill_pool_gpu(kv.data_ptr(), kv.numel(), g, w.content_seed, stream.cuda_stream)
+    db = ck.DeviceBatch(batch, device=dev)
+    steps, warm = args.steps, args.warmup
+    pool = ck.Pool(g, w.seed, kv, stream=stream, max_claims=2 * C, max_footprint=2 * batch.num_refs,
+                   event_capacity=2 * C * (steps + warm + 2) + 4 * C, timing=True)
+    pool.offload(db)
+    pool.restore(db, faults=faults)
+    pool.read(max_outcomes=1)
+
+    for _ in range(warm):
+        pool.check(db)
+    torch.cuda.synchronize()
+    pool.timing()  # discard warm-up stage times
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        pool.check(db)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stages = pool.timing()
+    out, ev = pool.read()
+    pool.close()
+
+    ms_per_step = (t1 - t0) * 1e3 / steps
+    phys_bytes = U * g.block_bytes
+    meta_bytes = (8 * C + 4 * (C + 1) + 4 * batch.num_refs + 8 * (C + 1) + 4 * batch.num_tokens
+                  + 64 * C + 40 * len(ev) // max(1, steps + warm))
+    value = phys_bytes / (ms_per_step * 1e-3) / 1e9
+    digest_ms = stages["digest_ms"] / max(1, stages["calls"])
+    achieved = phys_bytes / (digest_ms * 1e-3) / 1e9
+    n_fail = int((out["code"] == ck.RESTORE_FAILED_FAIL_CLOSED).sum())
+
+    line = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warm,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "num_blocks": g.num_blocks,
+            "block_bytes": g.block_bytes,
+            "unique_blocks": U,
+            "claims": C,
+            "block_refs": batch.num_refs,
+            "tokens": batch.num_tokens,
+            "corrupted_blocks": int(faults.flip_blocks.size),
+        },
+        "claims_per_s": round(C / (ms_per_step * 1e-3), 1),
+        "logical_GBps": round(present_refs * g.block_bytes / (ms_per_step * 1e-3) / 1e9, 2),
+        "pct_hbm_peak": round(100 * (phys_bytes + meta_bytes) / (ms_per_step * 1e-3) / 1e9
+                              / HBM_PEAK_GBPS, 2),
+        "stage_ms": {k: round(stages[k] / max(1, stages["calls"]), 4)
+                     for k in ("select_ms", "digest_ms", "finalize_ms", "claims_ms", "events_ms")},
+        "outcomes": {"failed_closed": n_fail, "materialized": int((out["code"] == ck.MATERIALIZED).sum()),
+                     "unknown": int((out["code"] == ck.UNKNOWN).sum())},
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_digest",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "bytes_per_launch": phys_bytes,
+            "avg_launch_ms": round(digest_ms, 4),
+        },
+    }
+    if not args.no_cpu_baseline:
+        base, want = cpu_baseline(w, batch, faults, args.cpu_sample_blocks)
+        line["cpu_baseline"] = base
+        line["verified_against_oracle"] = bool(np.array_equal(out["code"], want["code"]) and
+                                               np.array_equal(out["first_failing_block"],
+                                                              want["first_failing_block"]))
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
