@@ -98,12 +98,6 @@ __device__ __forceinline__ uint64_t lane_read64(uint64_t v, uint32_t src_lane) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-__device__ __forceinline__ uint64_t wave_sum64(uint64_t v) {
-  const uint32_t lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += lane_read64(v, lane ^ o);
-  return v;
-}
 
 template <int W>
 __device__ __forceinline__ uint64_t group_min64(uint64_t v) {
@@ -309,13 +303,50 @@ __global__ void __launch_bounds__(1024) k_compact(uint8_t* __restrict__ mark, ui
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// Partial digests of the unique blocks.  Wave w serves piece ps = w % PS
-// (plane p = ps / segs, segment s = ps % segs) and blocks u = w / PS,
-// w / PS + groups, ...  Lane l, slot k covers 16-byte vector
-// v = s*64*LPT + 64k + l of the plane's chunk, i.e. canonical words
-// i = p*2V + 2v and 2v + 1.  Optionally copies the vectors to staging
-// ([slot][plane][chunk], slot = unique index).
-template <int LPT>
+// Partial digests of the unique blocks.
+//
+// A piece is one 64-lane x LPT-vector segment of a plane's chunk (piece
+// index ps = plane * segs + segment).  Workgroup (piece group pg, group g)
+// runs 4 waves on the 4 consecutive pieces 4pg .. 4pg+3 of the same blocks
+// u = g, g + groups, g + 2 groups, ...: lane l, slot k of a wave covers
+// 16-byte vector v = s*64*LPT + 64k + l of the plane's chunk, i.e.
+// canonical words i = p*2V + 2v and 2v + 1, whose keys it keeps in VGPRs.
+// Each wave's per-block sum goes to an LDS ring; when the ring is full (or
+// the blocks run out) the workgroup adds its 4 rings and writes one
+// contiguous run of per-(piece group, block) partials,
+//   partial[(pg * groups + g) * NW + n],  NW = ceil(U / groups),
+// so the streaming reads are not interleaved with scattered small writes.
+// Optionally copies the vectors to staging ([slot][plane][chunk], slot =
+// unique index).
+constexpr int kRing = 256;
+
+__device__ __forceinline__ uint64_t dpp_wave_sum64(uint64_t v) {
+  // Out-of-row sources read 0 (old = 0): after row shifts by 1, 2, 4 and 8
+  // lane 15 of every row holds its row's total, and the two row broadcasts
+  // fold the rows into lane 63.
+  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+#define DPP_STEP(ctrl, row_mask)                                                       \
+  {                                                                                    \
+    const uint32_t l2 = __builtin_amdgcn_update_dpp(0u, lo, ctrl, row_mask, 0xf, false); \
+    const uint32_t h2 = __builtin_amdgcn_update_dpp(0u, hi, ctrl, row_mask, 0xf, false); \
+    const uint64_t t = (((uint64_t)hi << 32) | lo) + (((uint64_t)h2 << 32) | l2);       \
+    lo = (uint32_t)t;                                                                  \
+    hi = (uint32_t)(t >> 32);                                                          \
+  }
+  DPP_STEP(0x111, 0xf)  // row_shr:1
+  DPP_STEP(0x112, 0xf)  // row_shr:2
+  DPP_STEP(0x114, 0xf)  // row_shr:4
+  DPP_STEP(0x118, 0xf)  // row_shr:8
+  DPP_STEP(0x142, 0xa)  // row_bcast:15 into rows 1 and 3
+  DPP_STEP(0x143, 0xc)  // row_bcast:31 into rows 2 and 3
+#undef DPP_STEP
+  const uint32_t l = __builtin_amdgcn_readlane(lo, 63), h = __builtin_amdgcn_readlane(hi, 63);
+  return ((uint64_t)h << 32) | l;
+}
+
+// RAGGED: the chunk's last segment is partly past its end (masked slots).
+// STAGE: also copy the vectors to staging (offload with staging).
+template <int LPT, bool RAGGED, bool STAGE>
 __global__ void __launch_bounds__(kThreads) k_digest(const u32x4* __restrict__ pool, uint32_t nb,
                                                      uint32_t chunk_vecs, uint32_t planes,
                                                      uint32_t segs, uint32_t groups,
@@ -323,89 +354,107 @@ __global__ void __launch_bounds__(kThreads) k_digest(const u32x4* __restrict__ p
                                                      const Counters* __restrict__ ctr,
                                                      uint64_t seed, uint64_t* __restrict__ partial,
                                                      u32x4* __restrict__ staging) {
+  __shared__ uint64_t ring[kThreads / 64][kRing];
   const uint32_t lane = threadIdx.x & 63;
-  const uint32_t wave = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t ps_total = planes * segs;
-  const uint32_t ps = wave % ps_total;
-  const uint32_t g = wave / ps_total;
+  const uint32_t pgs = (ps_total + 3) / 4;
+  const uint32_t pg = blockIdx.x % pgs;
+  const uint32_t g = blockIdx.x / pgs;
   if (g >= groups) return;
-  const uint32_t p = ps / segs, s = ps % segs;
+  const uint32_t ps = pg * 4 + w;
+  const bool active = ps < ps_total;  // wave-uniform: the last piece group may be short
+  const uint32_t p = active ? ps / segs : 0, s = active ? ps % segs : 0;
+  const uint32_t v0 = s * 64u * LPT + lane;  // this lane's vector in slot 0
 
   uint32_t klo[LPT][2], khi[LPT][2];
-  bool valid[LPT];
 #pragma unroll
   for (int k = 0; k < LPT; ++k) {
-    const uint32_t v = s * 64u * LPT + 64u * k + lane;
-    valid[k] = v < chunk_vecs;
+    const uint32_t v = v0 + 64u * k;
+    const bool ok = !RAGGED || v < chunk_vecs;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const uint64_t key = stream_output(seed, (uint64_t)p * chunk_vecs * 2 + 2ull * v + h) | 1ull;
-      klo[k][h] = valid[k] ? (uint32_t)key : 0u;
-      khi[k][h] = valid[k] ? (uint32_t)(key >> 32) : 0u;
+      klo[k][h] = ok ? (uint32_t)key : 0u;  // a masked slot contributes 0
+      khi[k][h] = ok ? (uint32_t)(key >> 32) : 0u;
     }
   }
 
   const uint32_t U = ctr->uniq_count;
-  const uint64_t piece = (uint64_t)s * 64u * LPT + lane;
-  for (uint32_t u = g; u < U; u += groups) {
-    const uint32_t b = uniq[u];
-    const u32x4* chunk = pool + ((uint64_t)p * nb + b) * chunk_vecs;
-    u32x4 x[LPT];
+  const uint32_t NW = (U + groups - 1) / groups;
+  const u32x4* plane = pool + (uint64_t)p * nb * chunk_vecs;
+  uint32_t n = 0;
+  for (uint32_t u = g; u < U; u += groups, ++n) {
+    uint64_t sum = 0;
+    if (active) {
+      const u32x4* chunk = plane + (uint64_t)uniq[u] * chunk_vecs;
+      u32x4 x[LPT];
 #pragma unroll
-    for (int k = 0; k < LPT; ++k) {
-      // a masked slot (past the end of a ragged chunk) reads the chunk's
-      // first vector instead and discards it: no address outside the chunk
-      // is ever formed
-      const u32x4 t = __builtin_nontemporal_load(chunk + (valid[k] ? piece + 64 * k : 0));
-      x[k] = valid[k] ? t : u32x4{0u, 0u, 0u, 0u};
+      for (int k = 0; k < LPT; ++k) {
+        // a masked slot reads the chunk's first vector (its key is 0): no
+        // address outside the chunk is ever formed
+        const uint32_t v = v0 + 64u * k;
+        x[k] = __builtin_nontemporal_load(chunk + ((!RAGGED || v < chunk_vecs) ? v : 0u));
+      }
+      __builtin_amdgcn_sched_barrier(0);  // every load in flight before any use
+      uint64_t acc = 0;
+      uint32_t cross = 0;
+#pragma unroll
+      for (int k = 0; k < LPT; ++k) {
+        // word 0 = (x.y:x.x), word 1 = (x.w:x.z); only the low 32 bits of
+        // the cross terms reach the product mod 2^64
+        acc += (uint64_t)x[k].x * klo[k][0];
+        cross += x[k].x * khi[k][0] + x[k].y * klo[k][0];
+        acc += (uint64_t)x[k].z * klo[k][1];
+        cross += x[k].z * khi[k][1] + x[k].w * klo[k][1];
+      }
+      sum = dpp_wave_sum64(acc + ((uint64_t)cross << 32));
+      if constexpr (STAGE) {
+        u32x4* dst = staging + ((uint64_t)u * planes + p) * chunk_vecs;
+#pragma unroll
+        for (int k = 0; k < LPT; ++k) {
+          const uint32_t v = v0 + 64u * k;
+          if (!RAGGED || v < chunk_vecs) dst[v] = x[k];
+        }
+      }
     }
-    uint64_t acc = 0;
-    uint32_t cross = 0;
-#pragma unroll
-    for (int k = 0; k < LPT; ++k) {
-      // word 0 = (x.y:x.x), word 1 = (x.w:x.z)
-      acc += (uint64_t)x[k].x * klo[k][0];
-      cross += x[k].x * khi[k][0] + x[k].y * klo[k][0];
-      acc += (uint64_t)x[k].z * klo[k][1];
-      cross += x[k].z * khi[k][1] + x[k].w * klo[k][1];
-    }
-    const uint64_t sum = wave_sum64(acc + ((uint64_t)cross << 32));
-    if (lane == 0) partial[(uint64_t)u * ps_total + ps] = sum;
-    if (staging) {
-      u32x4* dst = staging + ((uint64_t)u * planes + p) * chunk_vecs + piece;
-#pragma unroll
-      for (int k = 0; k < LPT; ++k)
-        if (valid[k]) dst[64 * k] = x[k];
+    const uint32_t slot = n % kRing;
+    if (lane == 0) ring[w][slot] = sum;
+    if (slot == kRing - 1 || u + groups >= U) {  // the same for all 4 waves
+      __syncthreads();
+      const uint32_t n0 = n - slot;
+      for (uint32_t i = threadIdx.x; i <= slot; i += kThreads)
+        partial[((uint64_t)pg * groups + g) * NW + n0 + i] =
+            ring[0][i] + ring[1][i] + ring[2][i] + ring[3][i];
+      __syncthreads();
     }
   }
 }
 
-// Add each unique block's partials.  One wave per block.
+// Add each unique block's piece-group partials.  One thread per block.
 //   mode 0 (offload): d_off, valid_off = 1, load_failed = 0, slot_of
 //   mode 1 (check):   d_res
 __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restrict__ uniq,
                                                        const Counters* __restrict__ ctr,
                                                        const uint64_t* __restrict__ partial,
-                                                       uint32_t ps_total, int mode, int staged,
-                                                       uint64_t* __restrict__ d_out,
+                                                       uint32_t pgs, uint32_t groups, int mode,
+                                                       int staged, uint64_t* __restrict__ d_out,
                                                        uint8_t* __restrict__ valid_off,
                                                        uint8_t* __restrict__ load_failed,
                                                        uint32_t* __restrict__ slot_of) {
-  const uint32_t lane = threadIdx.x & 63;
-  const uint32_t waves = gridDim.x * (kThreads / 64);
   const uint32_t U = ctr->uniq_count;
-  for (uint32_t u = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6); u < U; u += waves) {
+  const uint32_t NW = (U + groups - 1) / groups;
+  const uint32_t stride = gridDim.x * kThreads;
+  for (uint32_t u = blockIdx.x * kThreads + threadIdx.x; u < U; u += stride) {
+    const uint32_t g = u % groups, n = u / groups;
     uint64_t sum = 0;
-    for (uint32_t q = lane; q < ps_total; q += 64) sum += partial[(uint64_t)u * ps_total + q];
-    sum = wave_sum64(sum);
-    if (lane == 0) {
-      const uint32_t b = uniq[u];
-      d_out[b] = sum;
-      if (mode == 0) {
-        valid_off[b] = 1;
-        load_failed[b] = 0;
-        slot_of[b] = staged ? u : kNone;
-      }
+    for (uint32_t pg = 0; pg < pgs; ++pg) sum += partial[((uint64_t)pg * groups + g) * NW + n];
+    const uint32_t b = uniq[u];
+    d_out[b] = sum;
+    if (mode == 0) {
+      valid_off[b] = 1;
+      load_failed[b] = 0;
+      slot_of[b] = staged ? u : kNone;
     }
   }
 }
@@ -856,7 +905,7 @@ struct claim_pool {
   void* kv = nullptr;
 
   int lpt = 8;
-  uint32_t segs = 1, ps_total = 1, groups = 1;
+  uint32_t segs = 1, ps_total = 1, pgs = 1, groups = 1;
 
   uint64_t *d_off = nullptr, *d_res = nullptr, *partial = nullptr;
   uint8_t *valid_off = nullptr, *load_failed = nullptr, *mark = nullptr;
@@ -1054,42 +1103,52 @@ int select_blocks(claim_pool* P, const claim_batch* b, int mode) {
   return hip_status(hipGetLastError());
 }
 
-int launch_digest(claim_pool* P, uint64_t* partial, void* staging) {
-  const uint64_t waves = (uint64_t)P->ps_total * P->groups;
-  const uint32_t grid = (uint32_t)((waves + kThreads / 64 - 1) / (kThreads / 64));
+template <int LPT>
+int launch_digest_lpt(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_cu) {
+  const bool ragged = (uint64_t)P->segs * 64 * LPT != P->chunk_vecs;
+  const void* fn;
+  if (ragged)
+    fn = staging ? (const void*)k_digest<LPT, true, true> : (const void*)k_digest<LPT, true, false>;
+  else
+    fn = staging ? (const void*)k_digest<LPT, false, true> : (const void*)k_digest<LPT, false, false>;
+  if (wgs_per_cu)  // occupancy query only
+    return hip_status(hipOccupancyMaxActiveBlocksPerMultiprocessor(wgs_per_cu, fn, kThreads, 0));
   const u32x4* pool = (const u32x4*)P->kv;
   u32x4* st = (u32x4*)staging;
+  const dim3 grid(P->pgs * P->groups), block(kThreads);
+  uint32_t cv = (uint32_t)P->chunk_vecs;
+#define GO(R, S)                                                                                \
+  hipLaunchKernelGGL((k_digest<LPT, R, S>), grid, block, 0, P->stream, pool, P->nb, cv, P->planes, \
+                     P->segs, P->groups, P->uniq, P->ctr, P->seed, partial, st)
+  if (ragged) {
+    if (staging) GO(true, true); else GO(true, false);
+  } else {
+    if (staging) GO(false, true); else GO(false, false);
+  }
+#undef GO
+  return hip_status(hipGetLastError());
+}
+
+// Launch the digest (or, with wgs_per_cu, query its occupancy).
+int launch_digest(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_cu = nullptr) {
   switch (P->lpt) {
-#define DIGEST_CASE(l)                                                                           \
-  case l:                                                                                        \
-    hipLaunchKernelGGL(k_digest<l>, dim3(grid), dim3(kThreads), 0, P->stream, pool, P->nb,       \
-                       (uint32_t)P->chunk_vecs, P->planes, P->segs, P->groups, P->uniq, P->ctr, \
-                       P->seed, partial, st);                                                    \
-    break;
-    DIGEST_CASE(1)
-    DIGEST_CASE(2)
-    DIGEST_CASE(3)
-    DIGEST_CASE(4)
-    DIGEST_CASE(5)
-    DIGEST_CASE(6)
-    DIGEST_CASE(7)
-    DIGEST_CASE(8)
-    DIGEST_CASE(9)
-    DIGEST_CASE(10)
-    DIGEST_CASE(11)
-    DIGEST_CASE(12)
+#define DIGEST_CASE(l) \
+  case l:              \
+    return launch_digest_lpt<l>(P, partial, staging, wgs_per_cu);
+    DIGEST_CASE(1) DIGEST_CASE(2) DIGEST_CASE(3) DIGEST_CASE(4) DIGEST_CASE(5) DIGEST_CASE(6)
+    DIGEST_CASE(7) DIGEST_CASE(8) DIGEST_CASE(9) DIGEST_CASE(10) DIGEST_CASE(11) DIGEST_CASE(12)
+    DIGEST_CASE(13) DIGEST_CASE(14) DIGEST_CASE(15) DIGEST_CASE(16)
 #undef DIGEST_CASE
     default:
       return CLAIM_EINVAL;
   }
-  return hip_status(hipGetLastError());
 }
 
 int launch_finalize(claim_pool* P, int mode, int staged) {
-  const uint32_t grid = P->nb / (kThreads / 64) + 1 < 8192 ? P->nb / (kThreads / 64) + 1 : 8192;
+  const uint32_t grid = P->nb / kThreads + 1 < 2048 ? P->nb / kThreads + 1 : 2048;
   hipLaunchKernelGGL(k_finalize, dim3(grid), dim3(kThreads), 0, P->stream, P->uniq, P->ctr,
-                     P->partial, P->ps_total, mode, staged, mode == 0 ? P->d_off : P->d_res,
-                     P->valid_off, P->load_failed, P->slot_of);
+                     P->partial, P->pgs, P->groups, mode, staged,
+                     mode == 0 ? P->d_off : P->d_res, P->valid_off, P->load_failed, P->slot_of);
   return hip_status(hipGetLastError());
 }
 
@@ -1136,32 +1195,38 @@ int append_events(claim_pool* P, const claim_batch* b) {
     HIP_TRY(hipGetLastError());                                                                 \
   } while (0)
 
-// Choose vectors per lane (LPT) and segments per chunk for the digest.
-void choose_digest_shape(claim_pool* P) {
+// Choose vectors per lane (LPT), segments per chunk and the digest grid.
+// LPT is the divisor of the chunk's vectors-per-lane closest to 16 (ties:
+// the larger), so every segment is full and each wave streams up to 16 KiB
+// per block; chunks that are not a whole number of 1 KiB rows use LPT 16
+// with a ragged last segment.  The grid holds exactly as many workgroups as
+// can be resident at once (no tail of late waves): groups = resident
+// workgroups / piece groups.
+int choose_digest_shape(claim_pool* P) {
   const uint64_t V = P->chunk_vecs;
   const uint64_t Q = (V + 63) / 64;  // vectors per lane to cover one chunk
-  // Prefer a divisor of Q in [4, 12] closest to 8 (ties: the larger), so
-  // every segment is full; otherwise 8 per lane with a ragged last segment.
-  int best = 0, best_dist = 1 << 30;
+  int best = 0;
   if (V % 64 == 0) {
-    for (int d = 4; d <= 12; ++d) {
-      const int dist = d > 8 ? d - 8 : 8 - d;
-      if (Q % d == 0 && (dist < best_dist || (dist == best_dist && d > best))) {
+    for (int d = 16; d >= 1; --d)
+      if (Q % d == 0) {
         best = d;
-        best_dist = dist;
+        break;
       }
-    }
+    if (best < 4 && Q > 16) best = 0;  // only tiny divisors: use a ragged tail instead
   }
-  if (best == 0) best = Q < 8 ? (int)Q : 8;
+  if (best == 0) best = Q < 16 ? (int)Q : 16;
   P->lpt = best;
   P->segs = (uint32_t)((Q + best - 1) / best);
   P->ps_total = P->planes * P->segs;
-  // enough waves to keep every CU's SIMDs busy (about 24 waves per CU)
-  const uint64_t target = (uint64_t)P->cus * 24;
-  uint64_t g = target / P->ps_total;
+  P->pgs = (P->ps_total + 3) / 4;
+  int per_cu = 0;
+  TRY(launch_digest(P, nullptr, nullptr, &per_cu));  // the check kernel's occupancy
+  if (per_cu < 1) per_cu = 1;
+  uint64_t g = (uint64_t)per_cu * P->cus / P->pgs;
   if (g < 1) g = 1;
   if (g > P->nb) g = P->nb;
   P->groups = (uint32_t)g;
+  return CLAIM_OK;
 }
 
 void free_pool(claim_pool* P) {
@@ -1262,11 +1327,12 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     P->block_bytes = planes * chunk;
     P->seed = d->seed;
     P->kv = d->kv_base;
-    choose_digest_shape(P);
+    if ((rc = choose_digest_shape(P))) break;
 
     const uint64_t nb = d->num_blocks;
     if ((rc = dalloc(&P->d_off, nb)) || (rc = dalloc(&P->d_res, nb)) ||
-        (rc = dalloc(&P->partial, nb * P->ps_total)) || (rc = dalloc(&P->valid_off, nb)) ||
+        (rc = dalloc(&P->partial, (uint64_t)P->pgs * (nb + P->groups))) ||
+        (rc = dalloc(&P->valid_off, nb)) ||
         (rc = dalloc(&P->load_failed, nb)) || (rc = dalloc(&P->mark, nb)) ||
         (rc = dalloc(&P->uniq, nb)) || (rc = dalloc(&P->slot_of, nb)))
       break;
