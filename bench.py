@@ -26,6 +26,24 @@ METRIC = "verified claim-KV GB/s (gather+digest+compare) and claims/s; % of HBM 
 HBM_PEAK_GBPS = 8000.0  # MI355X published HBM3E bandwidth
 
 
+def digest_traffic(workload: str):
+    """Calibrated HBM bytes per digest launch from the committed counter
+    summary, or None if there is none or the kernel source changed since."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", f"k_digest_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    if "```json" not in text:
+        return None
+    data = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    src = os.path.join(ROOT, data["source"])
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != data["source_sha256"]:
+        return None
+    return int(data["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(w, batch, faults, sample_blocks: int):
     """The oracle as it stands, single-threaded, on a bounded sample: the
     digest of `sample_blocks` distinct unique blocks (content generated
@@ -106,15 +124,31 @@ def main() -> int:
     present_refs = int((batch.block_ids < g.num_blocks).sum())
 
     if args.copy_probe_gib > 0:
+        # a plain copy kernel that reads and writes exactly n bytes with the
+        # checker's load form: the reference for scaling the HBM counters
         n = int(args.copy_probe_gib * (1 << 30))
-        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        a = torch.zeros(n, dtype=torch.uint8, device=dev)
         b = torch.empty_like(a)
-        b.copy_(a)
+        content.copy_probe(b.data_ptr(), a.data_ptr(), n, stream.cuda_stream)
         torch.cuda.synchronize()
         del a, b
 
     kv = torch.empty(g.pool_bytes, dtype=torch.uint8, device=dev)
     content.fill_pool_gpu(kv.data_ptr(), kv.numel(), g, w.content_seed, stream.cuda_stream)
+
+    # measured streaming-read ceiling of this machine (context for the roofline)
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    probe_ms = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        content.read_probe(kv.data_ptr(), kv.numel(), cus, sink.data_ptr(), stream.cuda_stream)
+        e1.record(stream)
+        e1.synchronize()
+        probe_ms.append(e0.elapsed_time(e1))
+    probe_bytes = kv.numel() // 32768 * 32768
+    read_ceiling = probe_bytes / (sorted(probe_ms)[1] * 1e-3) / 1e9
     db = ck.DeviceBatch(batch, device=dev)
     steps, warm = args.steps, args.warmup
     pool = ck.Pool(g, w.seed, kv, stream=stream, max_claims=2 * C, max_footprint=2 * batch.num_refs,
@@ -185,9 +219,12 @@ def main() -> int:
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": digest_traffic(w.name),
+            "traffic_unit": "bytes/launch",
             "bytes_per_launch": phys_bytes,
             "avg_launch_ms": round(digest_ms, 4),
+            "measured_read_ceiling": round(read_ceiling, 1),
+            "frac_of_read_ceiling": round(achieved / read_ceiling, 4),
         },
     }
     if not args.no_cpu_baseline:

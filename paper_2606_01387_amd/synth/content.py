@@ -67,6 +67,10 @@ def _fill_lib():
         vp, u32, u64 = ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64
         L.synth_fill_pool.argtypes = [vp, u64, u64, ctypes.c_int, u32, u32, u64, vp]
         L.synth_fill_pool.restype = ctypes.c_int
+        L.synth_copy_probe.argtypes = [vp, vp, u64, vp]
+        L.synth_copy_probe.restype = ctypes.c_int
+        L.synth_read_probe.argtypes = [vp, u64, u32, vp, vp]
+        L.synth_read_probe.restype = ctypes.c_int
         _fill = L
     return _fill
 
@@ -107,3 +111,17 @@ def fill_pool_gpu(ptr: int, nbytes: int, g: Geometry, content_seed: int, stream:
                                      g.num_blocks, g.chunk_bytes, stream)
     if rc:
         raise RuntimeError(f"synth_fill_pool failed ({rc})")
+
+
+def copy_probe(dst: int, src: int, nbytes: int, stream: int) -> None:
+    """Plain streaming copy (the checker's load form), for counter calibration."""
+    rc = _fill_lib().synth_copy_probe(dst, src, nbytes, stream)
+    if rc:
+        raise RuntimeError(f"synth_copy_probe failed ({rc})")
+
+
+def read_probe(src: int, nbytes: int, cus: int, sink: int, stream: int) -> None:
+    """Plain streaming read of a buffer (the measured bandwidth ceiling)."""
+    rc = _fill_lib().synth_read_probe(src, nbytes, cus, sink, stream)
+    if rc:
+        raise RuntimeError(f"synth_read_probe failed ({rc})")

@@ -1,9 +1,14 @@
-// fill.hip -- seeded synthetic KV-pool content, generated on the GPU.
+// fill.hip -- GPU helpers for inputs and measurement (not the checker).
 //
-// Part of the input generator (not the checker): it writes the same bytes as
-// content_host.c, from the same definition (Philox4x32-10 counters per
-// 16-byte unit; bf16 Irwin-Hall values or raw bytes), directly into a pool
-// that is too large to build on the host.  A GPU test compares the two.
+//  * synth_fill_pool writes the seeded synthetic pool content: the same
+//    bytes as content_host.c, from the same definition (Philox4x32-10
+//    counters per 16-byte unit; bf16 Irwin-Hall values or raw bytes),
+//    directly into a pool too large to build on the host.  A GPU test
+//    compares the two.
+//  * synth_copy_probe and synth_read_probe are plain streaming kernels with
+//    the checker's load form (16-byte non-temporal loads, 1 KiB contiguous
+//    per wave instruction): the copy calibrates the HBM byte counters, the
+//    read measures the achievable streaming-read bandwidth of a buffer.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -83,9 +88,54 @@ __global__ void __launch_bounds__(256) fill_kernel(uint4* __restrict__ pool, uin
   }
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__global__ void __launch_bounds__(256) copy_kernel(u32x4* __restrict__ dst,
+                                                   const u32x4* __restrict__ src, uint64_t n) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    dst[i] = __builtin_nontemporal_load(src + i);
+}
+
+// Each thread reads 8 vectors per step, 256 apart (1 KiB per wave
+// instruction); n is a multiple of 2048 vectors.
+__global__ void __launch_bounds__(256) read_kernel(const u32x4* __restrict__ src, uint64_t n,
+                                                   uint32_t* __restrict__ sink) {
+  const uint64_t stride = (uint64_t)gridDim.x * 256 * 8;
+  uint32_t acc = 0;
+  for (uint64_t i = (uint64_t)blockIdx.x * 256 * 8 + threadIdx.x; i < n; i += stride) {
+    u32x4 x[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) x[k] = __builtin_nontemporal_load(src + i + 256 * k);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc ^= x[k].x ^ x[k].y ^ x[k].z ^ x[k].w;
+  }
+  if (acc == 0x9E3779B9u) sink[0] = acc;  // practically never: keeps the loads live
+}
+
 }  // namespace
 
 extern "C" {
+
+// Copy nbytes (a multiple of 16, both pointers 16-byte aligned) on stream.
+int synth_copy_probe(void* dst, const void* src, uint64_t nbytes, void* stream) {
+  if (!dst || !src || nbytes % 16 || ((uintptr_t)dst & 15) || ((uintptr_t)src & 15)) return -1;
+  hipLaunchKernelGGL(copy_kernel, dim3(4096), dim3(256), 0, (hipStream_t)stream, (u32x4*)dst,
+                     (const u32x4*)src, nbytes / 16);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// Stream-read the first nbytes of src (rounded down to a multiple of 32 KiB)
+// with grid = cus * 16 workgroups; sink is a 4-byte device scratch word.
+int synth_read_probe(const void* src, uint64_t nbytes, uint32_t cus, void* sink, void* stream) {
+  if (!src || !sink || ((uintptr_t)src & 15) || cus == 0) return -1;
+  const uint64_t n = (nbytes / 16) / 2048 * 2048;
+  if (n == 0) return -1;
+  hipLaunchKernelGGL(read_kernel, dim3(cus * 16), dim3(256), 0, (hipStream_t)stream,
+                     (const u32x4*)src, n, (uint32_t*)sink);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
 
 // Fill a [plane][block][chunk] pool on `stream` (a hipStream_t, may be null).
 // Returns 0, -1 for bad geometry or a too-small buffer, -3 for a HIP error.
