@@ -396,6 +396,11 @@ int orc_restore(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
 
 /* Check: record restored digests, then decide each claim's outcome.
  *
+ * The restored digest is refreshed for every in-range, offloaded block
+ * listed anywhere in the batch's block table; only well-formed rows are
+ * evaluated, so a malformed row can refresh a block's digest but never
+ * contribute to an outcome.
+ *
  * Every failure or ambiguity is a key (class << 32 | position); class 0 is
  * an ambiguity (no claim outcome), class 1 a restoration failure, and a
  * claim-level ambiguity sits at position NONE.  The smallest key decides:
@@ -408,13 +413,11 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
   Pool* p = static_cast<Pool*>(handle);
   Batch bt = {num_claims, num_refs, num_tokens, ids, blk_off, blk_ids, tok_off, tokens};
 
-  /* restored digests of every block the well-formed claims reference */
-  for (uint32_t c = 0; c < num_claims; ++c) {
-    if (malformed(bt, c)) continue;
-    for (uint32_t j = blk_off[c]; j < blk_off[c + 1]; ++j) {
-      uint32_t b = blk_ids[j];
-      if (b < p->num_blocks && p->valid_off[b]) p->d_res[b] = digest_now[b];
-    }
+  /* restored digests of every offloaded block listed in the batch's block
+   * table (all num_refs entries, whichever rows hold them) */
+  for (uint64_t i = 0; i < num_refs; ++i) {
+    uint32_t b = blk_ids[i];
+    if (b < p->num_blocks && p->valid_off[b]) p->d_res[b] = digest_now[b];
   }
 
   for (uint32_t c = 0; c < num_claims; ++c) {

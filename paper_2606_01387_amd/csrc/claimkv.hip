@@ -92,6 +92,28 @@ __device__ __forceinline__ uint32_t lane_read(uint32_t v, uint32_t src_lane) {
   return (uint32_t)__builtin_amdgcn_ds_bpermute((int)(src_lane << 2), (int)v);
 }
 
+// Wave-uniform read of lane `lane` (an SGPR index): the result lives in
+// SGPRs, so a chain of such values runs on the scalar ALU.
+__device__ __forceinline__ uint64_t uniform_read64(uint64_t v, uint32_t lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, lane);
+  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), lane);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// The claim a group serves.  With one claim per wave (W = 64) the index is
+// made provably wave-uniform, so its row is read with scalar loads and its
+// chain runs on the scalar ALU.
+template <int W>
+__device__ __forceinline__ uint64_t group_claim() {
+  const uint64_t c = ((uint64_t)blockIdx.x * 256 + threadIdx.x) / W;
+  if constexpr (W == 64) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)c);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(c >> 32));
+    return ((uint64_t)hi << 32) | lo;
+  }
+  return c;
+}
+
 __device__ __forceinline__ uint64_t lane_read64(uint64_t v, uint32_t src_lane) {
   const uint32_t lo = lane_read((uint32_t)v, src_lane);
   const uint32_t hi = lane_read((uint32_t)(v >> 32), src_lane);
@@ -129,14 +151,19 @@ struct BatchDev {
   const uint32_t* tok;
 };
 
+struct RegEntry {  // one 64-byte line per slot: a probe touches one line
+  uint64_t key;     // claim id; kEmptyId marks an empty slot
+  uint32_t state;   // kSt* bits
+  uint32_t nblk;    // accepted block-table entries
+  uint64_t ntok;    // accepted token count
+  uint64_t chain;   // accepted chain hash h_{nt-1}
+  uint64_t fpoff;   // accepted footprint: fp[fpoff .. fpoff + nblk)
+  uint64_t pad[3];
+};
+
 struct RegDev {
   uint64_t mask;
-  uint64_t* key;
-  uint32_t* state;
-  uint32_t* nblk;
-  uint64_t* ntok;
-  uint64_t* chain;
-  uint64_t* fpoff;
+  RegEntry* e;
   const uint32_t* fp;
 };
 
@@ -162,6 +189,7 @@ static_assert(sizeof(Counters) == 48, "Counters layout");
 static_assert(sizeof(claim_outcome) == 64, "claim_outcome layout");
 static_assert(sizeof(claim_event) == 40, "claim_event layout");
 static_assert(sizeof(Pend) == 32, "Pend layout");
+static_assert(sizeof(RegEntry) == 64, "RegEntry layout");
 
 struct Row {
   uint64_t id;
@@ -187,7 +215,7 @@ __device__ __forceinline__ int64_t reg_find(const RegDev& r, uint64_t id) {
   if (id == kEmptyId) return -1;
   uint64_t s = slot_of_id(id, r.mask);
   for (uint64_t probe = 0; probe <= r.mask; ++probe) {
-    const uint64_t k = r.key[s];
+    const uint64_t k = r.e[s].key;
     if (k == id) return (int64_t)s;
     if (k == kEmptyId) return -1;
     s = (s + 1) & r.mask;
@@ -216,6 +244,13 @@ __global__ void __launch_bounds__(kThreads) k_fill(T* p, uint64_t n, T v) {
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
 }
 
+__global__ void __launch_bounds__(kThreads) k_fill_strided(uint64_t* p, uint64_t n,
+                                                           uint32_t stride_words, uint64_t v) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+    p[i * stride_words] = v;
+}
+
 __global__ void __launch_bounds__(kThreads) k_copy_u32(uint32_t* dst, const uint32_t* src,
                                                        uint64_t n) {
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
@@ -230,7 +265,7 @@ __global__ void __launch_bounds__(kThreads) k_mark(BatchDev b, uint32_t nb, int 
                                                    const uint8_t* __restrict__ valid_off,
                                                    const uint32_t* __restrict__ slot_of,
                                                    uint8_t* __restrict__ mark) {
-  const uint64_t c = ((uint64_t)blockIdx.x * kThreads + threadIdx.x) / W;
+  const uint64_t c = group_claim<W>();
   if (c >= b.C) return;
   const uint32_t gl = threadIdx.x & (W - 1);
   const Row r = read_row(b, c);
@@ -240,6 +275,19 @@ __global__ void __launch_bounds__(kThreads) k_mark(BatchDev b, uint32_t nb, int 
     if (mode == kMarkOffloaded && !valid_off[blk]) continue;
     if (mode == kMarkStaged && slot_of[blk] == kNone) continue;
     mark[blk] = 1;
+  }
+}
+
+// Mark every in-range, offloaded block listed among the batch's block-table
+// entries (the check's selection: one thread per entry, no row validation).
+__global__ void __launch_bounds__(kThreads) k_mark_entries(const uint32_t* __restrict__ bi,
+                                                           uint64_t N, uint32_t nb,
+                                                           const uint8_t* __restrict__ valid_off,
+                                                           uint8_t* __restrict__ mark) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += stride) {
+    const uint32_t blk = bi[i];
+    if (blk < nb && valid_off[blk]) mark[blk] = 1;
   }
 }
 
@@ -272,27 +320,32 @@ __device__ uint32_t block_exclusive_scan_1024(uint32_t v, uint32_t* total, uint3
 }
 
 // Ordered compaction of the marks into the unique-block list (ascending
-// block id).  One workgroup of 1024 threads; clears the marks it reads.
+// block id).  One workgroup of 1024 threads, 16 marks per thread per step
+// read as one 16-byte vector (the mark array is padded to a multiple of 16
+// bytes with zeros); clears the marks it reads.
 __global__ void __launch_bounds__(1024) k_compact(uint8_t* __restrict__ mark, uint32_t nb,
                                                   uint32_t* __restrict__ uniq,
                                                   Counters* __restrict__ ctr) {
   __shared__ uint32_t lds[17];
   uint32_t base = 0;
   constexpr uint32_t kPer = 16;
-  for (uint64_t t0 = 0; t0 < nb; t0 += 1024ull * kPer) {
+  const uint64_t padded = ((uint64_t)nb + 15) / 16 * 16;
+  for (uint64_t t0 = 0; t0 < padded; t0 += 1024ull * kPer) {
     const uint64_t first = t0 + (uint64_t)threadIdx.x * kPer;
     uint32_t bits = 0;
-    for (uint32_t k = 0; k < kPer; ++k) {
-      const uint64_t i = first + k;
-      if (i < nb && mark[i]) bits |= 1u << k;
+    if (first < padded) {
+      const uint4 m = *(const uint4*)(mark + first);
+      const uint32_t w[4] = {m.x, m.y, m.z, m.w};
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        if ((w[k / 4] >> (8 * (k % 4))) & 0xFFu) bits |= 1u << k;
     }
     uint32_t total;
     uint32_t pos = base + block_exclusive_scan_1024(__builtin_popcount(bits), &total, lds);
-    for (uint32_t k = 0; k < kPer; ++k) {
-      if (bits & (1u << k)) {
-        uniq[pos++] = (uint32_t)(first + k);
-        mark[first + k] = 0;
-      }
+    if (bits) {
+      for (uint32_t k = 0; k < kPer; ++k)
+        if (bits & (1u << k)) uniq[pos++] = (uint32_t)(first + k);
+      *(uint4*)(mark + first) = make_uint4(0u, 0u, 0u, 0u);
     }
     base += total;
   }
@@ -431,7 +484,8 @@ __global__ void __launch_bounds__(kThreads) k_digest(const u32x4* __restrict__ p
   }
 }
 
-// Add each unique block's piece-group partials.  One thread per block.
+// Add each unique block's piece-group partials.  One wave per block, lanes
+// over piece groups.
 //   mode 0 (offload): d_off, valid_off = 1, load_failed = 0, slot_of
 //   mode 1 (check):   d_res
 __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restrict__ uniq,
@@ -442,19 +496,24 @@ __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restric
                                                        uint8_t* __restrict__ valid_off,
                                                        uint8_t* __restrict__ load_failed,
                                                        uint32_t* __restrict__ slot_of) {
+  const uint32_t lane = threadIdx.x & 63;
   const uint32_t U = ctr->uniq_count;
   const uint32_t NW = (U + groups - 1) / groups;
-  const uint32_t stride = gridDim.x * kThreads;
-  for (uint32_t u = blockIdx.x * kThreads + threadIdx.x; u < U; u += stride) {
+  const uint32_t waves = gridDim.x * (kThreads / 64);
+  for (uint32_t u = blockIdx.x * (kThreads / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+       u < U; u += waves) {
     const uint32_t g = u % groups, n = u / groups;
     uint64_t sum = 0;
-    for (uint32_t pg = 0; pg < pgs; ++pg) sum += partial[((uint64_t)pg * groups + g) * NW + n];
-    const uint32_t b = uniq[u];
-    d_out[b] = sum;
-    if (mode == 0) {
-      valid_off[b] = 1;
-      load_failed[b] = 0;
-      slot_of[b] = staged ? u : kNone;
+    for (uint32_t pg = lane; pg < pgs; pg += 64) sum += partial[((uint64_t)pg * groups + g) * NW + n];
+    sum = dpp_wave_sum64(sum);
+    if (lane == 0) {
+      const uint32_t b = uniq[u];
+      d_out[b] = sum;
+      if (mode == 0) {
+        valid_off[b] = 1;
+        load_failed[b] = 0;
+        slot_of[b] = staged ? u : kNone;
+      }
     }
   }
 }
@@ -497,7 +556,7 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, uin
                                                      Pend* __restrict__ pend) {
   __shared__ uint64_t tkey[kMaxBlockSize];
   load_token_keys(tkey, bs, seed);
-  const uint64_t c = ((uint64_t)blockIdx.x * kThreads + threadIdx.x) / W;
+  const uint64_t c = group_claim<W>();
   if (c >= b.C) return;
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t gl = lane & (W - 1), gbase = lane & ~(uint32_t)(W - 1);
@@ -517,7 +576,11 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, uin
       m_sum = token_multilinear(b.tok, r.to0 + first, count, tkey);
     }
     const uint64_t steps = j0 < nt ? (nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W) : 0;
-    for (uint32_t t = 0; t < steps; ++t) h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
+    if constexpr (W == 64) {  // one claim per wave: the chain runs on the scalar ALU
+      for (uint32_t t = 0; t < steps; ++t) h = splitmix_step(h ^ uniform_read64(m_sum, t));
+    } else {
+      for (uint32_t t = 0; t < steps; ++t) h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
+    }
   }
   missing = group_or<W>(missing);
   if (gl != 0) return;
@@ -529,7 +592,7 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, uin
   uint64_t s = slot_of_id(r.id, reg.mask);
   bool inserted = false;
   for (uint64_t probe = 0; probe <= reg.mask && !inserted; ++probe) {
-    const unsigned long long old = atomicCAS((unsigned long long*)reg.key + s,
+    const unsigned long long old = atomicCAS((unsigned long long*)&reg.e[s].key,
                                              (unsigned long long)kEmptyId,
                                              (unsigned long long)r.id);
     if (old == kEmptyId)
@@ -541,11 +604,12 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, uin
     cnt[c] = 0;
     return;
   }
-  reg.state[s] = kStAccepted | (offloaded ? kStOffloaded : 0u);
-  reg.nblk[s] = r.n;
-  reg.ntok[s] = r.ntok;
-  reg.chain[s] = h;
-  reg.fpoff[s] = fp_base + r.bo0;
+  RegEntry& e = reg.e[s];
+  e.state = kStAccepted | (offloaded ? kStOffloaded : 0u);
+  e.nblk = r.n;
+  e.ntok = r.ntok;
+  e.chain = h;
+  e.fpoff = fp_base + r.bo0;
   atomicAdd((unsigned long long*)&ctr->reg_count, 1ull);
   Pend pe;
   pe.aux0 = h;
@@ -606,10 +670,10 @@ __global__ void __launch_bounds__(kThreads) k_restore_claims(BatchDev b, RegDev 
   cnt[c] = 0;
   if (r.malformed) return;
   const int64_t s = reg_find(reg, r.id);
-  if (s < 0 || !(reg.state[s] & kStOffloaded)) return;
-  atomicOr(reg.state + s, kStRestoreRequired);
+  if (s < 0 || !(reg.e[s].state & kStOffloaded)) return;
+  atomicOr(&reg.e[s].state, kStRestoreRequired);
   Pend pe;
-  pe.aux0 = reg.nblk[s];
+  pe.aux0 = reg.e[s].nblk;
   pe.aux1 = 0;
   pe.kinds = CLAIM_EV_RESTORE_REQUIRED;
   pe.j = kNone;
@@ -636,7 +700,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
                                                     Pend* __restrict__ pend) {
   __shared__ uint64_t tkey[kMaxBlockSize];
   load_token_keys(tkey, bs, seed);
-  const uint64_t c = ((uint64_t)blockIdx.x * kThreads + threadIdx.x) / W;
+  const uint64_t c = group_claim<W>();
   if (c >= b.C) return;
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t gl = lane & (W - 1), gbase = lane & ~(uint32_t)(W - 1);
@@ -658,11 +722,12 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       reasons |= CLAIM_R_NOT_ACCEPTED;
       special = kClaimLevelKey;
     } else {
-      state = reg.state[slot];
-      na = reg.nblk[slot];
-      acc_ntok = reg.ntok[slot];
-      acc_chain = reg.chain[slot];
-      fpo = reg.fpoff[slot];
+      const RegEntry& e = reg.e[slot];
+      state = e.state;
+      na = e.nblk;
+      acc_ntok = e.ntok;
+      acc_chain = e.chain;
+      fpo = e.fpoff;
       if (!(state & kStOffloaded)) {
         reasons |= CLAIM_R_NOT_OFFLOADED;
         special = kClaimLevelKey;
@@ -726,9 +791,16 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     }
     const uint64_t steps = j0 < nt ? (nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W) : 0;
     uint64_t my_h = 0;
-    for (uint32_t t = 0; t < steps; ++t) {
-      h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
-      if (gl == t) my_h = h;
+    if constexpr (W == 64) {  // one claim per wave: the chain runs on the scalar ALU
+      for (uint32_t t = 0; t < steps; ++t) {
+        h = splitmix_step(h ^ uniform_read64(m_sum, t));
+        if (gl == t) my_h = h;
+      }
+    } else {
+      for (uint32_t t = 0; t < steps; ++t) {
+        h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
+        if (gl == t) my_h = h;
+      }
     }
     const uint64_t rk = group_min64<W>(my_key);
     if (rk < best_pos) {
@@ -795,6 +867,54 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
 }
 
 // ------------------------------------------------------------ event append
+
+// Batches of up to kSmallEvents claims: one workgroup scans the per-claim
+// event counts, appends the events and advances the log, in one launch.
+constexpr uint32_t kSmallPer = 16;
+constexpr uint64_t kSmallEvents = 1024ull * kSmallPer;
+
+__global__ void __launch_bounds__(1024) k_events_small(const uint32_t* __restrict__ cnt,
+                                                       const Pend* __restrict__ pend,
+                                                       const uint64_t* __restrict__ ids, uint64_t C,
+                                                       Counters* __restrict__ ctr,
+                                                       claim_event* __restrict__ log) {
+  __shared__ uint32_t lds[17];
+  __shared__ uint64_t base_pos, base_seq;
+  if (threadIdx.x == 0) {
+    base_pos = ctr->log_count;
+    base_seq = ctr->seq_next;
+  }
+  const uint64_t first = (uint64_t)threadIdx.x * kSmallPer;
+  uint32_t v[kSmallPer];
+  uint32_t sum = 0;
+#pragma unroll
+  for (uint32_t k = 0; k < kSmallPer; ++k) {
+    v[k] = first + k < C ? cnt[first + k] : 0;
+    sum += v[k];
+  }
+  uint32_t total;
+  uint64_t pos = block_exclusive_scan_1024(sum, &total, lds);  // also orders base_* reads
+  for (uint32_t k = 0; k < kSmallPer; ++k) {
+    if (v[k] == 0) continue;
+    const uint64_t c = first + k;
+    const Pend pe = pend[c];
+    for (uint32_t e = 0; e < v[k]; ++e, ++pos) {
+      claim_event ev;
+      ev.seq = base_seq + pos;
+      ev.claim_id = ids[c];
+      ev.aux = e == 0 ? pe.aux0 : pe.aux1;
+      ev.kind = (pe.kinds >> (8 * e)) & 0xFFu;
+      ev.block_index = pe.j;
+      ev.phys_block = pe.phys;
+      ev.reserved = 0;
+      log[base_pos + pos] = ev;
+    }
+  }
+  if (threadIdx.x == 0) {
+    ctr->log_count = base_pos + total;
+    ctr->seq_next = base_seq + total;
+  }
+}
 
 __global__ void __launch_bounds__(kThreads) k_tile_sums(const uint32_t* __restrict__ cnt,
                                                         uint64_t C, uint32_t* __restrict__ tsum) {
@@ -912,8 +1032,7 @@ struct claim_pool {
   uint32_t *uniq = nullptr, *slot_of = nullptr;
 
   uint64_t reg_mask = 0, max_claims = 0;
-  uint64_t *r_key = nullptr, *r_ntok = nullptr, *r_chain = nullptr, *r_fpoff = nullptr;
-  uint32_t *r_state = nullptr, *r_nblk = nullptr;
+  RegEntry* reg = nullptr;
   uint32_t* fp_store = nullptr;
   uint64_t max_fp = 0, fp_used = 0;
   uint64_t staged_blocks = 0;  // blocks written by the last staged offload
@@ -991,6 +1110,13 @@ int fill(claim_pool* P, T* p, uint64_t n, T v) {
   return hip_status(hipGetLastError());
 }
 
+int fill_strided_u64(claim_pool* P, uint64_t* p, uint64_t n, uint32_t stride_words, uint64_t v) {
+  if (n == 0) return CLAIM_OK;
+  hipLaunchKernelGGL(k_fill_strided, dim3(grid_for(n, 4096)), dim3(kThreads), 0, P->stream, p, n,
+                     stride_words, v);
+  return hip_status(hipGetLastError());
+}
+
 uint64_t next_pow2(uint64_t x) {
   uint64_t p = 1;
   while (p < x) p <<= 1;
@@ -1022,12 +1148,7 @@ BatchDev batch_dev(const claim_batch* b) {
 RegDev reg_dev(claim_pool* P) {
   RegDev r;
   r.mask = P->reg_mask;
-  r.key = P->r_key;
-  r.state = P->r_state;
-  r.nblk = P->r_nblk;
-  r.ntok = P->r_ntok;
-  r.chain = P->r_chain;
-  r.fpoff = P->r_fpoff;
+  r.e = P->reg;
   r.fp = P->fp_store;
   return r;
 }
@@ -1145,7 +1266,7 @@ int launch_digest(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_
 }
 
 int launch_finalize(claim_pool* P, int mode, int staged) {
-  const uint32_t grid = P->nb / kThreads + 1 < 2048 ? P->nb / kThreads + 1 : 2048;
+  const uint32_t grid = P->nb / 4 + 1 < 8192 ? P->nb / 4 + 1 : 8192;
   hipLaunchKernelGGL(k_finalize, dim3(grid), dim3(kThreads), 0, P->stream, P->uniq, P->ctr,
                      P->partial, P->pgs, P->groups, mode, staged,
                      mode == 0 ? P->d_off : P->d_res, P->valid_off, P->load_failed, P->slot_of);
@@ -1156,6 +1277,11 @@ int launch_finalize(claim_pool* P, int mode, int staged) {
 int append_events(claim_pool* P, const claim_batch* b) {
   const uint64_t C = b->num_claims;
   if (C == 0) return CLAIM_OK;
+  if (C <= kSmallEvents) {
+    hipLaunchKernelGGL(k_events_small, dim3(1), dim3(1024), 0, P->stream, P->cnt, P->pend,
+                       b->claim_ids, C, P->ctr, P->log);
+    return hip_status(hipGetLastError());
+  }
   const uint64_t ntiles = (C + kTile - 1) / kTile;
   hipLaunchKernelGGL(k_tile_sums, dim3((uint32_t)ntiles), dim3(kThreads), 0, P->stream, P->cnt, C,
                      P->tsum);
@@ -1231,10 +1357,9 @@ int choose_digest_shape(claim_pool* P) {
 
 void free_pool(claim_pool* P) {
   if (!P) return;
-  void* ptrs[] = {P->d_off,    P->d_res,     P->partial,  P->valid_off, P->load_failed,
-                  P->mark,     P->uniq,      P->slot_of,  P->r_key,     P->r_ntok,
-                  P->r_chain,  P->r_fpoff,   P->r_state,  P->r_nblk,    P->fp_store,
-                  P->log,      P->ctr,       P->outcomes, P->cnt,       P->pend,
+  void* ptrs[] = {P->d_off,    P->d_res,    P->partial, P->valid_off, P->load_failed,
+                  P->mark,     P->uniq,     P->slot_of, P->reg,       P->fp_store,
+                  P->log,      P->ctr,      P->outcomes, P->cnt,      P->pend,
                   P->tsum,     P->dup_table, P->f_blocks, P->f_bits};
   for (void* p : ptrs)
     if (p) dfree(p);
@@ -1333,16 +1458,13 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     if ((rc = dalloc(&P->d_off, nb)) || (rc = dalloc(&P->d_res, nb)) ||
         (rc = dalloc(&P->partial, (uint64_t)P->pgs * (nb + P->groups))) ||
         (rc = dalloc(&P->valid_off, nb)) ||
-        (rc = dalloc(&P->load_failed, nb)) || (rc = dalloc(&P->mark, nb)) ||
+        (rc = dalloc(&P->load_failed, nb)) || (rc = dalloc(&P->mark, (nb + 15) / 16 * 16)) ||
         (rc = dalloc(&P->uniq, nb)) || (rc = dalloc(&P->slot_of, nb)))
       break;
     P->max_claims = d->max_claims;
     const uint64_t cap = next_pow2(2 * d->max_claims);
     P->reg_mask = cap - 1;
-    if ((rc = dalloc(&P->r_key, cap)) || (rc = dalloc(&P->r_ntok, cap)) ||
-        (rc = dalloc(&P->r_chain, cap)) || (rc = dalloc(&P->r_fpoff, cap)) ||
-        (rc = dalloc(&P->r_state, cap)) || (rc = dalloc(&P->r_nblk, cap)))
-      break;
+    if ((rc = dalloc(&P->reg, cap))) break;
     P->max_fp = d->max_footprint;
     if ((rc = dalloc(&P->fp_store, d->max_footprint))) break;
     P->ev_cap = d->event_capacity;
@@ -1362,8 +1484,9 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     }
     if ((rc = fill<uint64_t>(P, P->d_off, nb, 0)) || (rc = fill<uint64_t>(P, P->d_res, nb, 0)) ||
         (rc = fill<uint8_t>(P, P->valid_off, nb, 0)) || (rc = fill<uint8_t>(P, P->load_failed, nb, 0)) ||
-        (rc = fill<uint8_t>(P, P->mark, nb, 0)) || (rc = fill<uint32_t>(P, P->slot_of, nb, kNone)) ||
-        (rc = fill<uint64_t>(P, P->r_key, cap, kEmptyId)) || (rc = fill<uint32_t>(P, P->r_state, cap, 0)))
+        (rc = fill<uint8_t>(P, P->mark, (nb + 15) / 16 * 16, 0)) || (rc = fill<uint32_t>(P, P->slot_of, nb, kNone)) ||
+        (rc = fill<uint64_t>(P, (uint64_t*)P->reg, cap * (sizeof(RegEntry) / 8), 0)) ||
+        (rc = fill_strided_u64(P, (uint64_t*)P->reg, cap, sizeof(RegEntry) / 8, kEmptyId)))
       break;
     if ((rc = fill<uint64_t>(P, (uint64_t*)P->ctr, sizeof(Counters) / 8, 0))) break;
     if (hipStreamSynchronize(P->stream) != hipSuccess) { rc = CLAIM_EHIP; break; }
@@ -1512,7 +1635,13 @@ int claim_check(claim_pool* P, const claim_batch* b) {
     slot = P->t_head;
   }
   TRY(record_stage(P, slot, 0));
-  TRY(select_blocks(P, b, kMarkOffloaded));
+  if (b->num_refs) {
+    hipLaunchKernelGGL(k_mark_entries, dim3(grid_for(b->num_refs, 8192)), dim3(kThreads), 0,
+                       P->stream, b->block_ids, b->num_refs, P->nb, P->valid_off, P->mark);
+    HIP_TRY(hipGetLastError());
+  }
+  hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, P->stream, P->mark, P->nb, P->uniq, P->ctr);
+  HIP_TRY(hipGetLastError());
   TRY(record_stage(P, slot, 1));
   TRY(launch_digest(P, P->partial, nullptr));
   TRY(record_stage(P, slot, 2));
