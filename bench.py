@@ -96,6 +96,11 @@ def main() -> int:
     ap.add_argument("--workload", default="llama3-8b")
     ap.add_argument("--cpu-sample-blocks", type=int, default=512)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--round-trip", action="store_true",
+                    help="offload through pinned host staging, drop the device copy, restore from "
+                         "staging; time the two transfers separately from the on-device verify")
+    ap.add_argument("--stages", action="store_true",
+                    help="also time every stage of the check (two more hipEvents per stage)")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="run one plain device copy of this size first (counter calibration)")
     args = ap.parse_args()
@@ -152,9 +157,39 @@ def main() -> int:
     db = ck.DeviceBatch(batch, device=dev)
     steps, warm = args.steps, args.warmup
     pool = ck.Pool(g, w.seed, kv, stream=stream, max_claims=2 * C, max_footprint=2 * batch.num_refs,
-                   event_capacity=2 * C * (steps + warm + 2) + 4 * C, timing=True)
-    pool.offload(db)
-    pool.restore(db, faults=faults)
+                   event_capacity=2 * C * (steps + warm + 2) + 4 * C, timing=True,
+                   stage_timing=args.stages)
+    round_trip = None
+    if args.round_trip:
+        # the host-link leg of the lifecycle: gather + digest straight into
+        # pinned host memory, lose the device copy, scatter back from host
+        staging = torch.empty(U * g.block_bytes, dtype=torch.uint8, pin_memory=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pool.offload(db, staging=staging)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        kv.zero_()
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        pool.restore(db, staging=staging, faults=faults)
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        moved = U * g.block_bytes
+        round_trip = {
+            "staging": "pinned host memory (hipHostMalloc), written and read by the kernels",
+            "bytes": moved,
+            "offload_ms": round((t1 - t0) * 1e3, 3),
+            "offload_GBps": round(moved / (t1 - t0) / 1e9, 2),
+            "restore_ms": round((t3 - t2) * 1e3, 3),
+            "restore_GBps": round(moved / (t3 - t2) / 1e9, 2),
+            "note": "whole claim_offload / claim_restore calls (acceptance, digest, events "
+                    "included); the timed verify below runs on the restored pool",
+        }
+        del staging
+    else:
+        pool.offload(db)
+        pool.restore(db, faults=faults)
     pool.read(max_outcomes=1)
 
     for _ in range(warm):
@@ -209,7 +244,8 @@ def main() -> int:
         "pct_hbm_peak": round(100 * (phys_bytes + meta_bytes) / (ms_per_step * 1e-3) / 1e9
                               / HBM_PEAK_GBPS, 2),
         "stage_ms": {k: round(stages[k] / max(1, stages["calls"]), 4)
-                     for k in ("select_ms", "digest_ms", "finalize_ms", "claims_ms", "events_ms")},
+                     for k in (("select_ms", "digest_ms", "finalize_ms", "claims_ms", "events_ms")
+                               if args.stages else ("digest_ms",))},
         "outcomes": {"failed_closed": n_fail, "materialized": int((out["code"] == ck.MATERIALIZED).sum()),
                      "unknown": int((out["code"] == ck.UNKNOWN).sum())},
         "roofline": {
@@ -227,6 +263,8 @@ def main() -> int:
             "frac_of_read_ceiling": round(achieved / read_ceiling, 4),
         },
     }
+    if round_trip is not None:
+        line["round_trip"] = round_trip
     if not args.no_cpu_baseline:
         base, want = cpu_baseline(w, batch, faults, args.cpu_sample_blocks)
         line["cpu_baseline"] = base

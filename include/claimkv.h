@@ -106,7 +106,8 @@ extern "C" {
 #define CLAIM_NONE 0xFFFFFFFFu                   /* no position; missing block-table entry */
 #define CLAIM_RESERVED_ID 0xFFFFFFFFFFFFFFFFull /* never a valid claim id */
 
-#define CLAIM_POOL_TIMING 0x1u /* desc.flags: record per-stage hipEvents in claim_check */
+#define CLAIM_POOL_TIMING 0x1u       /* desc.flags: time the digest kernel of every claim_check */
+#define CLAIM_POOL_STAGE_TIMING 0x2u /* desc.flags: also time every other stage (adds ~14 us per check) */
 
 typedef struct claim_pool claim_pool;
 
@@ -197,16 +198,19 @@ typedef struct claim_event {
 } claim_event;
 
 /* Stage times of the claim_check calls queued since the last
- * claim_timing_read (pools created with CLAIM_POOL_TIMING). */
+ * claim_timing_read, measured with hipEvents on the pool's stream.  With
+ * CLAIM_POOL_TIMING only digest_ms is filled (two events per check around
+ * the gather + digest kernel); with CLAIM_POOL_STAGE_TIMING as well, every
+ * field. */
 typedef struct claim_timing {
   uint32_t calls;          /* checks measured */
   uint32_t last_unique;    /* unique blocks digested by the last check */
-  double total_ms;         /* sum over calls: whole check */
+  double total_ms;         /* sum over calls: whole check (stage timing) */
   double digest_ms;        /* sum over calls: the gather + digest kernel */
-  double select_ms;        /* sum over calls: unique-block selection */
-  double finalize_ms;      /* sum over calls: per-block digest combine */
-  double claims_ms;        /* sum over calls: chain, compare, min-reduction, outcomes */
-  double events_ms;        /* sum over calls: event scan and append */
+  double select_ms;        /* sum over calls: unique-block selection (stage timing) */
+  double finalize_ms;      /* sum over calls: per-block digest combine (stage timing) */
+  double claims_ms;        /* sum over calls: chain, compare, min-reduction, outcomes (stage timing) */
+  double events_ms;        /* sum over calls: event scan and append (stage timing) */
 } claim_timing;
 
 /* Create a pool over caller-owned KV memory (section 7: the connector's
@@ -273,7 +277,7 @@ int outcomes_read(claim_pool* pool, claim_outcome* out, uint32_t out_cap, uint32
 
 /* Wait for the pool's stream and return the summed stage times of the
  * checks queued since the previous call (EINVAL unless the pool was created
- * with CLAIM_POOL_TIMING). */
+ * with CLAIM_POOL_TIMING or CLAIM_POOL_STAGE_TIMING). */
 int claim_timing_read(claim_pool* pool, claim_timing* out);
 
 /* Wait for the pool's stream and copy the per-block state of blocks

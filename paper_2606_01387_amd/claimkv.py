@@ -30,6 +30,7 @@ EV_RESTORATION_FAILED, EV_ACTIVE_REQUEST_REFUSED, EV_OUTCOME_UNKNOWN = 5, 6, 7
 NONE = 0xFFFFFFFF
 RESERVED_ID = 0xFFFFFFFFFFFFFFFF
 POOL_TIMING = 0x1
+POOL_STAGE_TIMING = 0x2
 
 OUTCOME_DTYPE = np.dtype(
     [("claim_id", "<u8"), ("code", "<u4"), ("first_failing_block", "<u4"), ("phys_block", "<u4"),
@@ -183,7 +184,8 @@ class Pool:
     out [plane][block][chunk]."""
 
     def __init__(self, geometry, seed: int, kv, *, stream=None, max_claims: int = 1 << 16,
-                 max_footprint: int = 1 << 22, event_capacity: int = 1 << 20, timing: bool = False):
+                 max_footprint: int = 1 << 22, event_capacity: int = 1 << 20, timing: bool = False,
+                 stage_timing: bool = False):
         torch = _torch()
         if not kv.is_cuda or not kv.is_contiguous():
             raise ValueError("kv must be a contiguous device tensor")
@@ -197,7 +199,8 @@ class Pool:
             num_layers=geometry.num_layers, planes_per_layer=geometry.planes_per_layer,
             block_size=geometry.block_size, num_kv_heads=geometry.num_kv_heads,
             head_dim=geometry.head_dim, elem_bytes=geometry.elem_bytes,
-            num_blocks=geometry.num_blocks, flags=POOL_TIMING if timing else 0, seed=seed,
+            num_blocks=geometry.num_blocks,
+            flags=(POOL_TIMING if timing else 0) | (POOL_STAGE_TIMING if stage_timing else 0), seed=seed,
             kv_base=kv.data_ptr(), kv_bytes=kv.numel() * kv.element_size(),
             stream=stream.cuda_stream, max_claims=max_claims, max_footprint=max_footprint,
             event_capacity=event_capacity)

@@ -1379,22 +1379,27 @@ int read_counters(claim_pool* P) {
 // Fold the oldest recorded check's stage times into the accumulator.
 int fold_timing_slot(claim_pool* P) {
   const int i = (P->t_head - P->t_count + kTimingSlots) % kTimingSlots;
-  HIP_TRY(hipEventSynchronize(P->tev[i][kStages - 1]));
-  float ms[kStages - 1];
-  for (int s = 0; s + 1 < kStages; ++s) HIP_TRY(hipEventElapsedTime(&ms[s], P->tev[i][s], P->tev[i][s + 1]));
+  const bool stages = P->flags & CLAIM_POOL_STAGE_TIMING;
+  HIP_TRY(hipEventSynchronize(P->tev[i][stages ? kStages - 1 : 2]));
+  float ms[kStages - 1] = {0, 0, 0, 0, 0};
+  for (int s = 0; s + 1 < kStages; ++s)
+    if (stages || s == 1) HIP_TRY(hipEventElapsedTime(&ms[s], P->tev[i][s], P->tev[i][s + 1]));
   P->t_acc.calls += 1;
   P->t_acc.select_ms += ms[0];
   P->t_acc.digest_ms += ms[1];
   P->t_acc.finalize_ms += ms[2];
   P->t_acc.claims_ms += ms[3];
   P->t_acc.events_ms += ms[4];
-  P->t_acc.total_ms += ms[0] + ms[1] + ms[2] + ms[3] + ms[4];
+  if (stages) P->t_acc.total_ms += ms[0] + ms[1] + ms[2] + ms[3] + ms[4];
   P->t_count -= 1;
   return CLAIM_OK;
 }
 
+// Stage events: 0 start, 1 selected, 2 digested, 3 finalized, 4 claims,
+// 5 events.  Plain timing records only 1 and 2 (around the digest kernel).
 int record_stage(claim_pool* P, int slot, int stage) {
   if (!(P->flags & CLAIM_POOL_TIMING)) return CLAIM_OK;
+  if (!(P->flags & CLAIM_POOL_STAGE_TIMING) && stage != 1 && stage != 2) return CLAIM_OK;
   return hip_status(hipEventRecord(P->tev[slot][stage], P->stream));
 }
 
@@ -1421,7 +1426,7 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
       d->block_size == 0 || d->block_size > kMaxBlockSize || d->num_kv_heads == 0 ||
       d->head_dim == 0 || d->elem_bytes == 0 || d->num_blocks == 0 || d->num_blocks >= kNone ||
       !d->kv_base || ((uintptr_t)d->kv_base & 15) || d->max_claims == 0 ||
-      d->event_capacity == 0 || (d->flags & ~CLAIM_POOL_TIMING))
+      d->event_capacity == 0 || (d->flags & ~(CLAIM_POOL_TIMING | CLAIM_POOL_STAGE_TIMING)))
     return CLAIM_EINVAL;
   const uint64_t planes = (uint64_t)d->num_layers * d->planes_per_layer;
   const uint64_t chunk = (uint64_t)d->block_size * d->num_kv_heads * d->head_dim * d->elem_bytes;
@@ -1444,6 +1449,7 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     P->cus = cus > 0 ? (uint32_t)cus : 256;
     P->stream = (hipStream_t)d->stream;
     P->flags = d->flags;
+    if (P->flags & CLAIM_POOL_STAGE_TIMING) P->flags |= CLAIM_POOL_TIMING;
     P->planes = (uint32_t)planes;
     P->bs = d->block_size;
     P->nb = d->num_blocks;

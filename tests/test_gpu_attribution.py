@@ -1,0 +1,121 @@
+"""Claim attribution and false-positive controls at scale, on the GPU.
+
+The paper's section 7 path C and its Table 8 / Table 9 controls as a
+property test over many seeded pools: each pool has silently corrupted
+blocks (referenced or not), reported load failures, flips that cancel, and
+blocks no claim references.  For every seed the GPU result must equal the
+oracle's bit for bit, and the outcomes must satisfy the paper's attribution
+rules against a failing set computed by comparing bytes:
+
+* a claim fails closed iff one of its own blocks is in the failing set
+  (target-only attribution; unclaimed and wrong-claim failures never count);
+* every ACTIVE_REQUEST_REFUSED names its own claim as the blocking claim and
+  follows that claim's RESTORATION_FAILED;
+* a claim none of whose blocks failed is MATERIALIZED (generic failure
+  elsewhere in the pool does not touch it).
+"""
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2606_01387_amd.synth import FaultSpec, Geometry, Workload, content, make_batch, make_faults
+from tests.helpers import apply_flips, digests
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+
+    assert t.cuda.is_available()
+    return t
+
+
+@pytest.fixture(scope="module")
+def ck():
+    from paper_2606_01387_amd import claimkv
+
+    claimkv.lib()
+    return claimkv
+
+
+def seeded(seed):
+    w = Workload(
+        name=f"attribution-{seed}", geometry=Geometry(2, 2, 16, 2, 32, 2, 400), seed=9000 + seed,
+        num_claims=120, length=("blocks", 1, 6, True), sharing=("zipf", 1.2, 6),
+        corrupt_rate=0.05, num_load_failed=4, gen_seed=seed * 31 + 1, content_seed=seed * 17 + 3)
+    batch = make_batch(w)
+    f = make_faults(w, batch)
+    rng = np.random.default_rng(seed)
+    # a flip applied twice cancels; a second flip in an already corrupted block
+    b0, bit0 = int(f.flip_blocks[0]), int(rng.integers(0, 8 * w.geometry.block_bytes))
+    # and one flip in a block no claim references (an unclaimed failure)
+    unref = np.setdiff1d(np.arange(w.geometry.num_blocks), batch.unique_blocks(w.geometry.num_blocks))
+    assert unref.size, "the pool must have unreferenced blocks"
+    bu = int(rng.choice(unref))
+    blocks = np.concatenate([f.flip_blocks, [b0, b0, bu]]).astype(np.uint32)
+    bits = np.concatenate([f.flip_bits, [bit0, bit0, 12345]]).astype(np.uint64)
+    return w, batch, FaultSpec(blocks, bits, f.load_failed)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_attribution_and_controls(torch, ck, seed):
+    w, batch, faults = seeded(seed)
+    g = w.geometry
+    print(f"attribution seed {seed}: {batch.num_claims} claims, "
+          f"{batch.unique_blocks(g.num_blocks).size}/{g.num_blocks} blocks referenced", flush=True)
+    kv = torch.empty(g.pool_bytes, dtype=torch.uint8, device="cuda")
+    content.fill_pool_gpu(kv.data_ptr(), kv.numel(), g, w.content_seed,
+                          torch.cuda.current_stream().cuda_stream)
+    db = ck.DeviceBatch(batch)
+    with ck.Pool(g, w.seed, kv, max_claims=256, max_footprint=4096, event_capacity=4096) as pool:
+        pool.offload(db)
+        pool.restore(db, faults=faults)
+        pool.read(max_outcomes=1)
+        pool.check(db)
+        out, ev = pool.read()
+
+    host = content.pool_host(g, w.content_seed)
+    restored = apply_flips(host, w, faults)
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    op.offload(batch, digests(host, w))
+    op.restore(batch, faults.load_failed)
+    op.events(clear=True)
+    want = op.check(batch, digests(restored, w))
+    for f in want.dtype.names:
+        if f != "pad":
+            assert np.array_equal(out[f], want[f]), f
+    want_ev = op.events()
+    for f in ("seq", "claim_id", "aux", "kind", "block_index", "phys_block"):
+        assert np.array_equal(ev[f] - (ev["seq"][0] if f == "seq" else 0),
+                              want_ev[f] - (want_ev["seq"][0] if f == "seq" else 0)), f
+
+    # failing set by comparing bytes, plus reported failures
+    failing = set(int(b) for b in faults.load_failed)
+    for b in range(g.num_blocks):
+        if not np.array_equal(O.canonical_block(host, g.planes, g.num_blocks, g.chunk_bytes, b),
+                              O.canonical_block(restored, g.planes, g.num_blocks, g.chunk_bytes, b)):
+            failing.add(b)
+    assert int(faults.flip_blocks[0]) in failing  # the cancelled pair left the first flip
+    referenced = set(int(b) for b in batch.unique_blocks(g.num_blocks))
+    assert failing - referenced, "the seed must also exercise unclaimed failures"
+
+    for c in range(batch.num_claims):
+        cid, blks, _ = batch.claim(c)
+        own = [j for j, b in enumerate(blks) if int(b) in failing]
+        if own:
+            assert out[c]["code"] == ck.RESTORE_FAILED_FAIL_CLOSED
+            assert out[c]["first_failing_block"] == own[0]
+        else:
+            assert out[c]["code"] == ck.MATERIALIZED
+    failed_ids = {int(x) for x in out["claim_id"][out["code"] == ck.RESTORE_FAILED_FAIL_CLOSED]}
+    for i, e in enumerate(ev):
+        if e["kind"] == ck.EV_ACTIVE_REQUEST_REFUSED:
+            assert int(e["aux"]) == int(e["claim_id"]) and int(e["claim_id"]) in failed_ids
+            prev = ev[i - 1]
+            assert prev["kind"] == ck.EV_RESTORATION_FAILED and prev["claim_id"] == e["claim_id"]
+        if e["kind"] == ck.EV_RESTORATION_FAILED:
+            assert int(e["claim_id"]) in failed_ids
+    del kv
