@@ -102,6 +102,7 @@ extern "C" {
 #define CLAIM_R_MALFORMED 0x200         /* offsets inconsistent, or reserved id */
 #define CLAIM_R_LOAD_FAILED 0x400       /* reported load failure */
 #define CLAIM_R_DIGEST_MISMATCH 0x800   /* restored digest != offload digest */
+#define CLAIM_R_BEYOND_PREDICATE 0x1000 /* a failed block lies past the predicate (not a failure) */
 
 #define CLAIM_NONE 0xFFFFFFFFu                   /* no position; missing block-table entry */
 #define CLAIM_RESERVED_ID 0xFFFFFFFFFFFFFFFFull /* never a valid claim id */
@@ -141,7 +142,16 @@ typedef struct claim_pool_desc {
  * tokens[token_offsets[c] .. token_offsets[c+1]).  Rows whose offsets run
  * backwards or past num_refs / num_tokens, or whose id is
  * CLAIM_RESERVED_ID, are malformed: never accepted, UNKNOWN at check.
- * Claim ids are stable and distinct from request ids (Table 5). */
+ * Claim ids are stable and distinct from request ids (Table 5).
+ *
+ * predicate_tokens gives each claim's materialization predicate
+ * leading_prefix_at_least(k) (section 1 running example, k = 448; Table 5
+ * fixed predicate): the claim is materialized when the blocks holding its
+ * first k tokens (ceil(k / block_size) leading block-table positions) are
+ * restored intact.  It is read by claim_offload only and fixed at
+ * acceptance; NULL, or k >= the claim's tokens, means the whole claim.  A
+ * failed block past the predicate does not fail the claim (it sets
+ * CLAIM_R_BEYOND_PREDICATE); ambiguity anywhere still gives UNKNOWN. */
 typedef struct claim_batch {
   uint32_t num_claims;
   uint32_t reserved; /* must be 0 */
@@ -152,6 +162,7 @@ typedef struct claim_batch {
   const uint32_t* block_ids;     /* [num_refs] */
   const uint64_t* token_offsets; /* [num_claims + 1] */
   const uint32_t* tokens;        /* [num_tokens] */
+  const uint64_t* predicate_tokens; /* [num_claims] or NULL: see below */
 } claim_batch;
 
 /* Faults applied by claim_restore (host memory, read before it returns).
@@ -175,7 +186,7 @@ typedef struct claim_outcome {
   uint32_t phys_block;          /* block-table entry at j* (CLAIM_NONE if j* >= blocks) */
   uint32_t num_blocks;          /* block-table entries presented (0 if malformed) */
   uint32_t reasons;             /* OR of CLAIM_R_* found anywhere in the claim */
-  uint32_t reserved;
+  uint32_t intact_blocks;       /* leading positions with no problem at all (<= num_blocks) */
   uint64_t expected_digest;     /* offload digest at j* (failures only, else 0) */
   uint64_t observed_digest;     /* restored digest at j* (failures only, else 0) */
   uint64_t chain_hash;          /* h_{nt-1} of the presented tokens (S if none) */

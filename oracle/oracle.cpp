@@ -96,7 +96,7 @@ uint64_t token_multilinear(const uint32_t* tok, uint64_t n, uint64_t seed) {
   return m_sum;
 }
 
-uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+uint64_t ceil_div(uint64_t a, uint64_t b) { return a / b + (a % b != 0); }
 
 /* Chain over a claim's tokens: h_{-1} = S, h_j = splitmix64(h_{j-1} ^ M_j).
  * Writes h_0 .. h_{nt-1} (nt = ceil(ntok / bs)) and returns h_{nt-1}, or S
@@ -152,6 +152,7 @@ enum {
   R_MALFORMED = 0x200,
   R_LOAD_FAILED = 0x400,
   R_DIGEST_MISMATCH = 0x800,
+  R_BEYOND_PREDICATE = 0x1000,
 };
 
 enum { ORC_OK = 0, ORC_EINVAL = -1, ORC_EDUP = -5 };
@@ -168,7 +169,7 @@ typedef struct orc_outcome {
   uint32_t phys_block;
   uint32_t num_blocks;
   uint32_t reasons;
-  uint32_t pad;
+  uint32_t intact_blocks;
   uint64_t expected_digest;
   uint64_t observed_digest;
   uint64_t chain_hash;
@@ -194,6 +195,7 @@ struct Claim {
   std::vector<uint32_t> footprint;
   uint64_t n_tokens;
   uint64_t chain_hash;
+  uint32_t pred_blocks; /* leading positions the predicate covers */
 };
 
 struct Pool {
@@ -326,7 +328,8 @@ void orc_pool_free(void* handle) { delete static_cast<Pool*>(handle); }
  * is marked OFFLOADED. */
 int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num_tokens,
                 const uint64_t* ids, const uint32_t* blk_off, const uint32_t* blk_ids,
-                const uint64_t* tok_off, const uint32_t* tokens, const uint64_t* digest_now) {
+                const uint64_t* tok_off, const uint32_t* tokens, const uint64_t* predicate_tokens,
+                const uint64_t* digest_now) {
   Pool* p = static_cast<Pool*>(handle);
   Batch bt = {num_claims, num_refs, num_tokens, ids, blk_off, blk_ids, tok_off, tokens};
 
@@ -349,6 +352,11 @@ int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
     cl.footprint.assign(fp, fp + n);
     cl.n_tokens = ntok;
     cl.chain_hash = chain(tokens + tok_off[c], ntok, p->block_size, p->seed, nullptr);
+    /* leading_prefix_at_least(k): the blocks holding the first k tokens;
+     * no predicate array means the whole claim */
+    cl.pred_blocks = n;
+    if (predicate_tokens && ceil_div(predicate_tokens[c], p->block_size) < n)
+      cl.pred_blocks = (uint32_t)ceil_div(predicate_tokens[c], p->block_size);
     p->registry[ids[c]] = cl;
     append_event(p, ids[c], EV_ACCEPTED, kNone, kNone, cl.chain_hash);
 
@@ -403,7 +411,10 @@ int orc_restore(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
  *
  * Every failure or ambiguity is a key (class << 32 | position); class 0 is
  * an ambiguity (no claim outcome), class 1 a restoration failure, and a
- * claim-level ambiguity sits at position NONE.  The smallest key decides:
+ * claim-level ambiguity sits at position NONE.  A failure beyond the
+ * claim's predicate (the leading blocks its accepted
+ * leading_prefix_at_least(k) covers, section 1 running example) is not a
+ * key: it only sets the BEYOND_PREDICATE reason.  The smallest key decides:
  * none -> MATERIALIZED, class 0 -> UNKNOWN, class 1 ->
  * RESTORE_FAILED_FAIL_CLOSED.  Events are appended in batch order. */
 int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num_tokens,
@@ -442,6 +453,8 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
     std::vector<uint64_t> h;
     uint64_t chain_hash = chain(tok, ntok, p->block_size, p->seed, &h);
     uint64_t nt = h.size();
+    uint32_t pred = n;       /* predicate coverage: accepted value, else the whole claim */
+    uint32_t intact = n;     /* first position with any problem, else n */
 
     if (!(reasons & R_MALFORMED)) {
       auto it = p->registry.find(ids[c]);
@@ -450,6 +463,7 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
         if (none_key < best) best = none_key;
       } else {
         const Claim& cl = it->second;
+        pred = cl.pred_blocks < n ? cl.pred_blocks : n;
         if (!(cl.state & ST_OFFLOADED)) {
           reasons |= R_NOT_OFFLOADED;
           if (none_key < best) best = none_key;
@@ -469,12 +483,14 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
             reasons |= R_FOOTPRINT_MISMATCH;
             uint64_t k = ((uint64_t)0 << 32) | j;
             if (k < best) best = k;
+            if (j < intact) intact = j;
           }
         }
         if (n != na) {
           reasons |= R_FOOTPRINT_MISMATCH;
           uint64_t k = ((uint64_t)0 << 32) | common;
           if (k < best) best = k;
+          if (common < intact) intact = common;
         }
       }
       if (n == 0) {
@@ -482,9 +498,11 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
         if (none_key < best) best = none_key;
       }
       if (n != nt) {
+        uint32_t q = (uint32_t)(n < nt ? n : nt);
         reasons |= R_SHAPE_MISMATCH;
-        uint64_t k = ((uint64_t)0 << 32) | (uint32_t)(n < nt ? n : nt);
+        uint64_t k = ((uint64_t)0 << 32) | q;
         if (k < best) best = k;
+        if (q < intact) intact = q;
       }
       for (uint32_t j = 0; j < n; ++j) {
         uint32_t b = fp[j];
@@ -492,13 +510,21 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
           reasons |= R_MISSING_ENTRY;
           uint64_t k = ((uint64_t)0 << 32) | j;
           if (k < best) best = k;
+          if (j < intact) intact = j;
         } else if (!p->valid_off[b]) {
           reasons |= R_NO_OFFLOAD_RECORD;
           uint64_t k = ((uint64_t)0 << 32) | j;
           if (k < best) best = k;
+          if (j < intact) intact = j;
         } else {
           bool lf = p->load_failed[b] != 0;
           bool mm = p->d_res[b] != p->d_off[b];
+          if ((lf || mm) && j < intact) intact = j;
+          if (j >= pred) {
+            /* beyond the predicate: the claimed prefix is intact */
+            if (lf || mm) reasons |= R_BEYOND_PREDICATE;
+            continue;
+          }
           if (lf) reasons |= R_LOAD_FAILED;
           if (mm) reasons |= R_DIGEST_MISMATCH;
           if (lf || mm) {
@@ -514,6 +540,7 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
     o.claim_id = ids[c];
     o.num_blocks = n;
     o.reasons = reasons;
+    o.intact_blocks = intact;
     o.chain_hash = chain_hash;
     if (best == ~0ull) {
       o.code = OUT_MATERIALIZED;
@@ -571,6 +598,14 @@ void orc_block_state(void* handle, uint64_t* d_off, uint64_t* d_res, uint8_t* va
 
 /* Registry state of one claim id: returns the state bits, or 0 if the id is
  * not registered. */
+/* Predicate coverage (leading positions) recorded for a claim at
+ * acceptance, or 0xFFFFFFFF if the id is not registered. */
+uint32_t orc_claim_predicate(void* handle, uint64_t id) {
+  Pool* p = static_cast<Pool*>(handle);
+  auto it = p->registry.find(id);
+  return it == p->registry.end() ? kNone : it->second.pred_blocks;
+}
+
 uint32_t orc_claim_state(void* handle, uint64_t id) {
   Pool* p = static_cast<Pool*>(handle);
   auto it = p->registry.find(id);

@@ -32,7 +32,7 @@ OUTCOME_DTYPE = np.dtype(
         ("phys_block", "<u4"),
         ("num_blocks", "<u4"),
         ("reasons", "<u4"),
-        ("pad", "<u4"),
+        ("intact_blocks", "<u4"),
         ("expected_digest", "<u8"),
         ("observed_digest", "<u8"),
         ("chain_hash", "<u8"),
@@ -69,6 +69,7 @@ R_EMPTY = 0x100
 R_MALFORMED = 0x200
 R_LOAD_FAILED = 0x400
 R_DIGEST_MISMATCH = 0x800
+R_BEYOND_PREDICATE = 0x1000
 OK, EINVAL, EDUP = 0, -1, -5
 
 
@@ -106,7 +107,7 @@ def lib() -> ctypes.CDLL:
             ("orc_apply_flip", [vp, u32, u32, u64, u32, u64], ctypes.c_int),
             ("orc_pool_new", [u32, u32, u64], vp),
             ("orc_pool_free", [vp], None),
-            ("orc_offload", [vp, u32, u64, u64, vp, vp, vp, vp, vp, vp], ctypes.c_int),
+            ("orc_offload", [vp, u32, u64, u64, vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
             ("orc_restore", [vp, u32, u64, u64, vp, vp, vp, vp, vp, u32, vp], ctypes.c_int),
             ("orc_check", [vp, u32, u64, u64, vp, vp, vp, vp, vp, vp, vp], ctypes.c_int),
             ("orc_num_events", [vp], u64),
@@ -114,6 +115,7 @@ def lib() -> ctypes.CDLL:
             ("orc_events_clear", [vp], None),
             ("orc_block_state", [vp, vp, vp, vp, vp], None),
             ("orc_claim_state", [vp, u64], u32),
+            ("orc_claim_predicate", [vp, u64], u32),
         ]:
             f = getattr(L, name)
             f.argtypes = args
@@ -242,10 +244,14 @@ class OraclePool:
         return keep, [ids.size, bi.size, tk.size, _ptr(ids), _ptr(bo), _ptr(bi), _ptr(to), _ptr(tk)]
 
     def offload(self, batch, digest_now: np.ndarray) -> int:
+        """Accept and offload; ``batch.predicate_tokens`` (optional, u64 per
+        claim) sets each claim's leading_prefix_at_least(k)."""
         keep, args = self._batch_args(batch)
         d = _arr(digest_now, np.uint64)
         assert d.size == self.num_blocks
-        return lib().orc_offload(self._h, *args, _ptr(d))
+        pred = getattr(batch, "predicate_tokens", None)
+        pred = None if pred is None else _arr(pred, np.uint64)
+        return lib().orc_offload(self._h, *args, _ptr(pred), _ptr(d))
 
     def restore(self, batch, load_failed_blocks=()) -> int:
         keep, args = self._batch_args(batch)
@@ -282,3 +288,6 @@ class OraclePool:
 
     def claim_state(self, claim_id: int) -> int:
         return lib().orc_claim_state(self._h, claim_id)
+
+    def claim_predicate(self, claim_id: int) -> int:
+        return lib().orc_claim_predicate(self._h, claim_id)

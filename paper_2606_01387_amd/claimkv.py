@@ -27,6 +27,7 @@ OK, EINVAL, ENOMEM, EHIP, ENOSPC, EDUP = 0, -1, -2, -3, -4, -5
 UNKNOWN, MATERIALIZED, RESTORE_FAILED_FAIL_CLOSED = 0, 1, 2
 EV_ACCEPTED, EV_OFFLOADED, EV_RESTORE_REQUIRED, EV_RESTORED = 1, 2, 3, 4
 EV_RESTORATION_FAILED, EV_ACTIVE_REQUEST_REFUSED, EV_OUTCOME_UNKNOWN = 5, 6, 7
+R_BEYOND_PREDICATE = 0x1000
 NONE = 0xFFFFFFFF
 RESERVED_ID = 0xFFFFFFFFFFFFFFFF
 POOL_TIMING = 0x1
@@ -34,7 +35,7 @@ POOL_STAGE_TIMING = 0x2
 
 OUTCOME_DTYPE = np.dtype(
     [("claim_id", "<u8"), ("code", "<u4"), ("first_failing_block", "<u4"), ("phys_block", "<u4"),
-     ("num_blocks", "<u4"), ("reasons", "<u4"), ("reserved", "<u4"), ("expected_digest", "<u8"),
+     ("num_blocks", "<u4"), ("reasons", "<u4"), ("intact_blocks", "<u4"), ("expected_digest", "<u8"),
      ("observed_digest", "<u8"), ("chain_hash", "<u8"), ("chain_hash_at_fail", "<u8")])
 EVENT_DTYPE = np.dtype(
     [("seq", "<u8"), ("claim_id", "<u8"), ("aux", "<u8"), ("kind", "<u4"), ("block_index", "<u4"),
@@ -61,7 +62,7 @@ class CBatch(ctypes.Structure):
                 ("num_refs", ctypes.c_uint64), ("num_tokens", ctypes.c_uint64),
                 ("claim_ids", ctypes.c_void_p), ("block_offsets", ctypes.c_void_p),
                 ("block_ids", ctypes.c_void_p), ("token_offsets", ctypes.c_void_p),
-                ("tokens", ctypes.c_void_p)]
+                ("tokens", ctypes.c_void_p), ("predicate_tokens", ctypes.c_void_p)]
 
 
 class CFaults(ctypes.Structure):
@@ -77,7 +78,7 @@ class CTiming(ctypes.Structure):
                 ("claims_ms", ctypes.c_double), ("events_ms", ctypes.c_double)]
 
 
-assert ctypes.sizeof(PoolDesc) == 88 and ctypes.sizeof(CBatch) == 64
+assert ctypes.sizeof(PoolDesc) == 88 and ctypes.sizeof(CBatch) == 72
 assert OUTCOME_DTYPE.itemsize == 64 and EVENT_DTYPE.itemsize == 40
 
 
@@ -146,7 +147,8 @@ class DeviceBatch:
 
     ``batch`` is any object with numpy arrays ``claim_ids`` (u64),
     ``block_offsets`` (u32), ``block_ids`` (u32), ``token_offsets`` (u64)
-    and ``tokens`` (u32)."""
+    and ``tokens`` (u32), and optionally ``predicate_tokens`` (u64 per claim
+    or None)."""
 
     def __init__(self, batch, device="cuda"):
         torch = _torch()
@@ -162,13 +164,21 @@ class DeviceBatch:
         self.bi = up(batch.block_ids, np.uint32, torch.int32)
         self.to = up(batch.token_offsets, np.uint64, torch.int64)
         self.tok = up(batch.tokens, np.uint32, torch.int32)
+        pred = getattr(batch, "predicate_tokens", None)
+        self.pred = None if pred is None else up(pred, np.uint64, torch.int64)
         n_claims = int(self.ids.numel())
+        # the kernels read offsets[c + 1] and predicate[c] for every claim c
+        if n_claims and (self.bo.numel() != n_claims + 1 or self.to.numel() != n_claims + 1):
+            raise ValueError("block_offsets and token_offsets need num_claims + 1 entries")
+        if self.pred is not None and self.pred.numel() != n_claims:
+            raise ValueError("predicate_tokens needs one entry per claim")
         self.struct = CBatch(
             num_claims=n_claims, reserved=0, num_refs=int(self.bi.numel()),
             num_tokens=int(self.tok.numel()),
             claim_ids=self.ids.data_ptr() or None, block_offsets=self.bo.data_ptr() or None,
             block_ids=self.bi.data_ptr() or None, token_offsets=self.to.data_ptr() or None,
-            tokens=self.tok.data_ptr() or None)
+            tokens=self.tok.data_ptr() or None,
+            predicate_tokens=(self.pred.data_ptr() or None) if self.pred is not None else None)
 
     @property
     def num_claims(self) -> int:

@@ -149,6 +149,7 @@ struct BatchDev {
   const uint32_t* bi;
   const uint64_t* to;
   const uint32_t* tok;
+  const uint64_t* pred;  // predicate tokens per claim, or null
 };
 
 struct RegEntry {  // one 64-byte line per slot: a probe touches one line
@@ -158,7 +159,9 @@ struct RegEntry {  // one 64-byte line per slot: a probe touches one line
   uint64_t ntok;    // accepted token count
   uint64_t chain;   // accepted chain hash h_{nt-1}
   uint64_t fpoff;   // accepted footprint: fp[fpoff .. fpoff + nblk)
-  uint64_t pad[3];
+  uint32_t pred;    // leading positions the accepted predicate covers
+  uint32_t pad0;
+  uint64_t pad[2];
 };
 
 struct RegDev {
@@ -610,6 +613,14 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, uin
   e.ntok = r.ntok;
   e.chain = h;
   e.fpoff = fp_base + r.bo0;
+  // leading_prefix_at_least(k): the blocks holding the first k tokens
+  uint32_t pred = r.n;
+  if (b.pred) {
+    const uint64_t k = b.pred[c];
+    const uint64_t kb = k / bs + (k % bs != 0);
+    if (kb < r.n) pred = (uint32_t)kb;
+  }
+  e.pred = pred;
   atomicAdd((unsigned long long*)&ctr->reg_count, 1ull);
   Pend pe;
   pe.aux0 = h;
@@ -711,7 +722,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   uint32_t reasons = 0;
   uint64_t special = kNoKey;  // claim-level and length keys
   int64_t slot = -1;
-  uint32_t na = 0, state = 0;
+  uint32_t na = 0, state = 0, pred = r.n;
   uint64_t acc_ntok = 0, acc_chain = 0, fpo = 0;
   if (r.malformed) {
     reasons |= CLAIM_R_MALFORMED;
@@ -725,6 +736,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       const RegEntry& e = reg.e[slot];
       state = e.state;
       na = e.nblk;
+      pred = e.pred < r.n ? e.pred : r.n;
       acc_ntok = e.ntok;
       acc_chain = e.chain;
       fpo = e.fpoff;
@@ -758,6 +770,9 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   const uint64_t q2 = (n != nt) ? (n < nt ? n : nt) : kNoKey;  // h may be needed
 
   uint64_t h = seed, best_pos = kNoKey, h_best = 0, h_q1 = 0, h_q2 = 0;
+  uint64_t intact = n;  // first position with any problem (lane-local, then group min)
+  if (q1 < intact) intact = q1;
+  if (q2 < intact) intact = q2;
   const uint64_t L = n > nt ? n : nt;
   for (uint64_t j0 = 0; j0 < L; j0 += W) {
     const uint64_t j = j0 + gl;
@@ -777,11 +792,18 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       } else {
         const bool lf = st.load_failed[blk] != 0;
         const bool mm = st.d_res[blk] != st.d_off[blk];
-        if (lf) reasons |= CLAIM_R_LOAD_FAILED;
-        if (mm) reasons |= CLAIM_R_DIGEST_MISMATCH;
-        const uint64_t k = (1ull << 32) | j;
-        if ((lf || mm) && k < my_key) my_key = k;
+        if ((lf || mm) && j < intact) intact = j;
+        if (j >= pred) {
+          // past the predicate: the claimed prefix is still intact
+          if (lf || mm) reasons |= CLAIM_R_BEYOND_PREDICATE;
+        } else {
+          if (lf) reasons |= CLAIM_R_LOAD_FAILED;
+          if (mm) reasons |= CLAIM_R_DIGEST_MISMATCH;
+          const uint64_t k = (1ull << 32) | j;
+          if ((lf || mm) && k < my_key) my_key = k;
+        }
       }
+      if (my_key != kNoKey && j < intact) intact = j;
     }
     uint64_t m_sum = 0;
     if (j < nt) {
@@ -815,6 +837,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     special = kClaimLevelKey < special ? kClaimLevelKey : special;
   }
   reasons = group_or<W>(reasons);
+  intact = group_min64<W>(intact);
   if (gl != 0) return;
 
   const uint64_t best = best_pos < special ? best_pos : special;
@@ -822,7 +845,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   o.claim_id = r.id;
   o.num_blocks = r.n;
   o.reasons = reasons;
-  o.reserved = 0;
+  o.intact_blocks = (uint32_t)intact;
   o.expected_digest = 0;
   o.observed_digest = 0;
   o.chain_hash = h;
@@ -1142,6 +1165,7 @@ BatchDev batch_dev(const claim_batch* b) {
   d.bi = b->block_ids;
   d.to = b->token_offsets;
   d.tok = b->tokens;
+  d.pred = b->predicate_tokens;
   return d;
 }
 

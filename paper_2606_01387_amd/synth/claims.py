@@ -32,6 +32,7 @@ class Batch:
     block_ids: np.ndarray  # u32 [N]
     token_offsets: np.ndarray  # u64 [C+1]
     tokens: np.ndarray  # u32 [T]
+    predicate_tokens: np.ndarray | None = None  # u64 [C]: leading_prefix_at_least(k)
 
     @property
     def num_claims(self) -> int:
@@ -54,7 +55,10 @@ class Batch:
     def subset(self, idx) -> "Batch":
         """A batch made of the listed claims, in the listed order."""
         parts = [self.claim(int(c)) for c in idx]
-        return from_claims(parts)
+        b = from_claims(parts)
+        if self.predicate_tokens is not None:
+            b.predicate_tokens = self.predicate_tokens[np.asarray(idx, dtype=np.int64)]
+        return b
 
     def unique_blocks(self, num_blocks: int) -> np.ndarray:
         b = self.block_ids[self.block_ids < num_blocks]
@@ -198,12 +202,21 @@ def make_batch(w: Workload) -> Batch:
         dup = np.setdiff1d(np.arange(C), first)
         ids[dup] = rng.integers(1, np.iinfo(np.int64).max, size=dup.size, dtype=np.int64)
 
+    pred = None
+    if w.predicate_fraction > 0:
+        # a fraction of the claims covers only a leading prefix: k uniform in
+        # [1, T_c]; the rest cover the whole claim
+        pred = T.astype(np.uint64).copy()
+        sel = rng.random(C) < w.predicate_fraction
+        pred[sel] = (1 + (rng.random(int(sel.sum())) * T[sel]).astype(np.int64)).astype(np.uint64)
+
     return Batch(
         claim_ids=ids,
         block_offsets=bo.astype(np.uint32),
         block_ids=blk.astype(np.uint32),
         token_offsets=to.astype(np.uint64),
         tokens=tok.astype(np.uint32),
+        predicate_tokens=pred,
     )
 
 

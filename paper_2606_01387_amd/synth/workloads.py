@@ -67,6 +67,7 @@ class Workload:
     corrupt_rate: float  # fraction of pool blocks with one flipped bit
     missing_claim_rate: float = 0.0  # fraction of claims with one missing entry
     num_load_failed: int = 0  # reported load failures (referenced blocks)
+    predicate_fraction: float = 0.0  # claims whose predicate covers only a prefix
     gen_seed: int = 0  # seed of the claim / fault generator
     content_seed: int = 0  # seed of the pool content generator
     vocab: int = 32000

@@ -72,8 +72,6 @@ def gpu_pool_tensor(torch, w: Workload):
 def same_outcomes(got, want):
     assert len(got) == len(want)
     for f in OUT_FIELDS:
-        if f == "reserved":
-            continue
         if not np.array_equal(got[f], want[f]):
             bad = np.flatnonzero(got[f] != want[f])[:5]
             raise AssertionError(f"outcome field {f} differs at claims {bad.tolist()}: "
@@ -83,8 +81,6 @@ def same_outcomes(got, want):
 def same_events(got, want):
     assert len(got) == len(want), (len(got), len(want))
     for f in EV_FIELDS:
-        if f == "reserved":
-            continue
         if not np.array_equal(got[f], want[f]):
             bad = np.flatnonzero(got[f] != want[f])[:5]
             raise AssertionError(f"event field {f} differs at {bad.tolist()}: "
@@ -133,6 +129,15 @@ SCALED = [
     RAGGED,
     TINY_CHUNK,
     LONG_CLAIMS,
+    # leading_prefix_at_least(k) predicates on part of the claims: one-claim-
+    # per-wave groups, mid-size groups and two-lane groups
+    replace(LONG_CLAIMS, name="long-claims-predicate", num_claims=16, predicate_fraction=0.7,
+            missing_claim_rate=0.0, corrupt_rate=0.005, num_load_failed=1,
+            geometry=replace(LONG_CLAIMS.geometry, num_blocks=400)),
+    replace(scaled(FULL["llama3-8b"], 48, 60, corrupt_rate=0.25, num_load_failed=4,
+                   predicate_fraction=0.6), name="llama3-8b-predicate"),
+    replace(scaled(FULL["small-claim-stress"], 256, 30000, corrupt_rate=0.05, num_load_failed=3,
+                   predicate_fraction=0.5), name="stress-predicate"),
 ]
 
 
@@ -175,6 +180,12 @@ def test_parity_scaled_real_digests(torch, ck, w):
     assert np.array_equal(kv.cpu().numpy(), host)
     codes = np.bincount(out["code"], minlength=3)
     note(f"  outcomes unknown/materialized/failed = {codes.tolist()}")
+    if w.predicate_fraction:
+        # the case must reach the predicate's own branch: a claim that is
+        # materialized although one of its blocks failed past the predicate
+        beyond = (out["reasons"] & ck.R_BEYOND_PREDICATE) != 0
+        assert (beyond & (out["code"] == ck.MATERIALIZED)).any()
+        assert (out["intact_blocks"] <= out["num_blocks"]).all()
     del kv
     free_gpu(torch)
 
@@ -284,6 +295,18 @@ def test_controls_mirrored(torch, ck):
     m.restore(p, load_failed=[55])
     out = m.check(p)
     assert out[0]["first_failing_block"] == 27
+    # the same example with a longer claim and its predicate fixed at
+    # acceptance: a failure past block 28 leaves it materialized
+    tp = toks(36)
+    lp = from_claims([(0x44A, list(range(20, 56)), tp), (0x44B, list(range(20, 56)), tp)])
+    lp.predicate_tokens = np.array([448, 449], np.uint64)
+    m.offload(lp)
+    m.restore(lp, flips=[(48, 77)])
+    lp.predicate_tokens = None
+    out = m.check(lp)
+    assert out["code"].tolist() == [ck_.MATERIALIZED, ck_.RESTORE_FAILED_FAIL_CLOSED]
+    assert out["intact_blocks"].tolist() == [28, 28]
+    assert out[0]["reasons"] == ck_.R_BEYOND_PREDICATE
     # a later offload of a block clears its reported failure (fresh record)
     q = from_claims([(0x449, [55], toks(1))])
     m.offload(q)
@@ -462,5 +485,11 @@ def test_full_size_parity(torch, ck, name):
     assert st["valid_off"][ref].all()
     codes = np.bincount(out["code"], minlength=3)
     note(f"  outcomes unknown/materialized/failed = {codes.tolist()}")
+    if w.predicate_fraction:
+        # the case must reach the predicate's own branch: a claim that is
+        # materialized although one of its blocks failed past the predicate
+        beyond = (out["reasons"] & ck.R_BEYOND_PREDICATE) != 0
+        assert (beyond & (out["code"] == ck.MATERIALIZED)).any()
+        assert (out["intact_blocks"] <= out["num_blocks"]).all()
     del kv, db
     free_gpu(torch)

@@ -7,6 +7,7 @@ oracle's min-reduction: sequential scans, enumeration, memcmp brute force.
 """
 
 import itertools
+from dataclasses import replace
 
 import numpy as np
 import pytest
@@ -321,6 +322,125 @@ def test_predicate_prefix_of_running_example(d0):
     h = O.chain(tk, BS, TINY.seed)
     assert out["chain_hash_at_fail"] == h[27] and out["chain_hash"] == h[27]
     assert O.chain_hash(tk[: 27 * BS], BS, TINY.seed) == h[26]
+
+
+def _scan_with_predicate(state, pred_blocks):
+    """Expected (code, first_failing_block, beyond, intact) by a plain left to
+    right scan: any ambiguity ('m') decides UNKNOWN at its first position;
+    else the first failure ('f') among the predicate's leading blocks fails
+    the claim; failures past them leave it MATERIALIZED and only mark
+    BEYOND_PREDICATE; intact is the first position that is not 'o'."""
+    intact = next((j for j, s in enumerate(state) if s != "o"), len(state))
+    beyond = any(s == "f" for s in state[pred_blocks:])
+    if "m" in state:
+        return O.UNKNOWN, state.index("m"), beyond, intact
+    for j, s in enumerate(state[:pred_blocks]):
+        if s == "f":
+            return O.RESTORE_FAILED_FAIL_CLOSED, j, beyond, intact
+    return O.MATERIALIZED, NONE32, beyond, intact
+
+
+def test_predicate_enumeration_matches_sequential_scan():
+    """Every ok / failed / missing assignment to a claim of 1..5 blocks of 4
+    tokens, under every predicate length k from 0 tokens to past the claim:
+    the predicate covers ceil(k / 4) leading blocks (section 1 running
+    example: the blocks holding the first k tokens)."""
+    nb, bs = 16, 4
+    base = np.arange(nb, dtype=np.uint64) * np.uint64(1000003) + np.uint64(17)
+    for n in range(1, 6):
+        for state in itertools.product("ofm", repeat=n):
+            blocks = [j if s != "m" else MISSING for j, s in enumerate(state)]
+            after = base.copy()
+            for j, s in enumerate(state):
+                if s == "f":
+                    after[j] ^= np.uint64(1 << (j % 64))
+            for k in range(0, bs * n + 3):
+                b = from_claims([(42, blocks, np.arange(n * bs, dtype=np.uint32))])
+                b.predicate_tokens = np.array([k], np.uint64)
+                op = O.OraclePool(nb, bs, 77)
+                assert op.offload(b, base) == O.OK
+                assert op.restore(b) == O.OK
+                out = op.check(b, after)[0]
+                pred_blocks = min(-(-k // bs), n)
+                assert op.claim_predicate(42) == pred_blocks
+                code, first, beyond, intact = _scan_with_predicate(state, pred_blocks)
+                got = (int(out["code"]), int(out["first_failing_block"]),
+                       bool(out["reasons"] & O.R_BEYOND_PREDICATE), int(out["intact_blocks"]))
+                assert got == (code, first, beyond, intact), (state, k)
+                # a failure inside the predicate is the only source of these bits
+                assert bool(out["reasons"] & O.R_DIGEST_MISMATCH) == ("f" in state[:pred_blocks])
+
+
+def test_predicate_running_example_on_a_longer_claim(d0):
+    """A 36-block claim whose predicate is leading_prefix_at_least(448): only
+    the first 28 blocks decide.  A lost block 30 leaves the claim
+    MATERIALIZED (path A events) with the loss recorded as beyond the
+    predicate and 30 intact leading blocks; a lost block 27 fails it (path
+    B); k = 449 stretches the predicate to block 28."""
+    rows = {r[0]: int(r[1]) for r in golden_lines("paper_event_paths.txt") if r[0].startswith("PRED")}
+    k = rows["PREDICATE_TOKENS"]
+    tk = toks(36)
+    cid = 0xC0DE
+    for pred_tokens, lost, want_code, want_first in [
+        (k, 30, O.MATERIALIZED, NONE32),
+        (k, 27, O.RESTORE_FAILED_FAIL_CLOSED, 27),
+        (k, 28, O.MATERIALIZED, NONE32),
+        (k + 1, 28, O.RESTORE_FAILED_FAIL_CLOSED, 28),
+    ]:
+        b = from_claims([(cid, list(range(36)), tk)])
+        b.predicate_tokens = np.array([pred_tokens], np.uint64)
+        op = fresh()
+        assert op.offload(b, d0) == O.OK
+        assert op.claim_predicate(cid) == -(-pred_tokens // BS)
+        op.restore(b, load_failed_blocks=[lost])
+        # the predicate was fixed at acceptance: the check's batch carries none
+        b.predicate_tokens = None
+        out = op.check(b, d0)[0]
+        assert (int(out["code"]), int(out["first_failing_block"])) == (want_code, want_first)
+        assert out["intact_blocks"] == lost
+        if want_code == O.MATERIALIZED:
+            assert out["reasons"] == O.R_BEYOND_PREDICATE
+            assert kinds_for(op.events(), cid) == PATHS["A"]
+        else:
+            assert out["reasons"] == O.R_LOAD_FAILED
+            assert kinds_for(op.events(), cid) == PATHS["B"]
+
+
+def test_predicate_of_section_6_2(d0):
+    """leading_prefix_at_least(17) over a 35-token claim: the predicate
+    covers blocks 0 and 1 only, so a failed partial tail block still leaves
+    32 >= 17 intact leading tokens and the claim materialized."""
+    rows = {r[0]: int(r[1]) for r in golden_lines("paper_event_paths.txt") if r[0].startswith("PRED")}
+    k, T = rows["PREDICATE2_TOKENS"], rows["PREDICATE2_CLAIM_TOKENS"]
+    tk = RNG.integers(0, 32000, size=T, dtype=np.uint32)
+    for lost, want_code in [(2, O.MATERIALIZED), (1, O.RESTORE_FAILED_FAIL_CLOSED),
+                            (0, O.RESTORE_FAILED_FAIL_CLOSED)]:
+        b = from_claims([(0x17, [40, 41, 42], tk)])
+        b.predicate_tokens = np.array([k], np.uint64)
+        op = fresh()
+        assert op.offload(b, d0) == O.OK
+        assert op.claim_predicate(0x17) == 2
+        op.restore(b, load_failed_blocks=[40 + lost])
+        out = op.check(b, d0)[0]
+        assert out["code"] == want_code and out["intact_blocks"] == lost
+        assert min(int(out["intact_blocks"]) * BS, T) >= k or want_code != O.MATERIALIZED
+
+
+def test_whole_claim_predicate_equals_no_predicate(pool):
+    """k >= the claim's token count, or no predicate array at all, both
+    cover the whole claim: outcomes and events are identical."""
+    w = replace(TINY, num_load_failed=2)
+    batch = make_batch(w)
+    faults = make_faults(w, batch)
+    T = np.diff(batch.token_offsets.astype(np.int64))
+    runs = []
+    for pred in (None, T.astype(np.uint64), (T + 1000).astype(np.uint64)):
+        batch.predicate_tokens = pred
+        _, out, ev, _, _ = oracle_lifecycle(w, batch, faults, pool)
+        runs.append((out, ev))
+        assert np.array_equal(out["intact_blocks"] <= out["num_blocks"], np.ones(len(out), bool))
+    for out, ev in runs[1:]:
+        assert np.array_equal(out, runs[0][0]) and np.array_equal(ev, runs[0][1])
 
 
 # --------------------------------------------------- tiny-pool brute force

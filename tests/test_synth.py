@@ -1,6 +1,8 @@
 """The seeded input generator: Philox known answers, content statistics and
 the structure of the generated claim batches."""
 
+from dataclasses import replace
+
 import numpy as np
 import pytest
 
@@ -92,3 +94,19 @@ def test_changed_blocks_cancels_repeated_flips():
     f = FaultSpec(np.array([3, 3, 5, 7, 7], np.uint32), np.array([10, 10, 1, 2, 3], np.uint64),
                   np.zeros(0, np.uint32))
     assert f.changed_blocks().tolist() == [5, 7]
+
+
+def test_predicates_cover_a_leading_prefix():
+    """With a predicate fraction, the selected claims get k in [1, T_c]
+    tokens and the rest exactly T_c; without one, no predicate array."""
+    assert make_batch(TINY).predicate_tokens is None
+    w = replace(TINY, num_claims=400, predicate_fraction=0.5)
+    b = make_batch(w)
+    T = np.diff(b.token_offsets.astype(np.int64))
+    k = b.predicate_tokens.astype(np.int64)
+    assert k.shape == T.shape and (k >= 1).all() and (k <= T).all()
+    assert 0.3 < np.mean(k < T) < 0.6
+    again = make_batch(w)
+    assert np.array_equal(again.predicate_tokens, b.predicate_tokens)
+    sub = b.subset([5, 2])
+    assert sub.predicate_tokens.tolist() == [b.predicate_tokens[5], b.predicate_tokens[2]]
