@@ -205,6 +205,16 @@ def main() -> int:
     t1 = time.perf_counter()
     stages = pool.timing()
     out, ev = pool.read()
+
+    # spread of single checks, in a separate pass after the timed region:
+    # hipEvents on the pool stream around each check
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    marks[0].record(stream)
+    for i in range(steps):
+        pool.check(db)
+        marks[i + 1].record(stream)
+    marks[-1].synchronize()
+    per_check = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(steps)])
     pool.close()
 
     ms_per_step = (t1 - t0) * 1e3 / steps
@@ -239,6 +249,7 @@ def main() -> int:
             "tokens": batch.num_tokens,
             "corrupted_blocks": int(faults.flip_blocks.size),
         },
+        "check_ms_p10_p50_p90": [round(float(np.percentile(per_check, q)), 4) for q in (10, 50, 90)],
         "claims_per_s": round(C / (ms_per_step * 1e-3), 1),
         "logical_GBps": round(present_refs * g.block_bytes / (ms_per_step * 1e-3) / 1e9, 2),
         "pct_hbm_peak": round(100 * (phys_bytes + meta_bytes) / (ms_per_step * 1e-3) / 1e9
