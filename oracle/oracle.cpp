@@ -38,6 +38,16 @@
  *      * token keys t_m = splitmix64(~S, m) | 1, the per-block token
  *        multilinear M_j = sum_m tok * t_m, and the chain
  *        h_{-1} = S, h_j = splitmix64(h_{j-1} xor M_j).
+ *  - Cache identity (section 5 cache_identity; Table 5 fixed cache identity
+ *    and joinable block hashes; section 7 reuse lookup E1 reporting a hit):
+ *    h_j names the token prefix held by a claim's j-th block.  Offload
+ *    registers (h_j -> physical block) for every offloaded claim; equal
+ *    registrations are stored once, and one identity registered to two
+ *    different blocks is duplicate ownership, which makes the identity
+ *    ambiguous.  A lookup reports the longest leading run of a request's
+ *    token blocks whose identities are registered and unambiguous.  The
+ *    check compares each h_j of the presented tokens with the one accepted
+ *    for that position.
  *
  * Parity pins (checked by the CPU tests): the published SplitMix64 outputs
  * for seed 0; D(0) = 0, D(e_i) = k_i, additivity, the exact single-bit-flip
@@ -155,6 +165,8 @@ enum {
   R_BEYOND_PREDICATE = 0x1000,
 };
 
+enum { LK_UNKNOWN = 0, LK_HIT = 1, LK_PARTIAL = 2, LK_MISS = 3 };
+
 enum { ORC_OK = 0, ORC_EINVAL = -1, ORC_EDUP = -5 };
 
 }  // namespace
@@ -176,6 +188,16 @@ typedef struct orc_outcome {
   uint64_t chain_hash_at_fail;
 } orc_outcome;
 
+typedef struct orc_lookup {
+  uint64_t request_id;
+  uint64_t hit_tokens;
+  uint64_t chain_hash_at_hit;
+  uint32_t status;
+  uint32_t hit_blocks;
+  uint32_t last_block;
+  uint32_t pad;
+} orc_lookup_result;
+
 typedef struct orc_event {
   uint64_t seq;
   uint64_t claim_id;
@@ -196,6 +218,14 @@ struct Claim {
   uint64_t n_tokens;
   uint64_t chain_hash;
   uint32_t pred_blocks; /* leading positions the predicate covers */
+  std::vector<uint64_t> identity; /* accepted h_j for j < min(blocks, token blocks) */
+};
+
+/* One registered cache identity: the physical block that holds it, and
+ * whether a second, different block was also registered for it. */
+struct Identity {
+  uint32_t block;
+  bool ambiguous;
 };
 
 struct Pool {
@@ -205,6 +235,7 @@ struct Pool {
   std::vector<uint64_t> d_off, d_res;
   std::vector<uint8_t> valid_off, load_failed;
   std::unordered_map<uint64_t, Claim> registry;
+  std::unordered_map<uint64_t, Identity> identities;
   std::vector<orc_event> log;
   uint64_t next_seq;
 };
@@ -351,7 +382,11 @@ int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
     cl.state = ST_ACCEPTED;
     cl.footprint.assign(fp, fp + n);
     cl.n_tokens = ntok;
-    cl.chain_hash = chain(tokens + tok_off[c], ntok, p->block_size, p->seed, nullptr);
+    std::vector<uint64_t> h;
+    cl.chain_hash = chain(tokens + tok_off[c], ntok, p->block_size, p->seed, &h);
+    /* the accepted identity of every position that has both a block and tokens */
+    uint64_t npos = n < h.size() ? n : h.size();
+    cl.identity.assign(h.begin(), h.begin() + npos);
     /* leading_prefix_at_least(k): the blocks holding the first k tokens;
      * no predicate array means the whole claim */
     cl.pred_blocks = n;
@@ -374,6 +409,20 @@ int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
     if (all_present && n == ceil_div(ntok, p->block_size)) {
       p->registry[ids[c]].state |= ST_OFFLOADED;
       append_event(p, ids[c], EV_OFFLOADED, kNone, kNone, n);
+      /* register h_j -> block for each position of the offloaded claim: an
+       * equal registration is stored once; a different block for the same
+       * identity is duplicate ownership */
+      for (uint32_t j = 0; j < n; ++j) {
+        auto it = p->identities.find(h[j]);
+        if (it == p->identities.end()) {
+          Identity idn;
+          idn.block = fp[j];
+          idn.ambiguous = false;
+          p->identities[h[j]] = idn;
+        } else if (it->second.block != fp[j]) {
+          it->second.ambiguous = true;
+        }
+      }
     }
   }
   return ORC_OK;
@@ -472,7 +521,26 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
           reasons |= R_NO_RESTORE;
           if (none_key < best) best = none_key;
         }
-        if (cl.n_tokens != ntok || cl.chain_hash != chain_hash) {
+        /* cache identity position by position: a token block whose chain
+         * hash differs from the accepted one, and the block where the token
+         * counts part; the whole-claim hash remains a claim-level check */
+        uint64_t npos = nt < cl.identity.size() ? nt : cl.identity.size();
+        for (uint64_t j = 0; j < npos; ++j) {
+          if (h[j] != cl.identity[j]) {
+            reasons |= R_TOKEN_MISMATCH;
+            uint64_t k = ((uint64_t)0 << 32) | j;
+            if (k < best) best = k;
+            if (j < intact) intact = (uint32_t)j;
+          }
+        }
+        if (cl.n_tokens != ntok) {
+          uint64_t q = (ntok < cl.n_tokens ? ntok : cl.n_tokens) / p->block_size;
+          reasons |= R_TOKEN_MISMATCH;
+          uint64_t k = ((uint64_t)0 << 32) | q;
+          if (k < best) best = k;
+          if (q < intact) intact = (uint32_t)q;
+        }
+        if (cl.chain_hash != chain_hash) {
           reasons |= R_TOKEN_MISMATCH;
           if (none_key < best) best = none_key;
         }
@@ -600,6 +668,77 @@ void orc_block_state(void* handle, uint64_t* d_off, uint64_t* d_res, uint8_t* va
  * not registered. */
 /* Predicate coverage (leading positions) recorded for a claim at
  * acceptance, or 0xFFFFFFFF if the id is not registered. */
+/* Lookup (the reuse lookup of section 7, E1, which reports how many of a
+ * request's tokens hit offloaded claim footprints).  For each request row,
+ * in order: the chain h_0 .. h_{nt-1} of its tokens; hit = the number of
+ * leading token blocks whose identity is registered and unambiguous.  The
+ * lookup stops at the first block that is not; if that block's identity is
+ * registered but ambiguous (duplicate ownership), the result is UNKNOWN
+ * rather than a shorter hit, as is a malformed row (reserved id, or token
+ * offsets that run backwards or past the array).  Otherwise HIT when every
+ * token block hit (and there is at least one), MISS when none did, PARTIAL
+ * in between.  hit_tokens = min(hit * bs, tokens); chain_hash_at_hit =
+ * h_{hit-1} (S when hit = 0); last_block = the block registered for
+ * h_{hit-1} (NONE when hit = 0).  Block rows are not read.  The registry
+ * and event log are not changed. */
+int orc_lookup(void* handle, uint32_t num_requests, uint64_t num_tokens, const uint64_t* ids,
+               const uint64_t* tok_off, const uint32_t* tokens, orc_lookup_result* out) {
+  Pool* p = static_cast<Pool*>(handle);
+  for (uint32_t c = 0; c < num_requests; ++c) {
+    orc_lookup_result r;
+    std::memset(&r, 0, sizeof(r));
+    r.request_id = ids[c];
+    r.last_block = kNone;
+    r.chain_hash_at_hit = p->seed;
+    bool bad = ids[c] == kReservedId || tok_off[c] > tok_off[c + 1] ||
+               tok_off[c + 1] > num_tokens;
+    if (bad) {
+      r.status = LK_UNKNOWN;
+      out[c] = r;
+      continue;
+    }
+    uint64_t ntok = tok_off[c + 1] - tok_off[c];
+    std::vector<uint64_t> h;
+    chain(tokens + tok_off[c], ntok, p->block_size, p->seed, &h);
+    uint64_t hit = 0;
+    bool ambiguous = false;
+    while (hit < h.size()) {
+      auto it = p->identities.find(h[hit]);
+      if (it == p->identities.end()) break;
+      if (it->second.ambiguous) {
+        ambiguous = true;
+        break;
+      }
+      ++hit;
+    }
+    r.hit_blocks = (uint32_t)hit;
+    r.hit_tokens = hit * p->block_size < ntok ? hit * p->block_size : ntok;
+    if (hit > 0) {
+      r.chain_hash_at_hit = h[hit - 1];
+      r.last_block = p->identities[h[hit - 1]].block;
+    }
+    if (ambiguous)
+      r.status = LK_UNKNOWN;
+    else if (hit == h.size() && hit > 0)
+      r.status = LK_HIT;
+    else if (hit == 0)
+      r.status = LK_MISS;
+    else
+      r.status = LK_PARTIAL;
+    out[c] = r;
+  }
+  return ORC_OK;
+}
+
+/* Registered identities, and how many of them are ambiguous. */
+void orc_identity_stats(void* handle, uint64_t* entries, uint64_t* ambiguous) {
+  Pool* p = static_cast<Pool*>(handle);
+  uint64_t a = 0;
+  for (const auto& kv : p->identities) a += kv.second.ambiguous ? 1 : 0;
+  *entries = p->identities.size();
+  *ambiguous = a;
+}
+
 uint32_t orc_claim_predicate(void* handle, uint64_t id) {
   Pool* p = static_cast<Pool*>(handle);
   auto it = p->registry.find(id);

@@ -50,7 +50,18 @@ EVENT_DTYPE = np.dtype(
         ("pad", "<u4"),
     ]
 )
-assert OUTCOME_DTYPE.itemsize == 64 and EVENT_DTYPE.itemsize == 40
+LOOKUP_DTYPE = np.dtype(
+    [
+        ("request_id", "<u8"),
+        ("hit_tokens", "<u8"),
+        ("chain_hash_at_hit", "<u8"),
+        ("status", "<u4"),
+        ("hit_blocks", "<u4"),
+        ("last_block", "<u4"),
+        ("pad", "<u4"),
+    ]
+)
+assert OUTCOME_DTYPE.itemsize == 64 and EVENT_DTYPE.itemsize == 40 and LOOKUP_DTYPE.itemsize == 40
 
 # vocabulary (the oracle's own copy)
 UNKNOWN, MATERIALIZED, RESTORE_FAILED_FAIL_CLOSED = 0, 1, 2
@@ -71,6 +82,7 @@ R_LOAD_FAILED = 0x400
 R_DIGEST_MISMATCH = 0x800
 R_BEYOND_PREDICATE = 0x1000
 OK, EINVAL, EDUP = 0, -1, -5
+LK_UNKNOWN, LK_HIT, LK_PARTIAL, LK_MISS = 0, 1, 2, 3
 
 
 def build(force: bool = True) -> str:
@@ -116,6 +128,8 @@ def lib() -> ctypes.CDLL:
             ("orc_block_state", [vp, vp, vp, vp, vp], None),
             ("orc_claim_state", [vp, u64], u32),
             ("orc_claim_predicate", [vp, u64], u32),
+            ("orc_lookup", [vp, u32, u64, vp, vp, vp, vp], ctypes.c_int),
+            ("orc_identity_stats", [vp, vp, vp], None),
         ]:
             f = getattr(L, name)
             f.argtypes = args
@@ -291,3 +305,20 @@ class OraclePool:
 
     def claim_predicate(self, claim_id: int) -> int:
         return lib().orc_claim_predicate(self._h, claim_id)
+
+    def lookup(self, batch) -> np.ndarray:
+        """Identity lookup of each row's tokens (block rows are not read)."""
+        ids = _arr(batch.claim_ids, np.uint64)
+        to = _arr(batch.token_offsets, np.uint64)
+        tk = _arr(batch.tokens, np.uint32)
+        out = np.zeros(ids.size, dtype=LOOKUP_DTYPE)
+        rc = lib().orc_lookup(self._h, ids.size, tk.size, _ptr(ids), _ptr(to), _ptr(tk), _ptr(out))
+        if rc != OK:
+            raise RuntimeError(f"orc_lookup failed: {rc}")
+        return out
+
+    def identity_stats(self) -> tuple[int, int]:
+        """(registered identities, ambiguous identities)."""
+        e, a = ctypes.c_uint64(), ctypes.c_uint64()
+        lib().orc_identity_stats(self._h, ctypes.byref(e), ctypes.byref(a))
+        return int(e.value), int(a.value)

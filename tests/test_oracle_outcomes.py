@@ -228,7 +228,8 @@ def test_cache_identity_mismatch_is_ambiguous(d0):
     tk2[20] += 1
     out = op.check(from_claims([(5, [1, 2, 3], tk2)]), d0)[0]
     assert out["code"] == O.UNKNOWN and out["reasons"] == O.R_TOKEN_MISMATCH
-    assert out["first_failing_block"] == NONE32
+    # the identity is compared block by block: token 20 lies in block 1
+    assert out["first_failing_block"] == 20 // BS and out["intact_blocks"] == 1
     out = op.check(from_claims([(5, [1, 9, 3], tk)]), d0)[0]
     assert out["code"] == O.UNKNOWN and out["first_failing_block"] == 1
     # block 9 differs from the accepted footprint and has no offload record
