@@ -208,6 +208,22 @@ typedef struct claim_event {
   uint32_t reserved;
 } claim_event;
 
+/* Result of a reuse lookup for one request row (40 bytes). */
+#define CLAIM_LOOKUP_UNKNOWN 0 /* malformed row, or the lookup reached an ambiguous identity */
+#define CLAIM_LOOKUP_HIT 1     /* every token block of the request hit */
+#define CLAIM_LOOKUP_PARTIAL 2 /* a leading run of token blocks hit, not all */
+#define CLAIM_LOOKUP_MISS 3    /* no token block hit (or the request has no tokens) */
+
+typedef struct claim_lookup_result {
+  uint64_t request_id;        /* claim_ids[c] of the request row */
+  uint64_t hit_tokens;        /* min(hit_blocks * block_size, request tokens) */
+  uint64_t chain_hash_at_hit; /* h_{hit_blocks-1}; the pool seed S when hit_blocks = 0 */
+  uint32_t status;            /* CLAIM_LOOKUP_* */
+  uint32_t hit_blocks;        /* leading token blocks whose identity is registered and unambiguous */
+  uint32_t last_block;        /* physical block registered for h_{hit_blocks-1}; CLAIM_NONE if none */
+  uint32_t reserved;
+} claim_lookup_result;
+
 /* Stage times of the claim_check calls queued since the last
  * claim_timing_read, measured with hipEvents on the pool's stream.  With
  * CLAIM_POOL_TIMING only digest_ms is filled (two events per check around
@@ -228,8 +244,10 @@ typedef struct claim_timing {
  * accepted-claim state; Table 5: fixed cache identity = seed + geometry).
  * Allocates the pool's device state: offload and restored digests, offload
  * records, reported-failure flags, the claim registry (ids, state, token
- * count, chain hash, footprint), the event log and scratch.  Returns
- * EINVAL for a bad description, ENOMEM / EHIP on allocation failure. */
+ * count, chain hash, footprint, per-position accepted identities), the
+ * cache-identity table (16 bytes per entry, next_pow2(2 * max_footprint)
+ * entries), the event log and scratch.  Returns EINVAL for a bad
+ * description, ENOMEM / EHIP on allocation failure. */
 int claim_pool_create(const claim_pool_desc* desc, claim_pool** out);
 
 /* Wait for the pool's stream, then free everything the pool owns (not the
@@ -244,7 +262,14 @@ int claim_pool_destroy(claim_pool* pool);
  * ACCEPTED); every in-range block it references gets an offload digest and
  * its reported-failure flag is cleared; a claim whose footprint is
  * non-empty, fully present and equal in length to ceil(tokens/block_size)
- * becomes OFFLOADED (event OFFLOADED).  With staging != NULL the canonical
+ * becomes OFFLOADED (event OFFLOADED).  Each claim's accepted identity
+ * h_j (its chain hash after token block j) is kept for every position with
+ * both a block and tokens.  For every OFFLOADED claim, (h_j -> block j) is
+ * registered in the cache-identity table (section 5 cache identity; Table 5
+ * joinable block hashes): a registration equal to an existing one is stored
+ * once; the same identity registered to a different block is duplicate
+ * ownership and makes the identity ambiguous (Table 2).  Entries are never
+ * removed.  With staging != NULL the canonical
  * bytes of every such block are also written to staging (device memory or
  * host memory from hipHostMalloc, 16-byte aligned, else EINVAL), one block
  * after another in ascending block-id order; staging_bytes must cover them
@@ -267,14 +292,42 @@ int claim_restore(claim_pool* pool, const claim_batch* batch, const void* stagin
 
 /* Check (section 7 path A step 5, path B steps 5-7, path C): digest every
  * in-range, offloaded block the well-formed claims reference, compare with
- * the offload digest, chain each claim's tokens and decide its outcome: the
- * smallest key (class << 32 | position) over the claim's problems wins,
+ * the offload digest, chain each claim's tokens and decide its outcome.
+ * The cache identity is compared position by position: a token block whose
+ * h_j differs from the accepted one, or the block where the token counts
+ * part (min(tokens, accepted tokens) / block_size), is an ambiguity at that
+ * position (CLAIM_R_TOKEN_MISMATCH); a different whole-claim chain hash is
+ * also a claim-level ambiguity.  The smallest key (class << 32 | position)
+ * over the claim's problems wins,
  * class 0 = ambiguity -> UNKNOWN, class 1 = load failure or digest mismatch
  * -> RESTORE_FAILED_FAIL_CLOSED, none -> MATERIALIZED.  Appends, in batch
  * order, RESTORED, or RESTORATION_FAILED then ACTIVE_REQUEST_REFUSED (the
  * claim is its own blocking id), or OUTCOME_UNKNOWN.  The registry is not
  * changed.  ENOSPC if the event log could overflow. */
 int claim_check(claim_pool* pool, const claim_batch* batch);
+
+/* Reuse lookup (section 7 paths A and B, order 3: the lookup reports how
+ * many of the request's tokens hit the offloaded claim footprint, hit=448
+ * in the running example).  For each request row c of the batch (its id,
+ * token_offsets and tokens; block rows are not read and may be NULL): the
+ * chain h_0 .. h_{nt-1} of its tokens, and hit_blocks = the number of
+ * leading token blocks whose identity is registered and unambiguous.  The
+ * lookup stops at the first block that is not; if that identity is
+ * registered but ambiguous (duplicate ownership), the status is
+ * CLAIM_LOOKUP_UNKNOWN rather than a shorter hit (Table 2: duplicate owners
+ * fail closed), as it is for a malformed row (reserved id, token offsets
+ * that run backwards or past num_tokens).  The registry and event log are
+ * not changed.  out is device memory with room for out_cap records; it is
+ * written in stream order on the pool's stream and is complete once the
+ * stream reaches this call (the call does not wait).  ENOSPC if out_cap <
+ * num_claims; EINVAL for a NULL out with requests, or a bad batch. */
+int claim_lookup(claim_pool* pool, const claim_batch* requests, claim_lookup_result* out,
+                 uint32_t out_cap);
+
+/* Wait for the pool's stream and return the number of registered
+ * identities and how many of them are ambiguous (registered to two or more
+ * different blocks).  Either pointer may be NULL. */
+int claim_identity_stats(claim_pool* pool, uint64_t* entries, uint64_t* ambiguous);
 
 /* Wait for the pool's stream and copy to the host the outcomes of the last
  * claim_check (into out, capacity out_cap; *num_out = their count) and the

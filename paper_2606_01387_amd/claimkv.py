@@ -27,7 +27,9 @@ OK, EINVAL, ENOMEM, EHIP, ENOSPC, EDUP = 0, -1, -2, -3, -4, -5
 UNKNOWN, MATERIALIZED, RESTORE_FAILED_FAIL_CLOSED = 0, 1, 2
 EV_ACCEPTED, EV_OFFLOADED, EV_RESTORE_REQUIRED, EV_RESTORED = 1, 2, 3, 4
 EV_RESTORATION_FAILED, EV_ACTIVE_REQUEST_REFUSED, EV_OUTCOME_UNKNOWN = 5, 6, 7
+R_TOKEN_MISMATCH = 0x008
 R_BEYOND_PREDICATE = 0x1000
+LOOKUP_UNKNOWN, LOOKUP_HIT, LOOKUP_PARTIAL, LOOKUP_MISS = 0, 1, 2, 3
 NONE = 0xFFFFFFFF
 RESERVED_ID = 0xFFFFFFFFFFFFFFFF
 POOL_TIMING = 0x1
@@ -41,9 +43,13 @@ EVENT_DTYPE = np.dtype(
     [("seq", "<u8"), ("claim_id", "<u8"), ("aux", "<u8"), ("kind", "<u4"), ("block_index", "<u4"),
      ("phys_block", "<u4"), ("reserved", "<u4")])
 
+LOOKUP_DTYPE = np.dtype(
+    [("request_id", "<u8"), ("hit_tokens", "<u8"), ("chain_hash_at_hit", "<u8"), ("status", "<u4"),
+     ("hit_blocks", "<u4"), ("last_block", "<u4"), ("reserved", "<u4")])
+
 EXPORTS = ("claim_pool_create", "claim_pool_destroy", "claim_offload", "claim_restore",
-           "claim_check", "outcomes_read", "claim_timing_read", "claim_block_state_read",
-           "claim_strerror")
+           "claim_check", "claim_lookup", "claim_identity_stats", "outcomes_read",
+           "claim_timing_read", "claim_block_state_read", "claim_strerror")
 
 
 class PoolDesc(ctypes.Structure):
@@ -79,7 +85,7 @@ class CTiming(ctypes.Structure):
 
 
 assert ctypes.sizeof(PoolDesc) == 88 and ctypes.sizeof(CBatch) == 72
-assert OUTCOME_DTYPE.itemsize == 64 and EVENT_DTYPE.itemsize == 40
+assert OUTCOME_DTYPE.itemsize == 64 and EVENT_DTYPE.itemsize == 40 and LOOKUP_DTYPE.itemsize == 40
 
 
 class ClaimError(RuntimeError):
@@ -114,6 +120,8 @@ def lib() -> ctypes.CDLL:
             "claim_offload": ([vp, ctypes.POINTER(CBatch), vp, u64], i32),
             "claim_restore": ([vp, ctypes.POINTER(CBatch), vp, u64, ctypes.POINTER(CFaults)], i32),
             "claim_check": ([vp, ctypes.POINTER(CBatch)], i32),
+            "claim_lookup": ([vp, ctypes.POINTER(CBatch), vp, u32], i32),
+            "claim_identity_stats": ([vp, ctypes.POINTER(u64), ctypes.POINTER(u64)], i32),
             "outcomes_read": ([vp, vp, u32, ctypes.POINTER(u32), vp, u64, ctypes.POINTER(u64)], i32),
             "claim_timing_read": ([vp, ctypes.POINTER(CTiming)], i32),
             "claim_block_state_read": ([vp, u32, u32, vp, vp, vp, vp], i32),
@@ -263,6 +271,32 @@ class Pool:
 
     def check(self, batch: DeviceBatch) -> None:
         _check(lib().claim_check(self._h, ctypes.byref(batch.struct)), "claim_check")
+
+    def lookup_async(self, batch: DeviceBatch, out=None):
+        """Queue a reuse lookup of the batch's token rows on the pool stream;
+        returns the device tensor (uint8, 40 bytes per row) it fills."""
+        torch = _torch()
+        n = batch.num_claims
+        if out is None:
+            out = torch.empty(max(1, n) * LOOKUP_DTYPE.itemsize, dtype=torch.uint8,
+                              device=self.kv.device)
+        cap = out.numel() // LOOKUP_DTYPE.itemsize
+        _check(lib().claim_lookup(self._h, ctypes.byref(batch.struct), out.data_ptr(), cap),
+               "claim_lookup")
+        return out
+
+    def lookup(self, batch: DeviceBatch) -> np.ndarray:
+        """Reuse lookup of the batch's token rows, read back to the host."""
+        out = self.lookup_async(batch)
+        self.stream.synchronize()
+        return out.cpu().numpy().view(LOOKUP_DTYPE)[: batch.num_claims].copy()
+
+    def identity_stats(self) -> tuple[int, int]:
+        """(registered identities, ambiguous identities)."""
+        e, a = ctypes.c_uint64(), ctypes.c_uint64()
+        _check(lib().claim_identity_stats(self._h, ctypes.byref(e), ctypes.byref(a)),
+               "claim_identity_stats")
+        return int(e.value), int(a.value)
 
     def read(self, max_outcomes: int = 1 << 22, max_events: int | None = None):
         """(outcomes of the last check, events since the last read)."""

@@ -168,6 +168,24 @@ struct RegDev {
   uint64_t mask;
   RegEntry* e;
   const uint32_t* fp;
+  uint64_t* idn;  // accepted identities h_j, at the footprint's offsets
+};
+
+// Cache-identity table: open addressing on the identity h_j, linear
+// probing, key 0 marks an empty slot (the identity 0 itself lives in the
+// extra entry e[mask + 1]).  block is the first block registered for the
+// identity; kIdAmbiguous is set once a different block is registered too.
+constexpr uint32_t kIdUsed = 1u, kIdAmbiguous = 2u;
+
+struct IdEntry {
+  uint64_t key;
+  uint32_t block;  // kNone until the first registration
+  uint32_t flags;  // kIdUsed | kIdAmbiguous
+};
+
+struct IdDev {
+  uint64_t mask;
+  IdEntry* e;  // mask + 2 entries
 };
 
 struct Pend {  // events a claim will append (0..2), written before the scan
@@ -178,17 +196,21 @@ struct Pend {  // events a claim will append (0..2), written before the scan
   uint32_t pad;
 };
 
-struct Counters {  // device-resident counters of one pool (48 bytes)
+struct Counters {  // device-resident counters of one pool (64 bytes)
   uint32_t uniq_count;
   uint32_t dup_flag;
-  uint64_t log_count;  // events held in the log
-  uint64_t seq_next;   // next global sequence number
-  uint64_t call_pos;   // log position of the current call's first event
-  uint64_t call_seq;   // its sequence number
-  uint64_t reg_count;  // claims registered
+  uint64_t log_count;     // events held in the log
+  uint64_t seq_next;      // next global sequence number
+  uint64_t call_pos;      // log position of the current call's first event
+  uint64_t call_seq;      // its sequence number
+  uint64_t reg_count;     // claims registered
+  uint64_t id_entries;    // identities registered
+  uint64_t id_ambiguous;  // identities registered to two or more blocks
 };
 
-static_assert(sizeof(Counters) == 48, "Counters layout");
+static_assert(sizeof(Counters) == 64, "Counters layout");
+static_assert(sizeof(IdEntry) == 16, "IdEntry layout");
+static_assert(sizeof(claim_lookup_result) == 40, "claim_lookup_result layout");
 static_assert(sizeof(claim_outcome) == 64, "claim_outcome layout");
 static_assert(sizeof(claim_event) == 40, "claim_event layout");
 static_assert(sizeof(Pend) == 32, "Pend layout");
@@ -224,6 +246,47 @@ __device__ __forceinline__ int64_t reg_find(const RegDev& r, uint64_t id) {
     s = (s + 1) & r.mask;
   }
   return -1;
+}
+
+// Slot of identity `key`, inserting the key if it is absent.
+__device__ IdEntry* id_claim_slot(const IdDev& t, uint64_t key) {
+  if (key == 0) return t.e + t.mask + 1;
+  uint64_t s = slot_of_id(key, t.mask);
+  for (uint64_t probe = 0; probe <= t.mask; ++probe) {
+    const unsigned long long old =
+        atomicCAS((unsigned long long*)&t.e[s].key, 0ull, (unsigned long long)key);
+    if (old == 0ull || old == key) return t.e + s;
+    s = (s + 1) & t.mask;
+  }
+  return nullptr;  // unreachable: the table is at most half full
+}
+
+// Register (key -> block).  Order-independent: the first registration sets
+// the block, any later one with another block marks the identity ambiguous.
+__device__ void id_register(const IdDev& t, uint64_t key, uint32_t block,
+                            Counters* __restrict__ ctr) {
+  IdEntry* e = id_claim_slot(t, key);
+  if (!e) return;
+  if (!(atomicOr(&e->flags, kIdUsed) & kIdUsed))
+    atomicAdd((unsigned long long*)&ctr->id_entries, 1ull);
+  const uint32_t prev = atomicCAS(&e->block, kNone, block);
+  if (prev != kNone && prev != block && !(atomicOr(&e->flags, kIdAmbiguous) & kIdAmbiguous))
+    atomicAdd((unsigned long long*)&ctr->id_ambiguous, 1ull);
+}
+
+__device__ __forceinline__ const IdEntry* id_find(const IdDev& t, uint64_t key) {
+  if (key == 0) {
+    const IdEntry* e = t.e + t.mask + 1;
+    return (e->flags & kIdUsed) ? e : nullptr;
+  }
+  uint64_t s = slot_of_id(key, t.mask);
+  for (uint64_t probe = 0; probe <= t.mask; ++probe) {
+    const uint64_t k = t.e[s].key;
+    if (k == key) return t.e + s;
+    if (k == 0) return nullptr;
+    s = (s + 1) & t.mask;
+  }
+  return nullptr;
 }
 
 __device__ __forceinline__ uint64_t token_multilinear(const uint32_t* __restrict__ tok,
@@ -552,9 +615,9 @@ __global__ void __launch_bounds__(kThreads) k_dupcheck(BatchDev b, RegDev reg,
 // Acceptance: chain hash of the claim's tokens, presence of its footprint,
 // registration, and the ACCEPTED (+ OFFLOADED) events.
 template <int W>
-__global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, uint32_t nb,
-                                                     uint32_t bs, uint64_t seed, uint64_t fp_base,
-                                                     Counters* __restrict__ ctr,
+__global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdDev ids,
+                                                     uint32_t nb, uint32_t bs, uint64_t seed,
+                                                     uint64_t fp_base, Counters* __restrict__ ctr,
                                                      uint32_t* __restrict__ cnt,
                                                      Pend* __restrict__ pend) {
   __shared__ uint64_t tkey[kMaxBlockSize];
@@ -565,33 +628,47 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, uin
   const uint32_t gl = lane & (W - 1), gbase = lane & ~(uint32_t)(W - 1);
   const Row r = read_row(b, c);
   const uint64_t nt = (r.ntok + bs - 1) / bs;
-  const uint64_t L = (uint64_t)r.n > nt ? (uint64_t)r.n : nt;
+
+  // presence first: only an offloaded claim registers its identities
+  uint32_t missing = 0;
+  for (uint64_t j = gl; j < r.n; j += W)
+    if (b.bi[(uint64_t)r.bo0 + j] >= nb) missing = 1;
+  missing = group_or<W>(missing);
+  const bool offloaded = !r.malformed && r.n > 0 && !missing && (uint64_t)r.n == nt;
+  const uint64_t npos = (uint64_t)r.n < nt ? (uint64_t)r.n : nt;  // positions with block and tokens
 
   uint64_t h = seed;
-  uint32_t missing = 0;
-  for (uint64_t j0 = 0; j0 < L; j0 += W) {
+  for (uint64_t j0 = 0; j0 < nt; j0 += W) {
     const uint64_t j = j0 + gl;
-    if (j < r.n && b.bi[(uint64_t)r.bo0 + j] >= nb) missing = 1;
     uint64_t m_sum = 0;
     if (j < nt) {
       const uint64_t first = j * bs;
       const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
       m_sum = token_multilinear(b.tok, r.to0 + first, count, tkey);
     }
-    const uint64_t steps = j0 < nt ? (nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W) : 0;
+    const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
+    uint64_t my_h = 0;
     if constexpr (W == 64) {  // one claim per wave: the chain runs on the scalar ALU
-      for (uint32_t t = 0; t < steps; ++t) h = splitmix_step(h ^ uniform_read64(m_sum, t));
+      for (uint32_t t = 0; t < steps; ++t) {
+        h = splitmix_step(h ^ uniform_read64(m_sum, t));
+        if (gl == t) my_h = h;
+      }
     } else {
-      for (uint32_t t = 0; t < steps; ++t) h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
+      for (uint32_t t = 0; t < steps; ++t) {
+        h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
+        if (gl == t) my_h = h;
+      }
+    }
+    if (j < npos) {
+      reg.idn[fp_base + r.bo0 + j] = my_h;
+      if (offloaded) id_register(ids, my_h, b.bi[(uint64_t)r.bo0 + j], ctr);
     }
   }
-  missing = group_or<W>(missing);
   if (gl != 0) return;
   if (r.malformed) {
     cnt[c] = 0;
     return;
   }
-  const bool offloaded = r.n > 0 && !missing && (uint64_t)r.n == nt;
   uint64_t s = slot_of_id(r.id, reg.mask);
   bool inserted = false;
   for (uint64_t probe = 0; probe <= reg.mask && !inserted; ++probe) {
@@ -723,7 +800,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   uint64_t special = kNoKey;  // claim-level and length keys
   int64_t slot = -1;
   uint32_t na = 0, state = 0, pred = r.n;
-  uint64_t acc_ntok = 0, acc_chain = 0, fpo = 0;
+  uint64_t acc_ntok = 0, acc_chain = 0, fpo = 0, q3 = kNoKey;
   if (r.malformed) {
     reasons |= CLAIM_R_MALFORMED;
     special = kClaimLevelKey;
@@ -753,6 +830,11 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
         const uint64_t k = n < na ? n : na;
         special = k < special ? k : special;
       }
+      if (acc_ntok != r.ntok) {  // the token counts part in this block
+        reasons |= CLAIM_R_TOKEN_MISMATCH;
+        q3 = (acc_ntok < r.ntok ? acc_ntok : r.ntok) / bs;
+        special = q3 < special ? q3 : special;
+      }
     }
     if (n == 0) {
       reasons |= CLAIM_R_EMPTY;
@@ -766,13 +848,22 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   }
   const bool found = slot >= 0;
   const uint64_t common = n < na ? n : na;
-  const uint64_t q1 = (found && n != na) ? common : kNoKey;  // positions whose
-  const uint64_t q2 = (n != nt) ? (n < nt ? n : nt) : kNoKey;  // h may be needed
+  // the smallest length key (footprint length, block rows vs token blocks,
+  // token counts): the only one of them that can decide, and whose h_j the
+  // outcome may need
+  uint64_t qmin = (found && n != na) ? common : kNoKey;
+  if (!r.malformed && n != nt) qmin = (n < nt ? n : nt) < qmin ? (n < nt ? n : nt) : qmin;
+  qmin = q3 < qmin ? q3 : qmin;
+  // positions whose accepted identity is compared with the presented one
+  uint64_t id_pos = 0;
+  if (found) {
+    const uint64_t acc_nt = (acc_ntok + bs - 1) / bs;
+    id_pos = na < acc_nt ? na : acc_nt;
+    id_pos = nt < id_pos ? nt : id_pos;
+  }
 
-  uint64_t h = seed, best_pos = kNoKey, h_best = 0, h_q1 = 0, h_q2 = 0;
-  uint64_t intact = n;  // first position with any problem (lane-local, then group min)
-  if (q1 < intact) intact = q1;
-  if (q2 < intact) intact = q2;
+  uint64_t h = seed, best_pos = kNoKey, h_best = 0, h_q = 0;
+  uint64_t intact = n < qmin ? n : qmin;  // first position with any problem (lane-local, then group min)
   const uint64_t L = n > nt ? n : nt;
   for (uint64_t j0 = 0; j0 < L; j0 += W) {
     const uint64_t j = j0 + gl;
@@ -824,15 +915,19 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
         if (gl == t) my_h = h;
       }
     }
+    if (j < id_pos && my_h != reg.idn[fpo + j]) {  // cache identity of block j
+      reasons |= CLAIM_R_TOKEN_MISMATCH;
+      my_key = j < my_key ? j : my_key;
+      if (j < intact) intact = j;
+    }
     const uint64_t rk = group_min64<W>(my_key);
     if (rk < best_pos) {
       best_pos = rk;
       h_best = lane_read64(my_h, gbase + (uint32_t)((rk & 0xFFFFFFFFull) - j0));
     }
-    if (q1 >= j0 && q1 < j0 + W) h_q1 = lane_read64(my_h, gbase + (uint32_t)(q1 - j0));
-    if (q2 >= j0 && q2 < j0 + W) h_q2 = lane_read64(my_h, gbase + (uint32_t)(q2 - j0));
+    if (qmin >= j0 && qmin < j0 + W) h_q = lane_read64(my_h, gbase + (uint32_t)(qmin - j0));
   }
-  if (found && (acc_ntok != r.ntok || acc_chain != h)) {
+  if (found && acc_chain != h) {  // whole-claim identity
     reasons |= CLAIM_R_TOKEN_MISMATCH;
     special = kClaimLevelKey < special ? kClaimLevelKey : special;
   }
@@ -871,7 +966,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       o.observed_digest = st.d_res[o.phys_block];
     }
     if (js != kNone && (uint64_t)js < nt)
-      o.chain_hash_at_fail = best == best_pos ? h_best : (js == q1 ? h_q1 : h_q2);
+      o.chain_hash_at_fail = best == best_pos ? h_best : h_q;
     if (cls == 1) {
       pe.kinds = CLAIM_EV_RESTORATION_FAILED | (CLAIM_EV_ACTIVE_REQUEST_REFUSED << 8);
       pe.aux0 = o.observed_digest;
@@ -887,6 +982,98 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   pe.phys = o.phys_block;
   out[c] = o;
   pend[c] = pe;
+}
+
+// ------------------------------------------------------------------ lookup
+
+// Reuse lookup: one group of W lanes per request.  Lanes hash one token
+// block each, the chain runs through the group, then every lane probes the
+// identity table for its h_j; the group stops at the first block that is
+// not a plain hit (absent, or registered but ambiguous).
+template <int W>
+__global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids, uint32_t bs,
+                                                     uint64_t seed,
+                                                     claim_lookup_result* __restrict__ out) {
+  __shared__ uint64_t tkey[kMaxBlockSize];
+  load_token_keys(tkey, bs, seed);
+  const uint64_t c = group_claim<W>();
+  if (c >= b.C) return;
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t gl = lane & (W - 1), gbase = lane & ~(uint32_t)(W - 1);
+  const uint64_t id = b.ids[c];
+  const uint64_t to0 = b.to[c], to1 = b.to[c + 1];
+  const bool bad = id == kEmptyId || to0 > to1 || to1 > b.T;
+  const uint64_t ntok = bad ? 0 : to1 - to0;
+  const uint64_t nt = (ntok + bs - 1) / bs;
+
+  uint64_t h = seed;
+  uint64_t stop = kNoKey;  // (j << 1) | plain_miss of the first block that did not hit
+  uint64_t h_at = seed;    // h_{hit - 1}
+  for (uint64_t j0 = 0; j0 < nt && stop == kNoKey; j0 += W) {
+    const uint64_t j = j0 + gl;
+    uint64_t m_sum = 0;
+    if (j < nt) {
+      const uint64_t first = j * bs;
+      const uint64_t count = ntok - first < bs ? ntok - first : bs;
+      m_sum = token_multilinear(b.tok, to0 + first, count, tkey);
+    }
+    const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
+    const uint64_t h_before = h;
+    uint64_t my_h = 0;
+    if constexpr (W == 64) {
+      for (uint32_t t = 0; t < steps; ++t) {
+        h = splitmix_step(h ^ uniform_read64(m_sum, t));
+        if (gl == t) my_h = h;
+      }
+    } else {
+      for (uint32_t t = 0; t < steps; ++t) {
+        h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
+        if (gl == t) my_h = h;
+      }
+    }
+    uint64_t my_stop = kNoKey;
+    if (j < nt) {
+      const IdEntry* e = id_find(ids, my_h);
+      if (!e)
+        my_stop = (j << 1) | 1u;
+      else if (e->flags & kIdAmbiguous)
+        my_stop = j << 1;
+    }
+    stop = group_min64<W>(my_stop);
+    if (stop == kNoKey) {
+      h_at = h;  // the whole window hit
+    } else {
+      const uint64_t js = stop >> 1;
+      h_at = js > j0 ? lane_read64(my_h, gbase + (uint32_t)(js - 1 - j0)) : h_before;
+    }
+  }
+  if (gl != 0) return;
+
+  claim_lookup_result o;
+  o.request_id = id;
+  o.reserved = 0;
+  o.last_block = kNone;
+  if (bad) {
+    o.status = CLAIM_LOOKUP_UNKNOWN;
+    o.hit_blocks = 0;
+    o.hit_tokens = 0;
+    o.chain_hash_at_hit = seed;
+  } else {
+    const uint64_t hit = stop == kNoKey ? nt : stop >> 1;
+    const bool ambiguous = stop != kNoKey && !(stop & 1u);
+    o.hit_blocks = (uint32_t)hit;
+    o.hit_tokens = hit * bs < ntok ? hit * bs : ntok;
+    o.chain_hash_at_hit = hit ? h_at : seed;
+    if (hit) {
+      const IdEntry* e = id_find(ids, h_at);
+      o.last_block = e ? e->block : kNone;
+    }
+    o.status = ambiguous                ? CLAIM_LOOKUP_UNKNOWN
+               : (hit == nt && hit > 0) ? CLAIM_LOOKUP_HIT
+               : hit == 0               ? CLAIM_LOOKUP_MISS
+                                        : CLAIM_LOOKUP_PARTIAL;
+  }
+  out[c] = o;
 }
 
 // ------------------------------------------------------------ event append
@@ -1057,7 +1244,10 @@ struct claim_pool {
   uint64_t reg_mask = 0, max_claims = 0;
   RegEntry* reg = nullptr;
   uint32_t* fp_store = nullptr;
+  uint64_t* idn_store = nullptr;  // accepted identities, parallel to fp_store
   uint64_t max_fp = 0, fp_used = 0;
+  IdEntry* id_table = nullptr;
+  uint64_t id_mask = 0;
   uint64_t staged_blocks = 0;  // blocks written by the last staged offload
   uint64_t reg_used_ub = 0;  // upper bound on registered claims
 
@@ -1174,7 +1364,24 @@ RegDev reg_dev(claim_pool* P) {
   r.mask = P->reg_mask;
   r.e = P->reg;
   r.fp = P->fp_store;
+  r.idn = P->idn_store;
   return r;
+}
+
+IdDev id_dev(claim_pool* P) {
+  IdDev t;
+  t.mask = P->id_mask;
+  t.e = P->id_table;
+  return t;
+}
+
+// Group width for a lookup batch: from the mean number of token blocks.
+int lookup_group_width(const claim_batch* b, uint32_t bs) {
+  const uint64_t per = b->num_claims ? (b->num_tokens + b->num_claims - 1) / b->num_claims : 1;
+  const uint64_t mean = (per + bs - 1) / bs;
+  int w = 2;
+  while (w < 64 && (uint64_t)w < mean) w <<= 1;
+  return w;
 }
 
 int check_batch(const claim_pool* P, const claim_batch* b) {
@@ -1318,9 +1525,11 @@ int append_events(claim_pool* P, const claim_batch* b) {
 }
 
 // Launch a claim-group kernel for the batch's group width.
-#define LAUNCH_GROUPED(KERNEL, P, b, ...)                                                       \
+#define LAUNCH_GROUPED(KERNEL, P, b, ...) LAUNCH_GROUPED_W(KERNEL, P, b, group_width(b), __VA_ARGS__)
+
+#define LAUNCH_GROUPED_W(KERNEL, P, b, WIDTH, ...)                                              \
   do {                                                                                          \
-    const int W_ = group_width(b);                                                              \
+    const int W_ = (WIDTH);                                                                     \
     const uint32_t grid_ = grid_for((uint64_t)(b)->num_claims * W_, 0x7FFFFFFFu);               \
     switch (W_) {                                                                               \
       case 2:                                                                                   \
@@ -1384,7 +1593,8 @@ void free_pool(claim_pool* P) {
   void* ptrs[] = {P->d_off,    P->d_res,    P->partial, P->valid_off, P->load_failed,
                   P->mark,     P->uniq,     P->slot_of, P->reg,       P->fp_store,
                   P->log,      P->ctr,      P->outcomes, P->cnt,      P->pend,
-                  P->tsum,     P->dup_table, P->f_blocks, P->f_bits};
+                  P->tsum,     P->dup_table, P->f_blocks, P->f_bits,   P->idn_store,
+                  P->id_table};
   for (void* p : ptrs)
     if (p) dfree(p);
   if (P->host_ctr) (void)hipHostFree(P->host_ctr);
@@ -1497,6 +1707,11 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     if ((rc = dalloc(&P->reg, cap))) break;
     P->max_fp = d->max_footprint;
     if ((rc = dalloc(&P->fp_store, d->max_footprint))) break;
+    if ((rc = dalloc(&P->idn_store, d->max_footprint))) break;
+    // every registered identity is a footprint position: at most half full
+    const uint64_t id_cap = next_pow2(2 * d->max_footprint < 64 ? 64 : 2 * d->max_footprint);
+    P->id_mask = id_cap - 1;
+    if ((rc = dalloc(&P->id_table, id_cap + 1))) break;
     P->ev_cap = d->event_capacity;
     if ((rc = dalloc(&P->log, d->event_capacity))) break;
     if ((rc = dalloc(&P->ctr, 1))) break;
@@ -1517,6 +1732,10 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
         (rc = fill<uint8_t>(P, P->mark, (nb + 15) / 16 * 16, 0)) || (rc = fill<uint32_t>(P, P->slot_of, nb, kNone)) ||
         (rc = fill<uint64_t>(P, (uint64_t*)P->reg, cap * (sizeof(RegEntry) / 8), 0)) ||
         (rc = fill_strided_u64(P, (uint64_t*)P->reg, cap, sizeof(RegEntry) / 8, kEmptyId)))
+      break;
+    // identity table: key 0 (empty), block kNone, flags 0
+    if ((rc = fill<uint64_t>(P, (uint64_t*)P->id_table, 2 * (P->id_mask + 2), 0)) ||
+        (rc = fill_strided_u64(P, (uint64_t*)P->id_table + 1, P->id_mask + 2, 2, (uint64_t)kNone)))
       break;
     if ((rc = fill<uint64_t>(P, (uint64_t*)P->ctr, sizeof(Counters) / 8, 0))) break;
     if (hipStreamSynchronize(P->stream) != hipSuccess) { rc = CLAIM_EHIP; break; }
@@ -1568,7 +1787,8 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
     hipLaunchKernelGGL(k_copy_u32, dim3(grid_for(b->num_refs, 4096)), dim3(kThreads), 0, P->stream,
                        P->fp_store + P->fp_used, b->block_ids, b->num_refs);
     HIP_TRY(hipGetLastError());
-    LAUNCH_GROUPED(k_accept, P, b, bd, rd, P->nb, P->bs, P->seed, P->fp_used, P->ctr, P->cnt, P->pend);
+    LAUNCH_GROUPED(k_accept, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->seed, P->fp_used, P->ctr,
+                   P->cnt, P->pend);
     TRY(append_events(P, b));
   }
   // offload record; a staged offload replaces every earlier staging slot
@@ -1696,6 +1916,29 @@ int claim_check(claim_pool* P, const claim_batch* b) {
   P->last_check_claims = C;
   P->have_outcomes = true;
   P->log_ub += 2 * C;
+  return CLAIM_OK;
+}
+
+int claim_lookup(claim_pool* P, const claim_batch* b, claim_lookup_result* out,
+                 uint32_t out_cap) {
+  if (!P || !b || b->reserved != 0) return CLAIM_EINVAL;
+  if (b->num_claims > 0x7FFFFFFFu) return CLAIM_EINVAL;
+  if (b->num_claims > 0 && (!b->claim_ids || !b->token_offsets || !out)) return CLAIM_EINVAL;
+  if (b->num_tokens > 0 && !b->tokens) return CLAIM_EINVAL;
+  if (out_cap < b->num_claims) return CLAIM_ENOSPC;
+  if (b->num_claims == 0) return CLAIM_OK;
+  HIP_TRY(hipSetDevice(P->device));
+  LAUNCH_GROUPED_W(k_lookup, P, b, lookup_group_width(b, P->bs), batch_dev(b), id_dev(P), P->bs,
+                   P->seed, out);
+  return CLAIM_OK;
+}
+
+int claim_identity_stats(claim_pool* P, uint64_t* entries, uint64_t* ambiguous) {
+  if (!P) return CLAIM_EINVAL;
+  HIP_TRY(hipSetDevice(P->device));
+  TRY(read_counters(P));
+  if (entries) *entries = P->host_ctr->id_entries;
+  if (ambiguous) *ambiguous = P->host_ctr->id_ambiguous;
   return CLAIM_OK;
 }
 

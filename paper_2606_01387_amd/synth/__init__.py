@@ -5,5 +5,5 @@ arithmetic and is shared by the product's tests, the oracle side and the
 benchmark.
 """
 
-from .claims import MISSING, Batch, FaultSpec, from_claims, make_batch, make_faults  # noqa: F401
+from .claims import MISSING, REQUEST_KINDS, Batch, FaultSpec, from_claims, make_batch, make_faults, make_requests  # noqa: F401
 from .workloads import FULL, LLAMA3_8B, LLAMA3_70B, MLA_FP8, STRESS, TINY, Geometry, Workload, scaled  # noqa: F401

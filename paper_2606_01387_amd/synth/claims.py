@@ -220,6 +220,58 @@ def make_batch(w: Workload) -> Batch:
     )
 
 
+REQUEST_KINDS = ("same", "cut", "changed", "extended", "fresh")
+
+
+def make_requests(w: Workload, batch: Batch, num_requests: int | None = None,
+                  mix=(0.3, 0.2, 0.2, 0.15, 0.15)) -> tuple[Batch, np.ndarray]:
+    """Reuse-lookup requests against an offloaded claim batch (token rows
+    only; block rows are empty).  Each request takes a uniformly chosen
+    source claim and is, with the probabilities in ``mix``: the same tokens;
+    a cut to a uniform length in [1, T]; the same length with one uniformly
+    chosen token changed; the tokens followed by 1..2*block_size fresh ones;
+    or T fresh tokens.  Returns the batch and the kind index of each row."""
+    bs = w.geometry.block_size
+    rng = np.random.default_rng(w.gen_seed ^ 0x10C0)
+    C = batch.num_claims
+    R = C if num_requests is None else num_requests
+    to = batch.token_offsets.astype(np.int64)
+    Tc = np.diff(to)
+    src = rng.integers(0, C, size=R)
+    kind = rng.choice(len(REQUEST_KINDS), size=R, p=np.asarray(mix) / np.sum(mix))
+    Ts = Tc[src]
+    L = Ts.copy()
+    cut = kind == 1
+    L[cut] = 1 + (rng.random(int(cut.sum())) * np.maximum(Ts[cut], 1)).astype(np.int64)
+    ext = kind == 3
+    L[ext] = Ts[ext] + rng.integers(1, 2 * bs + 1, size=int(ext.sum()))
+    L = np.maximum(L, 0)
+
+    ro = np.zeros(R + 1, np.int64)
+    ro[1:] = np.cumsum(L)
+    TT = int(ro[-1])
+    req_of_tok = np.repeat(np.arange(R), L)
+    m = np.arange(TT) - ro[req_of_tok]
+    copied = (kind[req_of_tok] != 4) & (m < Ts[req_of_tok])
+    tok = rng.integers(0, w.vocab, size=TT, dtype=np.int64)
+    tok[copied] = batch.tokens[(to[src[req_of_tok]] + m)[copied]]
+
+    # one changed token per "changed" request (never left equal)
+    ch = np.flatnonzero((kind == 2) & (L > 0))
+    pos = ro[ch] + (rng.random(ch.size) * L[ch]).astype(np.int64)
+    tok[pos] = (tok[pos] + 1 + rng.integers(0, w.vocab - 1, size=ch.size)) % w.vocab
+
+    ids = rng.integers(1, np.iinfo(np.int64).max, size=R, dtype=np.int64).astype(np.uint64)
+    req = Batch(
+        claim_ids=ids,
+        block_offsets=np.zeros(R + 1, np.uint32),
+        block_ids=np.zeros(0, np.uint32),
+        token_offsets=ro.astype(np.uint64),
+        tokens=tok.astype(np.uint32),
+    )
+    return req, kind
+
+
 def make_faults(w: Workload, batch: Batch | None = None) -> FaultSpec:
     """One flipped bit in each of round(rate * num_blocks) distinct pool
     blocks (referenced or not), plus num_load_failed reported load failures

@@ -43,6 +43,7 @@ def test_record_layouts_match_header(tmp_path):
     fields = {
         "claim_outcome": list(ck.OUTCOME_DTYPE.names),
         "claim_event": list(ck.EVENT_DTYPE.names),
+        "claim_lookup_result": list(ck.LOOKUP_DTYPE.names),
         "claim_pool_desc": [f for f, _ in ck.PoolDesc._fields_],
         "claim_batch": [f for f, _ in ck.CBatch._fields_],
         "claim_fault_spec": [f for f, _ in ck.CFaults._fields_],
@@ -60,7 +61,8 @@ def test_record_layouts_match_header(tmp_path):
     subprocess.run(["gcc", f"-I{ck.INCLUDE}", str(src), "-o", str(exe)], check=True)
     got = dict(ln.split() for ln in subprocess.run([str(exe)], capture_output=True, text=True,
                                                    check=True).stdout.splitlines())
-    for dt, st in ((ck.OUTCOME_DTYPE, "claim_outcome"), (ck.EVENT_DTYPE, "claim_event")):
+    for dt, st in ((ck.OUTCOME_DTYPE, "claim_outcome"), (ck.EVENT_DTYPE, "claim_event"),
+                   (ck.LOOKUP_DTYPE, "claim_lookup_result")):
         assert int(got[st]) == dt.itemsize
         for f in dt.names:
             assert int(got[f"{st}.{f}"]) == dt.fields[f][1], (st, f)
@@ -116,6 +118,8 @@ def test_null_arguments_are_rejected(L):
     assert L.outcomes_read(None, None, 0, None, None, 0, None) == ck.EINVAL
     assert L.claim_timing_read(None, None) == ck.EINVAL
     assert L.claim_block_state_read(None, 0, 0, None, None, None, None) == ck.EINVAL
+    assert L.claim_lookup(None, ctypes.byref(b), None, 0) == ck.EINVAL
+    assert L.claim_identity_stats(None, None, None) == ck.EINVAL
     assert L.claim_pool_destroy(None) == ck.OK
 
 

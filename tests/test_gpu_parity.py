@@ -11,7 +11,8 @@ first-failing-block indices are integers and must match bit for bit.
   outcomes and events, with real oracle digests for every block whose
   bytes change, every reported failure and a random sample of blocks (the
   other blocks keep their bytes, so their two digests are equal; the test
-  checks that on the GPU for every referenced block).
+  checks that on the GPU for every referenced block); and a reuse lookup of
+  as many requests as claims, with the identity-table counts.
 """
 
 from __future__ import annotations
@@ -25,7 +26,7 @@ import pytest
 
 from oracle import oracle as O
 from paper_2606_01387_amd.synth import (FULL, MISSING, TINY, FaultSpec, Geometry, Workload, content,
-                                        from_claims, make_batch, make_faults, scaled)
+                                        from_claims, make_batch, make_faults, make_requests, scaled)
 from tests.helpers import apply_flips, digests, modeled_digests
 
 pytestmark = pytest.mark.gpu
@@ -458,6 +459,7 @@ def test_full_size_parity(torch, ck, name):
     rng = np.random.default_rng(w.gen_seed + 1)
     ref = batch.unique_blocks(g.num_blocks)
     sample = rng.choice(ref, size=min(16, ref.size), replace=False)
+    reqs, _ = make_requests(w, batch)
     with ck.Pool(g, w.seed, kv, **capacities(batch)) as pool:
         pool.offload(db)
         pool.restore(db, faults=faults)
@@ -465,6 +467,8 @@ def test_full_size_parity(torch, ck, name):
         pool.check(db)
         out, ev = pool.read()
         st = pool.block_state()
+        lk = pool.lookup(ck.DeviceBatch(reqs))
+        stats = pool.identity_stats()
     note("  gpu done; oracle")
     d0, d1 = modeled_digests(w, faults, sample)
     op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
@@ -475,6 +479,13 @@ def test_full_size_parity(torch, ck, name):
     same_events(ev_pre, want_pre)
     same_outcomes(out, want)
     same_events(ev, op.events())
+    want_lk = op.lookup(reqs)
+    for f in want_lk.dtype.names:
+        if f != "pad":
+            assert np.array_equal(lk[f], want_lk[f]), f
+    assert stats == op.identity_stats()
+    note(f"  lookup status unknown/hit/partial/miss = {np.bincount(lk['status'], minlength=4).tolist()}, "
+         f"identities {stats}")
     changed = faults.changed_blocks()
     real = np.union1d(np.union1d(changed, faults.load_failed), sample).astype(np.int64)
     real = real[np.isin(real, ref)]

@@ -110,3 +110,33 @@ def test_predicates_cover_a_leading_prefix():
     assert np.array_equal(again.predicate_tokens, b.predicate_tokens)
     sub = b.subset([5, 2])
     assert sub.predicate_tokens.tolist() == [b.predicate_tokens[5], b.predicate_tokens[2]]
+
+
+def test_requests_follow_their_kinds():
+    """Lookup requests: same / cut / changed / extended copies of claim
+    token rows, or fresh rows, with the stated lengths."""
+    from paper_2606_01387_amd.synth import make_requests
+
+    w = replace(TINY, num_claims=200)
+    b = make_batch(w)
+    req, kind = make_requests(w, b, num_requests=500)
+    assert req.num_claims == 500 and req.num_refs == 0
+    assert np.unique(req.claim_ids).size == 500
+    counts = np.bincount(kind, minlength=5)
+    assert (counts > 40).all()
+    L = np.diff(req.token_offsets.astype(np.int64))
+    bs = w.geometry.block_size
+    rows = [req.tokens[int(req.token_offsets[i]):int(req.token_offsets[i + 1])] for i in range(500)]
+    claims = {tuple(b.claim(c)[2].tolist()) for c in range(b.num_claims)}
+    for i, k in enumerate(kind):
+        t = tuple(rows[i].tolist())
+        if k == 0:
+            assert t in claims
+        elif k == 1:
+            assert any(c[: len(t)] == t for c in claims) and len(t) >= 1
+        elif k == 2:
+            assert t not in claims or len(t) == 0
+        elif k == 3:
+            assert any(t[: len(c)] == c and 1 <= len(t) - len(c) <= 2 * bs for c in claims)
+    again, kind2 = make_requests(w, b, num_requests=500)
+    assert np.array_equal(again.tokens, req.tokens) and np.array_equal(kind, kind2)
