@@ -114,7 +114,7 @@ def main() -> int:
     import torch
 
     from paper_2606_01387_amd import claimkv as ck
-    from paper_2606_01387_amd.synth import FULL, content, make_batch, make_faults
+    from paper_2606_01387_amd.synth import FULL, content, make_batch, make_faults, make_requests
 
     w = FULL[args.workload]
     g = w.geometry
@@ -215,6 +215,20 @@ def main() -> int:
         marks[i + 1].record(stream)
     marks[-1].synchronize()
     per_check = np.array([marks[i].elapsed_time(marks[i + 1]) for i in range(steps)])
+
+    # reuse lookup of as many requests as claims, timed apart from the check
+    reqs, _ = make_requests(w, batch)
+    dreq = ck.DeviceBatch(reqs)
+    lk_buf = pool.lookup_async(dreq)
+    l0, l1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    l0.record(stream)
+    for _ in range(steps):
+        pool.lookup_async(dreq, out=lk_buf)
+    l1.record(stream)
+    l1.synchronize()
+    lookup_ms = l0.elapsed_time(l1) / steps
+    lk = lk_buf.cpu().numpy().view(ck.LOOKUP_DTYPE)[: reqs.num_claims]
+    identities = pool.identity_stats()
     pool.close()
 
     ms_per_step = (t1 - t0) * 1e3 / steps
@@ -273,6 +287,16 @@ def main() -> int:
             "measured_read_ceiling": round(read_ceiling, 1),
             "frac_of_read_ceiling": round(achieved / read_ceiling, 4),
         },
+    }
+    line["lookup"] = {
+        "requests": reqs.num_claims,
+        "request_tokens": reqs.num_tokens,
+        "ms": round(lookup_ms, 4),
+        "requests_per_s": round(reqs.num_claims / (lookup_ms * 1e-3), 1),
+        "tokens_per_s": round(reqs.num_tokens / (lookup_ms * 1e-3), 1),
+        "hit_tokens": int(lk["hit_tokens"].sum()),
+        "status_unknown_hit_partial_miss": np.bincount(lk["status"], minlength=4).tolist(),
+        "identities_registered_ambiguous": list(identities),
     }
     if round_trip is not None:
         line["round_trip"] = round_trip
