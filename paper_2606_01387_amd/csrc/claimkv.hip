@@ -289,12 +289,75 @@ __device__ __forceinline__ const IdEntry* id_find(const IdDev& t, uint64_t key) 
   return nullptr;
 }
 
-__device__ __forceinline__ uint64_t token_multilinear(const uint32_t* __restrict__ tok,
+// Token multilinear of one token block, sum over its tokens of tok * t_m.
+// With kPipelined the loads of a full 16-token chunk are issued together
+// and the next chunk is in flight while the current one is summed (the
+// tail of a partial block goes token by token); without it a plain loop
+// keeps the register count low.  The check takes the first form at every
+// group width (measured faster even at lower occupancy); lookup and
+// acceptance take it for wide groups only (narrow lookups were faster at
+// full occupancy).
+template <bool kPipelined>
+__device__ __forceinline__ uint64_t block_multilinear(const uint32_t* __restrict__ tok,
                                                       uint64_t first, uint64_t count,
                                                       const uint64_t* tkey) {
-  uint64_t m_sum = 0;
-  for (uint64_t m = 0; m < count; ++m) m_sum += (uint64_t)tok[first + m] * tkey[m];
+  constexpr int kChunk = 16;
+  uint64_t m_sum = 0, m = 0;
+  if constexpr (!kPipelined) {
+    for (; m < count; ++m) m_sum += (uint64_t)tok[first + m] * tkey[m];
+    return m_sum;
+  } else if (count >= kChunk) {
+    uint32_t cur[kChunk];
+#pragma unroll
+    for (int k = 0; k < kChunk; ++k) cur[k] = tok[first + k];
+    for (; m + kChunk <= count; m += kChunk) {
+      const bool more = m + 2 * kChunk <= count;
+      uint32_t nxt[kChunk];
+      if (more) {
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) nxt[k] = tok[first + m + kChunk + k];
+      }
+#pragma unroll
+      for (int k = 0; k < kChunk; ++k) m_sum += (uint64_t)cur[k] * tkey[m + k];
+      if (more) {
+#pragma unroll
+        for (int k = 0; k < kChunk; ++k) cur[k] = nxt[k];
+      }
+    }
+  }
+  for (; m < count; ++m) m_sum += (uint64_t)tok[first + m] * tkey[m];
   return m_sum;
+}
+
+// Put the wave-uniform value `val` into lane `lane` of `old` (v_writelane;
+// the lane select goes through M0, written by a scalar move, so the
+// instruction reads one scalar register besides it).
+__device__ __forceinline__ uint32_t write_lane(uint32_t old, uint32_t val, uint32_t lane) {
+  asm("v_writelane_b32 %0, %1, m0" : "+v"(old) : "s"(val), "{m0}"(lane));
+  return old;
+}
+
+// Chain steps t < steps of one window: h advances through the group's
+// multilinears, and lane t of the group keeps h_{j0 + t}.
+template <int W>
+__device__ __forceinline__ uint64_t chain_window(uint64_t& h, uint64_t m_sum, uint32_t gl,
+                                                 uint32_t gbase, uint64_t steps) {
+  if constexpr (W == 64) {  // one claim per wave: the chain runs on the scalar ALU
+    uint32_t lo = 0, hi = 0;
+    for (uint32_t t = 0; t < steps; ++t) {
+      h = splitmix_step(h ^ uniform_read64(m_sum, t));
+      lo = write_lane(lo, (uint32_t)h, t);
+      hi = write_lane(hi, (uint32_t)(h >> 32), t);
+    }
+    return ((uint64_t)hi << 32) | lo;
+  } else {
+    uint64_t my_h = 0;
+    for (uint32_t t = 0; t < steps; ++t) {
+      h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
+      if (gl == t) my_h = h;
+    }
+    return my_h;
+  }
 }
 
 __device__ __forceinline__ void load_token_keys(uint64_t* tkey, uint32_t bs, uint64_t seed) {
@@ -353,7 +416,9 @@ __global__ void __launch_bounds__(kThreads) k_mark_entries(const uint32_t* __res
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += stride) {
     const uint32_t blk = bi[i];
-    if (blk < nb && valid_off[blk]) mark[blk] = 1;
+    // most blocks are listed many times: read before writing, so that the
+    // stores (all of the same value) stay about one per block
+    if (blk < nb && !mark[blk] && valid_off[blk]) mark[blk] = 1;
   }
 }
 
@@ -644,21 +709,10 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
     if (j < nt) {
       const uint64_t first = j * bs;
       const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
-      m_sum = token_multilinear(b.tok, r.to0 + first, count, tkey);
+      m_sum = block_multilinear<(W >= 16)>(b.tok, r.to0 + first, count, tkey);
     }
     const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
-    uint64_t my_h = 0;
-    if constexpr (W == 64) {  // one claim per wave: the chain runs on the scalar ALU
-      for (uint32_t t = 0; t < steps; ++t) {
-        h = splitmix_step(h ^ uniform_read64(m_sum, t));
-        if (gl == t) my_h = h;
-      }
-    } else {
-      for (uint32_t t = 0; t < steps; ++t) {
-        h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
-        if (gl == t) my_h = h;
-      }
-    }
+    const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
     if (j < npos) {
       reg.idn[fp_base + r.bo0 + j] = my_h;
       if (offloaded) id_register(ids, my_h, b.bi[(uint64_t)r.bo0 + j], ctr);
@@ -867,22 +921,45 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   const uint64_t L = n > nt ? n : nt;
   for (uint64_t j0 = 0; j0 < L; j0 += W) {
     const uint64_t j = j0 + gl;
+    // the window's loads that depend only on j, issued together
+    uint32_t blk = kNone, acc_blk = kNone;
+    uint64_t acc_h = 0;
+    if (j < n) blk = b.bi[(uint64_t)r.bo0 + j];
+    if (found && j < common) acc_blk = reg.fp[fpo + j];
+    if (j < id_pos) acc_h = reg.idn[fpo + j];
+    uint64_t m_sum = 0;
+    if (j < nt) {
+      const uint64_t first = j * bs;
+      const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
+      m_sum = block_multilinear<true>(b.tok, r.to0 + first, count, tkey);
+    }
+    // per-block state, loaded unconditionally (block 0 stands in for a
+    // lane without a pool block) so that it is in flight while the chain
+    // runs; the empty asm keeps every use, and so the wait, after the chain
+    const uint32_t sb = (j < n && blk < nb) ? blk : 0u;
+    uint32_t rec = st.valid_off[sb];
+    uint32_t lfb = st.load_failed[sb];
+    uint64_t d_res = st.d_res[sb];
+    uint64_t d_off = st.d_off[sb];
+    const uint64_t steps = j0 < nt ? (nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W) : 0;
+    const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
+    asm volatile("" : "+v"(rec), "+v"(lfb), "+v"(d_res), "+v"(d_off));
+
     uint64_t my_key = kNoKey;
     if (j < n) {
-      const uint32_t blk = b.bi[(uint64_t)r.bo0 + j];
-      if (found && j < common && blk != reg.fp[fpo + j]) {
+      if (found && j < common && blk != acc_blk) {
         reasons |= CLAIM_R_FOOTPRINT_MISMATCH;
         my_key = j;
       }
       if (blk >= nb) {
         reasons |= CLAIM_R_MISSING_ENTRY;
         my_key = j < my_key ? j : my_key;
-      } else if (!st.valid_off[blk]) {
+      } else if (!rec) {
         reasons |= CLAIM_R_NO_OFFLOAD_RECORD;
         my_key = j < my_key ? j : my_key;
       } else {
-        const bool lf = st.load_failed[blk] != 0;
-        const bool mm = st.d_res[blk] != st.d_off[blk];
+        const bool lf = lfb != 0;
+        const bool mm = d_res != d_off;
         if ((lf || mm) && j < intact) intact = j;
         if (j >= pred) {
           // past the predicate: the claimed prefix is still intact
@@ -896,26 +973,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       }
       if (my_key != kNoKey && j < intact) intact = j;
     }
-    uint64_t m_sum = 0;
-    if (j < nt) {
-      const uint64_t first = j * bs;
-      const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
-      m_sum = token_multilinear(b.tok, r.to0 + first, count, tkey);
-    }
-    const uint64_t steps = j0 < nt ? (nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W) : 0;
-    uint64_t my_h = 0;
-    if constexpr (W == 64) {  // one claim per wave: the chain runs on the scalar ALU
-      for (uint32_t t = 0; t < steps; ++t) {
-        h = splitmix_step(h ^ uniform_read64(m_sum, t));
-        if (gl == t) my_h = h;
-      }
-    } else {
-      for (uint32_t t = 0; t < steps; ++t) {
-        h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
-        if (gl == t) my_h = h;
-      }
-    }
-    if (j < id_pos && my_h != reg.idn[fpo + j]) {  // cache identity of block j
+    if (j < id_pos && my_h != acc_h) {  // cache identity of block j
       reasons |= CLAIM_R_TOKEN_MISMATCH;
       my_key = j < my_key ? j : my_key;
       if (j < intact) intact = j;
@@ -1015,22 +1073,11 @@ __global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids, uint
     if (j < nt) {
       const uint64_t first = j * bs;
       const uint64_t count = ntok - first < bs ? ntok - first : bs;
-      m_sum = token_multilinear(b.tok, to0 + first, count, tkey);
+      m_sum = block_multilinear<(W >= 16)>(b.tok, to0 + first, count, tkey);
     }
     const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
     const uint64_t h_before = h;
-    uint64_t my_h = 0;
-    if constexpr (W == 64) {
-      for (uint32_t t = 0; t < steps; ++t) {
-        h = splitmix_step(h ^ uniform_read64(m_sum, t));
-        if (gl == t) my_h = h;
-      }
-    } else {
-      for (uint32_t t = 0; t < steps; ++t) {
-        h = splitmix_step(h ^ lane_read64(m_sum, gbase + t));
-        if (gl == t) my_h = h;
-      }
-    }
+    const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
     uint64_t my_stop = kNoKey;
     if (j < nt) {
       const IdEntry* e = id_find(ids, my_h);
