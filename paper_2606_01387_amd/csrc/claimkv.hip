@@ -10,30 +10,38 @@
 //
 //  * Block digest (the HBM-bound stage).  The pool is plane-major
 //    [plane][block][chunk].  D(b) = sum_i w_i k_i is linear in the words, so
-//    it splits into partial sums over (plane, segment) pieces of the
-//    canonical block: the key k_i depends only on the word's canonical
-//    position, so a wave pinned to one (plane, segment) keeps that piece's
-//    keys in VGPRs for its whole life and streams the same piece of many
-//    blocks.  A piece is 64 lanes x LPT 16-byte vectors (LPT = 8: 8 KiB);
-//    each load instruction moves 1 KiB of contiguous, coalesced bytes.
-//    Each 64-bit word costs one 32x32->64 multiply-add for lo(w) lo(k) and
-//    two 32-bit multiply-adds for the cross terms (only their low 32 bits
-//    reach the result mod 2^64).  The wave sum is written as one partial per
-//    (block, piece); a second small kernel adds a block's partials.  No
-//    atomics, so results are bitwise deterministic.
+//    it splits into partial sums over pieces of the canonical block: a piece
+//    is one 64-lane x LPT 16-byte-vector segment of a plane's chunk (LPT up
+//    to 16: 16 KiB), and since k_i depends only on the word's canonical
+//    position, a wave pinned to one piece keeps that piece's keys in VGPRs
+//    and streams the same piece of many blocks, with all LPT loads in flight
+//    before any use.  The 4 waves of a workgroup take 4 consecutive pieces
+//    of the same blocks and park their per-block sums in an LDS ring, which
+//    the workgroup adds and writes as one contiguous run of partials; the
+//    grid is exactly one resident round.  Each 64-bit word costs one
+//    32x32->64 multiply-add for lo(w) lo(k) and two 32-bit multiply-adds for
+//    the cross terms (only their low 32 bits reach the result mod 2^64).  A
+//    small kernel adds each block's partials.  No atomics: results are
+//    bitwise deterministic.
 //  * Unique blocks.  Blocks referenced by a batch are marked, then compacted
 //    in ascending order, so each physical block is read once however many
 //    claims alias it.
-//  * Claims.  A group of W lanes (W = 2..64, picked from the batch's mean
-//    claim length) owns one claim: lanes take block positions j = j0 + lane,
-//    test their block (footprint, missing entry, offload record, reported
-//    failure, digest mismatch) and compute the token multilinear M_j; the
-//    serial chain h_j = splitmix64(h_{j-1} ^ M_j) then walks the W
-//    positions of the round through lane shuffles.  The outcome is the
-//    minimum of packed keys (class << 32 | position).
-//  * Events.  Per-claim event counts (0..2) are scanned in three small
-//    kernels (tile sums, one-workgroup scan of the tile sums, write) so the
-//    log stays in batch order with no spin waits.
+//  * Claims.  A group of W lanes (W = 2..64, from the batch's mean claim
+//    length) owns one claim: lanes take block positions j = j0 + lane.  A
+//    window first issues every load that depends only on j (block id,
+//    accepted block and identity, the block's tokens), then the per-block
+//    state, which stays in flight while the serial chain
+//    h_j = splitmix64(h_{j-1} ^ M_j) walks the window (on the scalar unit
+//    when W = 64); the checks (footprint, identity, missing entry, offload
+//    record, reported failure, digest mismatch, predicate) follow.  The
+//    outcome is the minimum of packed keys (class << 32 | position).
+//  * Cache identity.  Offload registers (h_j -> block) of offloaded claims
+//    in an open-addressing table with order-independent atomics; a lookup
+//    walks a request's chain and probes it block by block.
+//  * Events.  Per-claim event counts (0..2) are scanned by one workgroup for
+//    batches up to 16K claims, else in three small kernels (tile sums,
+//    one-workgroup scan of the tile sums, write), so the log stays in batch
+//    order with no spin waits.
 
 #include <hip/hip_runtime.h>
 
@@ -105,7 +113,7 @@ __device__ __forceinline__ uint64_t uniform_read64(uint64_t v, uint32_t lane) {
 // chain runs on the scalar ALU.
 template <int W>
 __device__ __forceinline__ uint64_t group_claim() {
-  const uint64_t c = ((uint64_t)blockIdx.x * 256 + threadIdx.x) / W;
+  const uint64_t c = ((uint64_t)blockIdx.x * kThreads + threadIdx.x) / W;
   if constexpr (W == 64) {
     const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)c);
     const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(c >> 32));
