@@ -15,8 +15,8 @@ from oracle import oracle as O
 from paper_2606_01387_amd.synth import (FULL, TINY, Geometry, Workload, from_claims, make_batch,
                                         make_faults, make_requests, scaled)
 from tests.helpers import apply_flips, digests
-from tests.test_gpu_parity import (LONG_CLAIMS, capacities, free_gpu, gpu_pool_tensor, note,
-                                   same_events, same_outcomes)
+from tests.test_gpu_parity import (LONG_CLAIMS, MAX_BS_LONG, MAX_BS_SHORT, MIN_BS, capacities,
+                                   free_gpu, gpu_pool_tensor, note, same_events, same_outcomes)
 
 pytestmark = pytest.mark.gpu
 
@@ -55,6 +55,9 @@ LOOKUP_CASES = [
     scaled(FULL["small-claim-stress"], 256, 30000),
     scaled(FULL["mla-fp8"], 40, 60),
     LONG_CLAIMS,
+    MAX_BS_SHORT,
+    MAX_BS_LONG,
+    MIN_BS,
 ]
 
 
@@ -62,7 +65,7 @@ LOOKUP_CASES = [
 def test_lookup_parity(torch, ck, w):
     g = w.geometry
     batch = make_batch(w)
-    reqs, kind = make_requests(w, batch, num_requests=2 * batch.num_claims)
+    reqs, kind = make_requests(w, batch, num_requests=max(2 * batch.num_claims, 64))
     note(f"lookup parity {w.name}: {batch.num_claims} claims, {reqs.num_claims} requests, "
          f"{reqs.num_tokens} request tokens")
     kv = torch.zeros(g.pool_bytes, dtype=torch.uint8, device="cuda")

@@ -121,6 +121,22 @@ LONG_CLAIMS = Workload(
     length=("blocks", 100, 300, True), sharing=("fraction", 0.5), corrupt_rate=0.1,
     missing_claim_rate=0.25, num_load_failed=1, gen_seed=21, content_seed=22)
 
+# block-size extremes: 1024-token blocks (the largest a pool accepts) with
+# short claims (narrow groups) and long ones (one claim per wave), and
+# 1-token blocks, whose 16-byte chunks are the smallest possible
+MAX_BS_SHORT = Workload(
+    name="bs1024-short", geometry=Geometry(1, 1, 1024, 1, 8, 2, 12), seed=31, num_claims=40,
+    length=("blocks", 1, 3, True), sharing=("fraction", 0.3), corrupt_rate=0.25, num_load_failed=1,
+    gen_seed=32, content_seed=33)
+MAX_BS_LONG = Workload(
+    name="bs1024-long", geometry=Geometry(1, 1, 1024, 1, 8, 2, 12), seed=34, num_claims=6,
+    length=("blocks", 40, 70, True), sharing=("fraction", 0.5), corrupt_rate=0.2, num_load_failed=1,
+    gen_seed=35, content_seed=36)
+MIN_BS = Workload(
+    name="bs1-16-byte-chunk", geometry=Geometry(1, 2, 1, 1, 8, 2, 40), seed=37, num_claims=30,
+    length=("blocks", 1, 90, True), sharing=("zipf", 1.2, 5), corrupt_rate=0.1, num_load_failed=2,
+    gen_seed=38, content_seed=39)
+
 SCALED = [
     replace(TINY, num_load_failed=1),
     scaled(FULL["llama3-8b"], 48, 60, corrupt_rate=0.1, num_load_failed=2),
@@ -139,6 +155,9 @@ SCALED = [
                    predicate_fraction=0.6), name="llama3-8b-predicate"),
     replace(scaled(FULL["small-claim-stress"], 256, 30000, corrupt_rate=0.05, num_load_failed=3,
                    predicate_fraction=0.5), name="stress-predicate"),
+    MAX_BS_SHORT,
+    MAX_BS_LONG,
+    MIN_BS,
 ]
 
 
