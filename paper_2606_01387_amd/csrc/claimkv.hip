@@ -11,10 +11,10 @@
 //  * Block digest (the HBM-bound stage).  The pool is plane-major
 //    [plane][block][chunk].  D(b) = sum_i w_i k_i is linear in the words, so
 //    it splits into partial sums over pieces of the canonical block: a piece
-//    is one 64-lane x LPT 16-byte-vector segment of a plane's chunk (LPT up
-//    to 16: 16 KiB), and since k_i depends only on the word's canonical
+//    is one 64-lane x LPW 8-byte-word segment of a plane's chunk (LPW up
+//    to 32: 16 KiB), and since k_i depends only on the word's canonical
 //    position, a wave pinned to one piece keeps that piece's keys in VGPRs
-//    and streams the same piece of many blocks, with all LPT loads in flight
+//    and streams the same piece of many blocks, with all LPW loads in flight
 //    before any use.  The 4 waves of a workgroup take 4 consecutive pieces
 //    of the same blocks and park their per-block sums in an LDS ring, which
 //    the workgroup adds and writes as one contiguous run of partials; the
@@ -494,21 +494,27 @@ __global__ void __launch_bounds__(1024) k_compact(uint8_t* __restrict__ mark, ui
 // ----------------------------------------------------------- digest kernel
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Partial digests of the unique blocks.
 //
-// A piece is one 64-lane x LPT-vector segment of a plane's chunk (piece
-// index ps = plane * segs + segment).  Workgroup (piece group pg, group g)
-// runs 4 waves on the 4 consecutive pieces 4pg .. 4pg+3 of the same blocks
-// u = g, g + groups, g + 2 groups, ...: lane l, slot k of a wave covers
-// 16-byte vector v = s*64*LPT + 64k + l of the plane's chunk, i.e.
-// canonical words i = p*2V + 2v and 2v + 1, whose keys it keeps in VGPRs.
+// A piece is one 64-lane x LPW-word segment of a plane's chunk (piece index
+// ps = plane * segs + segment).  Workgroup (piece group pg, group g) runs 4
+// waves on the 4 consecutive pieces 4pg .. 4pg+3 of the same blocks
+// u = g, g + groups, g + 2 groups, ...: lane l, slot k of a wave covers the
+// 64-bit word q = s*64*LPW + 64k + l of the plane's chunk, canonical word
+// i = p*CW + q, whose key it keeps in VGPRs.  Each load instruction moves
+// 512 contiguous bytes (8 per lane); 8-byte loads measured about 2 % faster
+// than 16-byte loads at the same bytes in flight per wave.
 // Each wave's per-block sum goes to an LDS ring; when the ring is full (or
 // the blocks run out) the workgroup adds its 4 rings and writes one
 // contiguous run of per-(piece group, block) partials,
 //   partial[(pg * groups + g) * NW + n],  NW = ceil(U / groups),
 // so the streaming reads are not interleaved with scattered small writes.
-// Optionally copies the vectors to staging ([slot][plane][chunk], slot =
+// (Giving the 4 waves the same piece of 4 adjacent blocks instead, which
+// reads whole runs of adjacent chunks when a chunk is one piece, measured
+// about 1 % slower on 16 KiB chunks.)
+// Optionally copies the words to staging ([slot][plane][chunk], slot =
 // unique index).
 constexpr int kRing = 256;
 
@@ -537,15 +543,15 @@ __device__ __forceinline__ uint64_t dpp_wave_sum64(uint64_t v) {
 }
 
 // RAGGED: the chunk's last segment is partly past its end (masked slots).
-// STAGE: also copy the vectors to staging (offload with staging).
-template <int LPT, bool RAGGED, bool STAGE>
-__global__ void __launch_bounds__(kThreads) k_digest(const u32x4* __restrict__ pool, uint32_t nb,
-                                                     uint32_t chunk_vecs, uint32_t planes,
+// STAGE: also copy the words to staging (offload with staging).
+template <int LPW, bool RAGGED, bool STAGE>
+__global__ void __launch_bounds__(kThreads) k_digest(const u32x2* __restrict__ pool, uint32_t nb,
+                                                     uint32_t chunk_words, uint32_t planes,
                                                      uint32_t segs, uint32_t groups,
                                                      const uint32_t* __restrict__ uniq,
                                                      const Counters* __restrict__ ctr,
                                                      uint64_t seed, uint64_t* __restrict__ partial,
-                                                     u32x4* __restrict__ staging) {
+                                                     u32x2* __restrict__ staging) {
   __shared__ uint64_t ring[kThreads / 64][kRing];
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -557,57 +563,53 @@ __global__ void __launch_bounds__(kThreads) k_digest(const u32x4* __restrict__ p
   const uint32_t ps = pg * 4 + w;
   const bool active = ps < ps_total;  // wave-uniform: the last piece group may be short
   const uint32_t p = active ? ps / segs : 0, s = active ? ps % segs : 0;
-  const uint32_t v0 = s * 64u * LPT + lane;  // this lane's vector in slot 0
+  const uint32_t q0 = s * 64u * LPW + lane;  // this lane's word in slot 0
 
-  uint32_t klo[LPT][2], khi[LPT][2];
+  uint32_t klo[LPW], khi[LPW];
 #pragma unroll
-  for (int k = 0; k < LPT; ++k) {
-    const uint32_t v = v0 + 64u * k;
-    const bool ok = !RAGGED || v < chunk_vecs;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const uint64_t key = stream_output(seed, (uint64_t)p * chunk_vecs * 2 + 2ull * v + h) | 1ull;
-      klo[k][h] = ok ? (uint32_t)key : 0u;  // a masked slot contributes 0
-      khi[k][h] = ok ? (uint32_t)(key >> 32) : 0u;
-    }
+  for (int k = 0; k < LPW; ++k) {
+    const uint32_t q = q0 + 64u * k;
+    const uint64_t key = stream_output(seed, (uint64_t)p * chunk_words + q) | 1ull;
+    const bool ok = !RAGGED || q < chunk_words;
+    klo[k] = ok ? (uint32_t)key : 0u;  // a masked slot contributes 0
+    khi[k] = ok ? (uint32_t)(key >> 32) : 0u;
   }
 
   const uint32_t U = ctr->uniq_count;
   const uint32_t NW = (U + groups - 1) / groups;
-  const u32x4* plane = pool + (uint64_t)p * nb * chunk_vecs;
+  const u32x2* plane = pool + (uint64_t)p * nb * chunk_words;
   uint32_t n = 0;
   for (uint32_t u = g; u < U; u += groups, ++n) {
     uint64_t sum = 0;
     if (active) {
-      const u32x4* chunk = plane + (uint64_t)uniq[u] * chunk_vecs;
-      u32x4 x[LPT];
+      const u32x2* chunk = plane + (uint64_t)uniq[u] * chunk_words;
+      const u32x2* lanep = chunk + q0;  // slot k at lanep + 64k: immediate offsets
+      u32x2 x[LPW];
 #pragma unroll
-      for (int k = 0; k < LPT; ++k) {
-        // a masked slot reads the chunk's first vector (its key is 0): no
+      for (int k = 0; k < LPW; ++k) {
+        // a masked slot reads the chunk's first word (its key is 0): no
         // address outside the chunk is ever formed
-        const uint32_t v = v0 + 64u * k;
-        x[k] = __builtin_nontemporal_load(chunk + ((!RAGGED || v < chunk_vecs) ? v : 0u));
+        if (!RAGGED || q0 + 64u * k < chunk_words)
+          x[k] = __builtin_nontemporal_load(lanep + 64 * k);
+        else
+          x[k] = __builtin_nontemporal_load(chunk);
       }
       __builtin_amdgcn_sched_barrier(0);  // every load in flight before any use
       uint64_t acc = 0;
       uint32_t cross = 0;
 #pragma unroll
-      for (int k = 0; k < LPT; ++k) {
-        // word 0 = (x.y:x.x), word 1 = (x.w:x.z); only the low 32 bits of
-        // the cross terms reach the product mod 2^64
-        acc += (uint64_t)x[k].x * klo[k][0];
-        cross += x[k].x * khi[k][0] + x[k].y * klo[k][0];
-        acc += (uint64_t)x[k].z * klo[k][1];
-        cross += x[k].z * khi[k][1] + x[k].w * klo[k][1];
+      for (int k = 0; k < LPW; ++k) {
+        // word = (x.y:x.x); only the low 32 bits of the cross terms reach
+        // the product mod 2^64
+        acc += (uint64_t)x[k].x * klo[k];
+        cross += x[k].x * khi[k] + x[k].y * klo[k];
       }
       sum = dpp_wave_sum64(acc + ((uint64_t)cross << 32));
       if constexpr (STAGE) {
-        u32x4* dst = staging + ((uint64_t)u * planes + p) * chunk_vecs;
+        u32x2* dst = staging + ((uint64_t)u * planes + p) * chunk_words + q0;
 #pragma unroll
-        for (int k = 0; k < LPT; ++k) {
-          const uint32_t v = v0 + 64u * k;
-          if (!RAGGED || v < chunk_vecs) dst[v] = x[k];
-        }
+        for (int k = 0; k < LPW; ++k)
+          if (!RAGGED || q0 + 64u * k < chunk_words) dst[64 * k] = x[k];
       }
     }
     const uint32_t slot = n % kRing;
@@ -1289,7 +1291,7 @@ struct claim_pool {
   uint64_t chunk_bytes = 0, chunk_vecs = 0, block_bytes = 0, seed = 0;
   void* kv = nullptr;
 
-  int lpt = 8;
+  int lpw = 32;
   uint32_t segs = 1, ps_total = 1, pgs = 1, groups = 1;
 
   uint64_t *d_off = nullptr, *d_res = nullptr, *partial = nullptr;
@@ -1510,22 +1512,22 @@ int select_blocks(claim_pool* P, const claim_batch* b, int mode) {
   return hip_status(hipGetLastError());
 }
 
-template <int LPT>
-int launch_digest_lpt(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_cu) {
-  const bool ragged = (uint64_t)P->segs * 64 * LPT != P->chunk_vecs;
+template <int LPW>
+int launch_digest_lpw(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_cu) {
+  const uint32_t cw = (uint32_t)(2 * P->chunk_vecs);
+  const bool ragged = (uint64_t)P->segs * 64 * LPW != cw;
   const void* fn;
   if (ragged)
-    fn = staging ? (const void*)k_digest<LPT, true, true> : (const void*)k_digest<LPT, true, false>;
+    fn = staging ? (const void*)k_digest<LPW, true, true> : (const void*)k_digest<LPW, true, false>;
   else
-    fn = staging ? (const void*)k_digest<LPT, false, true> : (const void*)k_digest<LPT, false, false>;
+    fn = staging ? (const void*)k_digest<LPW, false, true> : (const void*)k_digest<LPW, false, false>;
   if (wgs_per_cu)  // occupancy query only
     return hip_status(hipOccupancyMaxActiveBlocksPerMultiprocessor(wgs_per_cu, fn, kThreads, 0));
-  const u32x4* pool = (const u32x4*)P->kv;
-  u32x4* st = (u32x4*)staging;
+  const u32x2* pool = (const u32x2*)P->kv;
+  u32x2* st = (u32x2*)staging;
   const dim3 grid(P->pgs * P->groups), block(kThreads);
-  uint32_t cv = (uint32_t)P->chunk_vecs;
 #define GO(R, S)                                                                                \
-  hipLaunchKernelGGL((k_digest<LPT, R, S>), grid, block, 0, P->stream, pool, P->nb, cv, P->planes, \
+  hipLaunchKernelGGL((k_digest<LPW, R, S>), grid, block, 0, P->stream, pool, P->nb, cw, P->planes, \
                      P->segs, P->groups, P->uniq, P->ctr, P->seed, partial, st)
   if (ragged) {
     if (staging) GO(true, true); else GO(true, false);
@@ -1538,13 +1540,12 @@ int launch_digest_lpt(claim_pool* P, uint64_t* partial, void* staging, int* wgs_
 
 // Launch the digest (or, with wgs_per_cu, query its occupancy).
 int launch_digest(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_cu = nullptr) {
-  switch (P->lpt) {
+  switch (P->lpw) {
 #define DIGEST_CASE(l) \
   case l:              \
-    return launch_digest_lpt<l>(P, partial, staging, wgs_per_cu);
-    DIGEST_CASE(1) DIGEST_CASE(2) DIGEST_CASE(3) DIGEST_CASE(4) DIGEST_CASE(5) DIGEST_CASE(6)
-    DIGEST_CASE(7) DIGEST_CASE(8) DIGEST_CASE(9) DIGEST_CASE(10) DIGEST_CASE(11) DIGEST_CASE(12)
-    DIGEST_CASE(13) DIGEST_CASE(14) DIGEST_CASE(15) DIGEST_CASE(16)
+    return launch_digest_lpw<l>(P, partial, staging, wgs_per_cu);
+    DIGEST_CASE(1) DIGEST_CASE(2) DIGEST_CASE(4) DIGEST_CASE(8) DIGEST_CASE(12) DIGEST_CASE(16)
+    DIGEST_CASE(24) DIGEST_CASE(32)
 #undef DIGEST_CASE
     default:
       return CLAIM_EINVAL;
@@ -1609,27 +1610,32 @@ int append_events(claim_pool* P, const claim_batch* b) {
     HIP_TRY(hipGetLastError());                                                                 \
   } while (0)
 
-// Choose vectors per lane (LPT), segments per chunk and the digest grid.
-// LPT is the divisor of the chunk's vectors-per-lane closest to 16 (ties:
-// the larger), so every segment is full and each wave streams up to 16 KiB
-// per block; chunks that are not a whole number of 1 KiB rows use LPT 16
-// with a ragged last segment.  The grid holds exactly as many workgroups as
-// can be resident at once (no tail of late waves): groups = resident
-// workgroups / piece groups.
+// Choose words per lane (LPW), segments per chunk and the digest grid.
+// LPW is the largest instantiated width (32, 24, 16, 12, 8, ...) that
+// divides the chunk's words-per-lane, so every segment is full and each wave
+// streams up to 16 KiB per block; chunks that are not a whole number of
+// 512-byte rows, or whose only exact widths are tiny, use the smallest width
+// covering the chunk (at most 32) with a ragged last segment.  The grid
+// holds exactly as many workgroups as can be resident at once (no tail of
+// late waves): groups = resident workgroups / piece groups.
 int choose_digest_shape(claim_pool* P) {
-  const uint64_t V = P->chunk_vecs;
-  const uint64_t Q = (V + 63) / 64;  // vectors per lane to cover one chunk
+  static const int kLpw[] = {32, 24, 16, 12, 8, 4, 2, 1};  // instantiated widths, descending
+  const uint64_t CW = 2 * P->chunk_vecs;  // 64-bit words per chunk
+  const uint64_t Q = (CW + 63) / 64;      // words per lane to cover one chunk
   int best = 0;
-  if (V % 64 == 0) {
-    for (int d = 16; d >= 1; --d)
+  if (CW % 64 == 0)
+    for (int d : kLpw)
       if (Q % d == 0) {
         best = d;
         break;
       }
-    if (best < 4 && Q > 16) best = 0;  // only tiny divisors: use a ragged tail instead
+  if (best && best < 8 && Q > 32) best = 0;  // only tiny exact widths: use a ragged tail
+  if (best == 0) {                           // ragged: the smallest width covering Q, at most 32
+    best = 32;
+    for (int d : kLpw)
+      if ((uint64_t)d >= Q) best = d;
   }
-  if (best == 0) best = Q < 16 ? (int)Q : 16;
-  P->lpt = best;
+  P->lpw = best;
   P->segs = (uint32_t)((Q + best - 1) / best);
   P->ps_total = P->planes * P->segs;
   P->pgs = (P->ps_total + 3) / 4;

@@ -6,9 +6,10 @@
 //    directly into a pool too large to build on the host.  A GPU test
 //    compares the two.
 //  * synth_copy_probe and synth_read_probe are plain streaming kernels with
-//    the checker's load form (16-byte non-temporal loads, 1 KiB contiguous
-//    per wave instruction): the copy calibrates the HBM byte counters, the
-//    read measures the achievable streaming-read bandwidth of a buffer.
+//    the checker's load form (8-byte non-temporal loads, 512 contiguous
+//    bytes per wave instruction): the copy calibrates the HBM byte counters,
+//    the read measures the achievable streaming-read bandwidth of a buffer
+//    (8-byte loads were the fastest plain read measured on this GPU).
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -88,27 +89,27 @@ __global__ void __launch_bounds__(256) fill_kernel(uint4* __restrict__ pool, uin
   }
 }
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-__global__ void __launch_bounds__(256) copy_kernel(u32x4* __restrict__ dst,
-                                                   const u32x4* __restrict__ src, uint64_t n) {
+__global__ void __launch_bounds__(256) copy_kernel(u32x2* __restrict__ dst,
+                                                   const u32x2* __restrict__ src, uint64_t n) {
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
     dst[i] = __builtin_nontemporal_load(src + i);
 }
 
-// Each thread reads 8 vectors per step, 256 apart (1 KiB per wave
-// instruction); n is a multiple of 2048 vectors.
-__global__ void __launch_bounds__(256) read_kernel(const u32x4* __restrict__ src, uint64_t n,
+// Each thread reads 16 words per step, 256 apart (512 bytes per wave
+// instruction); n is a multiple of 4096 words.
+__global__ void __launch_bounds__(256) read_kernel(const u32x2* __restrict__ src, uint64_t n,
                                                    uint32_t* __restrict__ sink) {
-  const uint64_t stride = (uint64_t)gridDim.x * 256 * 8;
+  const uint64_t stride = (uint64_t)gridDim.x * 256 * 16;
   uint32_t acc = 0;
-  for (uint64_t i = (uint64_t)blockIdx.x * 256 * 8 + threadIdx.x; i < n; i += stride) {
-    u32x4 x[8];
+  for (uint64_t i = (uint64_t)blockIdx.x * 256 * 16 + threadIdx.x; i < n; i += stride) {
+    u32x2 x[16];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) x[k] = __builtin_nontemporal_load(src + i + 256 * k);
+    for (int k = 0; k < 16; ++k) x[k] = __builtin_nontemporal_load(src + i + 256 * k);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) acc ^= x[k].x ^ x[k].y ^ x[k].z ^ x[k].w;
+    for (int k = 0; k < 16; ++k) acc ^= x[k].x ^ x[k].y;
   }
   if (acc == 0x9E3779B9u) sink[0] = acc;  // practically never: keeps the loads live
 }
@@ -120,8 +121,8 @@ extern "C" {
 // Copy nbytes (a multiple of 16, both pointers 16-byte aligned) on stream.
 int synth_copy_probe(void* dst, const void* src, uint64_t nbytes, void* stream) {
   if (!dst || !src || nbytes % 16 || ((uintptr_t)dst & 15) || ((uintptr_t)src & 15)) return -1;
-  hipLaunchKernelGGL(copy_kernel, dim3(4096), dim3(256), 0, (hipStream_t)stream, (u32x4*)dst,
-                     (const u32x4*)src, nbytes / 16);
+  hipLaunchKernelGGL(copy_kernel, dim3(4096), dim3(256), 0, (hipStream_t)stream, (u32x2*)dst,
+                     (const u32x2*)src, nbytes / 8);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
@@ -129,10 +130,10 @@ int synth_copy_probe(void* dst, const void* src, uint64_t nbytes, void* stream) 
 // with grid = cus * 16 workgroups; sink is a 4-byte device scratch word.
 int synth_read_probe(const void* src, uint64_t nbytes, uint32_t cus, void* sink, void* stream) {
   if (!src || !sink || ((uintptr_t)src & 15) || cus == 0) return -1;
-  const uint64_t n = (nbytes / 16) / 2048 * 2048;
+  const uint64_t n = (nbytes / 8) / 4096 * 4096;
   if (n == 0) return -1;
   hipLaunchKernelGGL(read_kernel, dim3(cus * 16), dim3(256), 0, (hipStream_t)stream,
-                     (const u32x4*)src, n, (uint32_t*)sink);
+                     (const u32x2*)src, n, (uint32_t*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -423,9 +423,16 @@ def test_capacity_errors(torch, ck):
 # ------------------------------------------------------------- staged round trip
 
 
+STAGED = [
+    scaled(FULL["mla-fp8"], 30, 40, corrupt_rate=0.1, num_load_failed=1),  # 3 pieces per chunk
+    scaled(FULL["small-claim-stress"], 96, 300, corrupt_rate=0.1, num_load_failed=1),  # 1 piece
+    TINY_CHUNK,  # 48-byte chunks: one ragged piece
+]
+
+
 @pytest.mark.parametrize("where", ["device", "pinned-host"])
-def test_staged_round_trip(torch, ck, where):
-    w = scaled(FULL["mla-fp8"], 30, 40, corrupt_rate=0.1, num_load_failed=1)
+@pytest.mark.parametrize("w", STAGED, ids=lambda w: w.name)
+def test_staged_round_trip(torch, ck, w, where):
     g = w.geometry
     batch = make_batch(w)
     faults = make_faults(w, batch)
