@@ -39,7 +39,7 @@
 //    in an open-addressing table with order-independent atomics; a lookup
 //    walks a request's chain and probes it block by block.
 //  * Events.  Per-claim event counts (0..2) are scanned by one workgroup for
-//    batches up to 16K claims, else in three small kernels (tile sums,
+//    batches up to 4096 claims, else in three small kernels (tile sums,
 //    one-workgroup scan of the tile sums, write), so the log stays in batch
 //    order with no spin waits.
 
@@ -1137,7 +1137,9 @@ __global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids, uint
 
 // Batches of up to kSmallEvents claims: one workgroup scans the per-claim
 // event counts, appends the events and advances the log, in one launch.
-constexpr uint32_t kSmallPer = 16;
+// The claims are spread over all 1024 threads (per = ceil(C / 1024) each),
+// and a thread issues the loads of all its claims before it writes.
+constexpr uint32_t kSmallPer = 4;
 constexpr uint64_t kSmallEvents = 1024ull * kSmallPer;
 
 __global__ void __launch_bounds__(1024) k_events_small(const uint32_t* __restrict__ cnt,
@@ -1151,28 +1153,36 @@ __global__ void __launch_bounds__(1024) k_events_small(const uint32_t* __restric
     base_pos = ctr->log_count;
     base_seq = ctr->seq_next;
   }
-  const uint64_t first = (uint64_t)threadIdx.x * kSmallPer;
+  const uint32_t per = (uint32_t)((C + 1023) / 1024);  // <= kSmallPer
+  const uint64_t first = (uint64_t)threadIdx.x * per;
   uint32_t v[kSmallPer];
+  Pend pe[kSmallPer];
+  uint64_t cid[kSmallPer];
   uint32_t sum = 0;
 #pragma unroll
   for (uint32_t k = 0; k < kSmallPer; ++k) {
-    v[k] = first + k < C ? cnt[first + k] : 0;
+    const bool mine = k < per && first + k < C;
+    v[k] = mine ? cnt[first + k] : 0;
     sum += v[k];
   }
+#pragma unroll
+  for (uint32_t k = 0; k < kSmallPer; ++k)
+    if (v[k]) {
+      pe[k] = pend[first + k];
+      cid[k] = ids[first + k];
+    }
   uint32_t total;
   uint64_t pos = block_exclusive_scan_1024(sum, &total, lds);  // also orders base_* reads
+#pragma unroll
   for (uint32_t k = 0; k < kSmallPer; ++k) {
-    if (v[k] == 0) continue;
-    const uint64_t c = first + k;
-    const Pend pe = pend[c];
     for (uint32_t e = 0; e < v[k]; ++e, ++pos) {
       claim_event ev;
       ev.seq = base_seq + pos;
-      ev.claim_id = ids[c];
-      ev.aux = e == 0 ? pe.aux0 : pe.aux1;
-      ev.kind = (pe.kinds >> (8 * e)) & 0xFFu;
-      ev.block_index = pe.j;
-      ev.phys_block = pe.phys;
+      ev.claim_id = cid[k];
+      ev.aux = e == 0 ? pe[k].aux0 : pe[k].aux1;
+      ev.kind = (pe[k].kinds >> (8 * e)) & 0xFFu;
+      ev.block_index = pe[k].j;
+      ev.phys_block = pe[k].phys;
       ev.reserved = 0;
       log[base_pos + pos] = ev;
     }
