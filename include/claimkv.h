@@ -24,7 +24,10 @@
  *                  UNKNOWN) with the first failing block, appending the
  *                  ordered events;
  *   outcomes_read  copy the last check's outcomes and the new events to the
- *                  host.
+ *                  host;
+ *   claim_lookup   the reuse lookup: how many leading token blocks of each
+ *                  request hit the identities that offloads registered;
+ *   claim_identity_stats  registered and ambiguous identities.
  *
  * The digest, keys and chain are this library's definitions (the paper
  * leaves the byte-level check open; section 7 path B only requires
@@ -50,8 +53,8 @@
  *   - work is queued on the pool's stream in call order; only
  *     claim_offload (for its acceptance verdict and to settle its counts),
  *     claim_restore (to read the host fault lists), outcomes_read,
- *     claim_block_state_read, claim_timing_read and claim_pool_destroy wait
- *     for the stream;
+ *     claim_block_state_read, claim_timing_read, claim_identity_stats and
+ *     claim_pool_destroy wait for the stream;
  *   - device arrays passed in a claim_batch must stay valid and unchanged
  *     until the queued work that reads them has completed;
  *   - calls on one pool must not overlap from several host threads.
@@ -93,7 +96,7 @@ extern "C" {
 #define CLAIM_R_NOT_ACCEPTED 0x001      /* id not registered */
 #define CLAIM_R_NOT_OFFLOADED 0x002     /* registered, footprint not fully offloaded */
 #define CLAIM_R_NO_RESTORE 0x004        /* no restore ordered before this check */
-#define CLAIM_R_TOKEN_MISMATCH 0x008    /* token count or chain hash differs from acceptance */
+#define CLAIM_R_TOKEN_MISMATCH 0x008    /* token count, or a block's chain hash, differs from acceptance */
 #define CLAIM_R_FOOTPRINT_MISMATCH 0x010 /* block list differs from acceptance */
 #define CLAIM_R_MISSING_ENTRY 0x020     /* entry is CLAIM_NONE or >= num_blocks */
 #define CLAIM_R_NO_OFFLOAD_RECORD 0x040 /* block has no offload digest */
@@ -108,7 +111,7 @@ extern "C" {
 #define CLAIM_RESERVED_ID 0xFFFFFFFFFFFFFFFFull /* never a valid claim id */
 
 #define CLAIM_POOL_TIMING 0x1u       /* desc.flags: time the digest kernel of every claim_check */
-#define CLAIM_POOL_STAGE_TIMING 0x2u /* desc.flags: also time every other stage (adds ~14 us per check) */
+#define CLAIM_POOL_STAGE_TIMING 0x2u /* desc.flags: also time every other stage (adds about 20 us per check) */
 
 typedef struct claim_pool claim_pool;
 
@@ -126,7 +129,7 @@ typedef struct claim_pool_desc {
   uint32_t head_dim;
   uint32_t elem_bytes;
   uint32_t num_blocks;       /* < CLAIM_NONE */
-  uint32_t flags;            /* CLAIM_POOL_TIMING */
+  uint32_t flags;            /* CLAIM_POOL_TIMING | CLAIM_POOL_STAGE_TIMING */
   uint64_t seed;             /* cache-identity seed S */
   void* kv_base;             /* device pointer, 16-byte aligned */
   uint64_t kv_bytes;         /* >= planes * num_blocks * chunk bytes */
@@ -162,7 +165,7 @@ typedef struct claim_batch {
   const uint32_t* block_ids;     /* [num_refs] */
   const uint64_t* token_offsets; /* [num_claims + 1] */
   const uint32_t* tokens;        /* [num_tokens] */
-  const uint64_t* predicate_tokens; /* [num_claims] or NULL: see below */
+  const uint64_t* predicate_tokens; /* [num_claims] or NULL: see above */
 } claim_batch;
 
 /* Faults applied by claim_restore (host memory, read before it returns).
