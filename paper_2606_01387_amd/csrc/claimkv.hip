@@ -424,9 +424,12 @@ __global__ void __launch_bounds__(kThreads) k_mark_entries(const uint32_t* __res
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += stride) {
     const uint32_t blk = bi[i];
+    if (blk >= nb) continue;
     // most blocks are listed many times: read before writing, so that the
-    // stores (all of the same value) stay about one per block
-    if (blk < nb && !mark[blk] && valid_off[blk]) mark[blk] = 1;
+    // stores (all of the same value) stay about one per block; both flags
+    // are loaded together
+    const uint32_t seen = mark[blk], rec = valid_off[blk];
+    if (!seen && rec) mark[blk] = 1;
   }
 }
 
@@ -459,34 +462,38 @@ __device__ uint32_t block_exclusive_scan_1024(uint32_t v, uint32_t* total, uint3
 }
 
 // Ordered compaction of the marks into the unique-block list (ascending
-// block id).  One workgroup of 1024 threads, 16 marks per thread per step
-// read as one 16-byte vector (the mark array is padded to a multiple of 16
-// bytes with zeros); clears the marks it reads.
+// block id).  One workgroup of 1024 threads, 8 marks per thread per step
+// read as one 8-byte word (the mark array is padded to a multiple of 16
+// bytes with zeros); a step's indices are gathered in LDS and written out
+// with coalesced stores; clears the marks it reads.
 __global__ void __launch_bounds__(1024) k_compact(uint8_t* __restrict__ mark, uint32_t nb,
                                                   uint32_t* __restrict__ uniq,
                                                   Counters* __restrict__ ctr) {
+  constexpr uint32_t kPer = 8;
   __shared__ uint32_t lds[17];
+  __shared__ uint32_t out[1024 * kPer];
   uint32_t base = 0;
-  constexpr uint32_t kPer = 16;
   const uint64_t padded = ((uint64_t)nb + 15) / 16 * 16;
   for (uint64_t t0 = 0; t0 < padded; t0 += 1024ull * kPer) {
     const uint64_t first = t0 + (uint64_t)threadIdx.x * kPer;
     uint32_t bits = 0;
     if (first < padded) {
-      const uint4 m = *(const uint4*)(mark + first);
-      const uint32_t w[4] = {m.x, m.y, m.z, m.w};
+      const uint2 m = *(const uint2*)(mark + first);
 #pragma unroll
-      for (int k = 0; k < 16; ++k)
-        if ((w[k / 4] >> (8 * (k % 4))) & 0xFFu) bits |= 1u << k;
+      for (int k = 0; k < 8; ++k)
+        if (((k < 4 ? m.x : m.y) >> (8 * (k % 4))) & 0xFFu) bits |= 1u << k;
     }
     uint32_t total;
-    uint32_t pos = base + block_exclusive_scan_1024(__builtin_popcount(bits), &total, lds);
+    uint32_t pos = block_exclusive_scan_1024(__builtin_popcount(bits), &total, lds);
     if (bits) {
       for (uint32_t k = 0; k < kPer; ++k)
-        if (bits & (1u << k)) uniq[pos++] = (uint32_t)(first + k);
-      *(uint4*)(mark + first) = make_uint4(0u, 0u, 0u, 0u);
+        if (bits & (1u << k)) out[pos++] = (uint32_t)(first + k);
+      *(uint2*)(mark + first) = make_uint2(0u, 0u);
     }
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < total; i += 1024) uniq[base + i] = out[i];
     base += total;
+    __syncthreads();
   }
   if (threadIdx.x == 0) ctr->uniq_count = base;
 }
@@ -1265,18 +1272,25 @@ __global__ void __launch_bounds__(kThreads) k_write_events(const uint32_t* __res
   for (uint32_t w = 0; w < wave; ++w) wbase += lds[w];
   uint64_t pos = (uint64_t)tprefix[blockIdx.x] + wbase + incl - sum;
   const uint64_t base_pos = ctr->call_pos, base_seq = ctr->call_seq;
+  // every load of this thread's claims before any write
+  Pend pe[kPer];
+  uint64_t cid[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k)
+    if (v[k]) {
+      pe[k] = pend[first + k];
+      cid[k] = ids[first + k];
+    }
+#pragma unroll
   for (int k = 0; k < kPer; ++k) {
-    const uint64_t c = first + k;
-    if (v[k] == 0) continue;
-    const Pend pe = pend[c];
     for (uint32_t e = 0; e < v[k]; ++e) {
       claim_event ev;
       ev.seq = base_seq + pos;
-      ev.claim_id = ids[c];
-      ev.aux = e == 0 ? pe.aux0 : pe.aux1;
-      ev.kind = (pe.kinds >> (8 * e)) & 0xFFu;
-      ev.block_index = pe.j;
-      ev.phys_block = pe.phys;
+      ev.claim_id = cid[k];
+      ev.aux = e == 0 ? pe[k].aux0 : pe[k].aux1;
+      ev.kind = (pe[k].kinds >> (8 * e)) & 0xFFu;
+      ev.block_index = pe[k].j;
+      ev.phys_block = pe[k].phys;
       ev.reserved = 0;
       log[base_pos + pos] = ev;
       ++pos;
