@@ -298,22 +298,30 @@ __device__ __forceinline__ const IdEntry* id_find(const IdDev& t, uint64_t key) 
 }
 
 // Token multilinear of one token block, sum over its tokens of tok * t_m.
-// With kPipelined the loads of a full 16-token chunk are issued together
-// and the next chunk is in flight while the current one is summed (the
-// tail of a partial block goes token by token); without it a plain loop
-// keeps the register count low.  The check takes the first form at every
-// group width (measured faster even at lower occupancy); lookup and
-// acceptance take it for wide groups only (narrow lookups were faster at
-// full occupancy).
-template <bool kPipelined>
+// kDepth 2: the loads of a full 16-token chunk are issued together and the
+// next chunk is in flight while the current one is summed (wide groups:
+// few, long claims, where latency rules).  kDepth 1: 16-token chunks loaded
+// together, one after another (16 registers: narrow groups of the check).
+// kDepth 0: a plain loop (fewest registers: narrow lookups and
+// acceptance, where occupancy rules).  The tail of a partial block goes
+// token by token.
+template <int kDepth>
 __device__ __forceinline__ uint64_t block_multilinear(const uint32_t* __restrict__ tok,
                                                       uint64_t first, uint64_t count,
                                                       const uint64_t* tkey) {
   constexpr int kChunk = 16;
   uint64_t m_sum = 0, m = 0;
-  if constexpr (!kPipelined) {
+  if constexpr (kDepth == 0) {
     for (; m < count; ++m) m_sum += (uint64_t)tok[first + m] * tkey[m];
     return m_sum;
+  } else if constexpr (kDepth == 1) {
+    for (; m + kChunk <= count; m += kChunk) {
+      uint32_t cur[kChunk];
+#pragma unroll
+      for (int k = 0; k < kChunk; ++k) cur[k] = tok[first + m + k];
+#pragma unroll
+      for (int k = 0; k < kChunk; ++k) m_sum += (uint64_t)cur[k] * tkey[m + k];
+    }
   } else if (count >= kChunk) {
     uint32_t cur[kChunk];
 #pragma unroll
@@ -351,6 +359,11 @@ template <int W>
 __device__ __forceinline__ uint64_t chain_window(uint64_t& h, uint64_t m_sum, uint32_t gl,
                                                  uint32_t gbase, uint64_t steps) {
   if constexpr (W == 64) {  // one claim per wave: the chain runs on the scalar ALU
+    // h is the same in every lane; say so, so that it lives in SGPRs
+    // (the builtin returns int: widen through uint32_t, never by sign extension)
+    const uint32_t h_lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)h);
+    const uint32_t h_hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(h >> 32));
+    h = ((uint64_t)h_hi << 32) | h_lo;
     uint32_t lo = 0, hi = 0;
     for (uint32_t t = 0; t < steps; ++t) {
       h = splitmix_step(h ^ uniform_read64(m_sum, t));
@@ -726,7 +739,7 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
     if (j < nt) {
       const uint64_t first = j * bs;
       const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
-      m_sum = block_multilinear<(W >= 16)>(b.tok, r.to0 + first, count, tkey);
+      m_sum = block_multilinear<(W >= 16 ? 2 : 0)>(b.tok, r.to0 + first, count, tkey);
     }
     const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
     const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
@@ -933,7 +946,23 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     id_pos = nt < id_pos ? nt : id_pos;
   }
 
-  uint64_t h = seed, best_pos = kNoKey, h_best = 0, h_q = 0;
+  // Both chains start from the seed, and wherever the accepted h_{j-1}
+  // equals the presented one, hh_j = splitmix64(acc_h_{j-1} ^ M_j) is the
+  // presented h_j.  Each lane tests its position with hh_j against acc_h_j,
+  // in parallel; by induction from j = 0, the first position q where they
+  // differ is the first position where the two chains differ, the presented
+  // h_j below it are the accepted ones, and hh_q is the presented h_q.  A
+  // test past q may disagree with the serial chain's, but its key is larger
+  // than q's and it lowers no minimum, so every output is the serial one.
+  // A serial chain is walked only from p0 = min(q, id_pos) on, and only if
+  // the outcome needs an h_j there.
+  uint64_t best_pos = kNoKey;
+  uint64_t q = kNoKey, h_qv = 0;  // first identity mismatch and the presented h there
+  const uint64_t last = nt ? nt - 1 : kNoKey;
+  // accepted h at the positions the outcome may report, taken from the
+  // lanes that hold them (no loads after the loop)
+  uint64_t acc_at_best = 0, acc_at_qmin = 0, acc_at_last = 0;
+  uint64_t carry = seed;           // accepted h just before the window
   uint64_t intact = n < qmin ? n : qmin;  // first position with any problem (lane-local, then group min)
   const uint64_t L = n > nt ? n : nt;
   for (uint64_t j0 = 0; j0 < L; j0 += W) {
@@ -944,23 +973,27 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     if (j < n) blk = b.bi[(uint64_t)r.bo0 + j];
     if (found && j < common) acc_blk = reg.fp[fpo + j];
     if (j < id_pos) acc_h = reg.idn[fpo + j];
+    // the token loads go out first (they do not wait for blk)
     uint64_t m_sum = 0;
     if (j < nt) {
       const uint64_t first = j * bs;
       const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
-      m_sum = block_multilinear<true>(b.tok, r.to0 + first, count, tkey);
+      m_sum = block_multilinear<(W >= 16 ? 2 : 1)>(b.tok, r.to0 + first, count, tkey);
     }
     // per-block state, loaded unconditionally (block 0 stands in for a
-    // lane without a pool block) so that it is in flight while the chain
-    // runs; the empty asm keeps every use, and so the wait, after the chain
+    // lane without a pool block) so that it is in flight while the identity
+    // step runs; the empty asm keeps every use, and so the wait, after it
     const uint32_t sb = (j < n && blk < nb) ? blk : 0u;
     uint32_t rec = st.valid_off[sb];
     uint32_t lfb = st.load_failed[sb];
     uint64_t d_res = st.d_res[sb];
     uint64_t d_off = st.d_off[sb];
-    const uint64_t steps = j0 < nt ? (nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W) : 0;
-    const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
+    // the cache identity of block j, from the accepted h_{j-1}
+    const uint64_t up = lane_read64(acc_h, gl == 0 ? gbase : gbase + gl - 1);
+    const uint64_t hh = splitmix_step((gl == 0 ? carry : up) ^ m_sum);
+    carry = lane_read64(acc_h, gbase + W - 1);
     asm volatile("" : "+v"(rec), "+v"(lfb), "+v"(d_res), "+v"(d_off));
+    const bool mism = j < id_pos && hh != acc_h;
 
     uint64_t my_key = kNoKey;
     if (j < n) {
@@ -990,19 +1023,64 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       }
       if (my_key != kNoKey && j < intact) intact = j;
     }
-    if (j < id_pos && my_h != acc_h) {  // cache identity of block j
+    if (mism) {  // cache identity of block j
       reasons |= CLAIM_R_TOKEN_MISMATCH;
       my_key = j < my_key ? j : my_key;
       if (j < intact) intact = j;
     }
+    if (q == kNoKey) {  // windows ascend: the first window with a mismatch holds q
+      const uint64_t qk = group_min64<W>(mism ? j : kNoKey);
+      if (qk != kNoKey) {
+        q = qk;
+        h_qv = lane_read64(hh, gbase + (uint32_t)(qk - j0));
+      }
+    }
     const uint64_t rk = group_min64<W>(my_key);
     if (rk < best_pos) {
       best_pos = rk;
-      h_best = lane_read64(my_h, gbase + (uint32_t)((rk & 0xFFFFFFFFull) - j0));
+      acc_at_best = lane_read64(acc_h, gbase + (uint32_t)((rk & 0xFFFFFFFFull) - j0));
     }
-    if (qmin >= j0 && qmin < j0 + W) h_q = lane_read64(my_h, gbase + (uint32_t)(qmin - j0));
+    if (qmin >= j0 && qmin < j0 + W) acc_at_qmin = lane_read64(acc_h, gbase + (uint32_t)(qmin - j0));
+    if (last >= j0 && last < j0 + W) acc_at_last = lane_read64(acc_h, gbase + (uint32_t)(last - j0));
   }
-  if (found && acc_chain != h) {  // whole-claim identity
+
+  // the presented h at the positions the outcome reports: the winning key's
+  // (if it has tokens) and the last token block's
+  const uint64_t best_key = best_pos < special ? best_pos : special;
+  const uint64_t js = best_key == kNoKey ? kNoKey : (best_key & 0xFFFFFFFFull);
+  const bool want_js = js != kNone && js != kNoKey && js < nt;
+  const uint64_t p0 = q < id_pos ? q : id_pos;  // presented h_j = accepted h_j below p0
+  uint64_t h_js = 0, h_last = seed;
+  bool tail = false;
+  if (want_js) {
+    // js is the winning position key's, or the smallest length key's (qmin)
+    if (js < p0) h_js = best_key == best_pos ? acc_at_best : acc_at_qmin;
+    else if (js == q) h_js = h_qv;
+    else tail = true;
+  }
+  if (nt) {
+    if (last < p0) h_last = acc_at_last;
+    else if (last == q) h_last = h_qv;
+    else tail = true;
+  }
+  if (tail) {  // serial chain from p0 (uncommon: a mismatch, or positions past the accepted ones)
+    uint64_t h = p0 == 0 ? seed : reg.idn[fpo + p0 - 1];
+    for (uint64_t j0 = p0; j0 < nt; j0 += W) {
+      const uint64_t j = j0 + gl;
+      uint64_t m_sum = 0;
+      if (j < nt) {
+        const uint64_t first = j * bs;
+        const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
+        m_sum = block_multilinear<(W >= 16 ? 2 : 1)>(b.tok, r.to0 + first, count, tkey);
+      }
+      const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
+      const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
+      if (want_js && js >= j0 && js < j0 + W && js != q && js >= p0)
+        h_js = lane_read64(my_h, gbase + (uint32_t)(js - j0));
+    }
+    if (last >= p0 && last != q) h_last = h;
+  }
+  if (found && acc_chain != h_last) {  // whole-claim identity
     reasons |= CLAIM_R_TOKEN_MISMATCH;
     special = kClaimLevelKey < special ? kClaimLevelKey : special;
   }
@@ -1018,7 +1096,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   o.intact_blocks = (uint32_t)intact;
   o.expected_digest = 0;
   o.observed_digest = 0;
-  o.chain_hash = h;
+  o.chain_hash = h_last;
   o.chain_hash_at_fail = 0;
   Pend pe;
   pe.pad = 0;
@@ -1028,7 +1106,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     o.first_failing_block = kNone;
     o.phys_block = kNone;
     pe.kinds = CLAIM_EV_RESTORED;
-    pe.aux0 = h;
+    pe.aux0 = h_last;
     cnt[c] = 1;
   } else {
     const uint32_t cls = (uint32_t)(best >> 32);
@@ -1040,8 +1118,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       o.expected_digest = st.d_off[o.phys_block];
       o.observed_digest = st.d_res[o.phys_block];
     }
-    if (js != kNone && (uint64_t)js < nt)
-      o.chain_hash_at_fail = best == best_pos ? h_best : h_q;
+    if (js != kNone && (uint64_t)js < nt) o.chain_hash_at_fail = h_js;
     if (cls == 1) {
       pe.kinds = CLAIM_EV_RESTORATION_FAILED | (CLAIM_EV_ACTIVE_REQUEST_REFUSED << 8);
       pe.aux0 = o.observed_digest;
@@ -1090,7 +1167,7 @@ __global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids, uint
     if (j < nt) {
       const uint64_t first = j * bs;
       const uint64_t count = ntok - first < bs ? ntok - first : bs;
-      m_sum = block_multilinear<(W >= 16)>(b.tok, to0 + first, count, tkey);
+      m_sum = block_multilinear<(W >= 16 ? 2 : 0)>(b.tok, to0 + first, count, tkey);
     }
     const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
     const uint64_t h_before = h;
