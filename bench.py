@@ -85,7 +85,19 @@ def cpu_baseline(w, batch, faults, sample_blocks: int):
                    f"{batch.num_claims} claims timed in {t_claims:.2f} s"),
         "claims_per_s": round(batch.num_claims / t_check, 2),
         "host_cpus": os.cpu_count(),
+        "host_cpu_model": _cpu_model(),
     }, out
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main() -> int:

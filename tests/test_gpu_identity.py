@@ -12,8 +12,8 @@ import numpy as np
 import pytest
 
 from oracle import oracle as O
-from paper_2606_01387_amd.synth import (FULL, TINY, Geometry, Workload, from_claims, make_batch,
-                                        make_faults, make_requests, scaled)
+from paper_2606_01387_amd.synth import (FULL, TINY, FaultSpec, Geometry, Workload, from_claims,
+                                        make_batch, make_faults, make_requests, scaled)
 from tests.helpers import apply_flips, digests
 from tests.test_gpu_parity import (LONG_CLAIMS, MAX_BS_LONG, MAX_BS_SHORT, MIN_BS, capacities,
                                    free_gpu, gpu_pool_tensor, note, same_events, same_outcomes)
@@ -194,5 +194,130 @@ def test_identity_check_parity(torch, ck, w):
     positioned = tm & (out["first_failing_block"] != ck.NONE)
     note(f"  token mismatch in {int(tm.sum())} claims, {int(positioned.sum())} at a block position")
     assert positioned.any()
+    del kv
+    free_gpu(torch)
+
+
+def _positioned_cases(W: int, bs: int, rng):
+    """Claims of 2W + W/2 + 3 blocks (several windows of a W-wide group)
+    whose presented tokens differ from the accepted ones at chosen block
+    positions: window edges, the last block, two places, cuts, extensions,
+    an accepted claim shorter than its rows, and digest faults, reported
+    failures or missing entries before or after the first identity
+    mismatch.  Returns (accepted parts, presented parts, flips (position),
+    load failures (position)) per claim, plus filler claims that bring the
+    mean row length to W."""
+    n = 2 * W + W // 2 + 3
+    r = 5  # the accepted claims end 5 tokens short of their last block
+
+    def toks(k):
+        return rng.integers(1, 32000, size=k, dtype=np.uint32)
+
+    def chg(t, blocks):
+        t = t.copy()
+        for j in blocks:
+            m = j * bs + int(rng.integers(0, bs if (j + 1) * bs <= t.size else t.size - j * bs))
+            t[m] = (int(t[m]) + 1 + int(rng.integers(0, 31998))) % 32000
+        return t
+
+    specs = [  # (name, presented(t), flip positions, load-failed positions, missing positions, accepted cut)
+        ("same", lambda t: t, [], [], [], None),
+        ("chg@0", lambda t: chg(t, [0]), [], [], [], None),
+        ("chg@W-1", lambda t: chg(t, [W - 1]), [], [], [], None),
+        ("chg@W", lambda t: chg(t, [W]), [], [], [], None),
+        ("chg@last", lambda t: chg(t, [n - 1]), [], [], [], None),
+        ("chg@2,n-2", lambda t: chg(t, [2, n - 2]), [], [], [], None),
+        ("cut@W", lambda t: t[: W * bs], [], [], [], None),
+        ("cut@W+7tok", lambda t: t[: W * bs + 7], [], [], [], None),
+        ("cut@0", lambda t: t[:0], [], [], [], None),
+        ("ext+3", lambda t: np.concatenate([t, toks(3)]), [], [], [], None),
+        ("ext+bs+5", lambda t: np.concatenate([t, toks(bs + 5)]), [], [], [], None),
+        ("acc-short", lambda t: t, [], [], [], (W + 1) * bs),
+        ("flip@1,chg@W+1", lambda t: chg(t, [W + 1]), [1], [], [], None),
+        ("flip@n-3", lambda t: t, [n - 3], [], [], None),
+        ("acc-short,flip@W+2", lambda t: t, [W + 2], [], [], W * bs),
+        ("lf@1,ext", lambda t: np.concatenate([t, toks(2 * bs)]), [], [1], [], None),
+        ("miss@1,chg@W+2", lambda t: chg(t, [W + 2]), [], [], [1], None),
+        ("chg@W+3,flip@W+5", lambda t: chg(t, [W + 3]), [W + 5], [], [], None),
+    ]
+    cases = []
+    for name, pres, flips, lfs, miss, acc_cut in specs:
+        full = toks(n * bs - r)
+        acc = full if acc_cut is None else full[:acc_cut]
+        cases.append((name, n, acc, pres(full), flips, lfs, miss))
+    # fillers: 1-block claims that bring the mean row length into (W/2, W]
+    refs = len(cases) * n
+    k = 0
+    while -(-(refs + k) // (len(cases) + k)) > W:
+        k += 1
+    fill = [toks(bs - 3) for _ in range(k)]
+    return cases, fill
+
+
+@pytest.mark.parametrize("W", [4, 16, 64])
+def test_identity_positions(torch, ck, W):
+    """Per-position identity at chosen positions, against the oracle: the
+    parallel compare's first mismatch, the values it takes from the
+    accepted chain below it, and the serial chain from the first mismatch
+    (or from the end of a shorter accepted claim) on."""
+    g = Geometry(1, 1, 16, 1, 8, 2, 4096)  # 256-byte blocks
+    bs = g.block_size
+    w = Workload(name=f"identity-positions-w{W}", geometry=g, seed=77 + W, num_claims=1,
+                 length=("blocks", 1, 1, False), sharing=("fraction", 0.0), corrupt_rate=0.0,
+                 content_seed=5 + W)
+    rng = np.random.default_rng(400 + W)
+    cases, fill = _positioned_cases(W, bs, rng)
+    acc_parts, pres_parts, flips, lfs = [], [], [], []
+    nxt = 0
+    for i, (name, n, acc, pres, fl, lf, miss) in enumerate(cases):
+        blks = np.arange(nxt, nxt + n, dtype=np.uint32)
+        nxt += n
+        pblks = blks.copy()
+        pblks[miss] = 0xFFFFFFFF
+        acc_parts.append((1000 + i, blks, acc))
+        pres_parts.append((1000 + i, pblks, pres))
+        flips += [(int(blks[j]), int(rng.integers(0, 8 * g.block_bytes))) for j in fl]
+        lfs += [int(blks[j]) for j in lf]
+    for i, t in enumerate(fill):
+        part = (5000 + i, np.array([nxt], np.uint32), t)
+        nxt += 1
+        acc_parts.append(part)
+        pres_parts.append(part)
+    assert nxt <= g.num_blocks
+    accepted, presented = from_claims(acc_parts), from_claims(pres_parts)
+    mean = -(-presented.num_refs // presented.num_claims)
+    assert W // 2 < mean <= W or (W == 4 and mean <= 4)
+    faults = FaultSpec(np.array([f[0] for f in flips], np.uint32),
+                       np.array([f[1] for f in flips], np.uint64), np.array(lfs, np.uint32))
+    note(f"identity positions W={W}: {len(cases)} positioned claims of {cases[0][1]} blocks, "
+         f"{len(fill)} fillers")
+    kv = gpu_pool_tensor(torch, w)
+    with ck.Pool(g, w.seed, kv, **capacities(accepted)) as pool:
+        pool.offload(ck.DeviceBatch(accepted))
+        pool.restore(ck.DeviceBatch(accepted), faults=faults)
+        pool.read(max_outcomes=1)
+        pool.check(ck.DeviceBatch(presented))
+        out, ev = pool.read()
+    host = __import__("paper_2606_01387_amd.synth", fromlist=["content"]).content.pool_host(
+        g, w.content_seed)
+    op = O.OraclePool(g.num_blocks, bs, w.seed)
+    assert op.offload(accepted, digests(host, w)) == O.OK
+    assert op.restore(accepted, faults.load_failed) == O.OK
+    op.events(clear=True)
+    want = op.check(presented, digests(apply_flips(host, w, faults), w))
+    for i, case in enumerate(cases):
+        note(f"  {case[0]}: code {int(want['code'][i])} block {int(want['first_failing_block'][i])} "
+             f"reasons {int(want['reasons'][i]):#x}")
+    same_outcomes(out, want)
+    same_events(ev, op.events())
+    # the cases reach what they are for: a mismatch at the changed block
+    names = [c[0] for c in cases]
+    ffb = out["first_failing_block"]
+    assert ffb[names.index("chg@0")] == 0
+    assert ffb[names.index("chg@W")] == W
+    assert ffb[names.index("chg@last")] == cases[0][1] - 1
+    assert ffb[names.index("flip@1,chg@W+1")] == W + 1
+    assert ffb[names.index("miss@1,chg@W+2")] == 1
+    assert out["code"][names.index("same")] == ck.MATERIALIZED
     del kv
     free_gpu(torch)
