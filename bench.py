@@ -44,11 +44,19 @@ def digest_traffic(workload: str):
     return int(data["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(w, batch, faults, sample_blocks: int):
-    """The oracle as it stands, single-threaded, on a bounded sample: the
-    digest of `sample_blocks` distinct unique blocks (content generated
-    untimed) gives the per-byte rate; the claim stage (chain, compare,
-    min-reduction, events) runs on the whole batch with modeled digests."""
+def cpu_baseline(w, batch, faults, sample_gb: float):
+    """The oracle as it stands, single-threaded, on a bounded sample of the
+    workload: the unique blocks are taken in order up to `sample_gb` of block
+    bytes (all of them when they fit), their content is generated untimed on
+    all host threads and their restored bytes (the flips applied) are
+    digested by the oracle, timed; the per-byte rate is extrapolated to the
+    whole unique set.  The claim stage (chain, compare, min-reduction,
+    events) runs on the whole batch, timed.  Digests of blocks outside the
+    sample are modeled (equal before and after, real for changed blocks).
+    Returns the baseline record, the oracle's outcomes and events, its
+    per-block digests and the blocks whose digests are real."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import numpy as np
 
     from oracle import oracle as O
@@ -57,13 +65,31 @@ def cpu_baseline(w, batch, faults, sample_blocks: int):
 
     g = w.geometry
     uniq = batch.unique_blocks(g.num_blocks)
-    blocks = uniq[:sample_blocks]
-    canon = [content.block_canonical(g, w.content_seed, int(b)) for b in blocks]
-    t0 = time.perf_counter()
-    for c in canon:
-        O.block_digest(c, w.seed)
-    t_digest = time.perf_counter() - t0
+    n_sample = int(min(uniq.size, max(1, sample_gb * 1e9 // g.block_bytes)))
+    blocks = uniq[:n_sample]
+    changed = set(int(b) for b in faults.changed_blocks())
+    flips = {}
+    for b, bit in zip(faults.flip_blocks, faults.flip_bits):
+        flips.setdefault(int(b), []).append(int(bit))
     d0, d1 = modeled_digests(w, faults, blocks_needed=[])
+    threads = max(1, min(16, os.cpu_count() or 1))
+    t_digest = 0.0
+    t_gen = time.perf_counter()
+    with ThreadPoolExecutor(threads) as ex:
+        for lo in range(0, n_sample, 256):
+            part = [int(b) for b in blocks[lo:lo + 256]]
+            canon = list(ex.map(lambda b: content.block_canonical(g, w.content_seed, b), part))
+            for b, c in zip(part, canon):
+                for bit in flips.get(b, []):  # restored bytes
+                    c[bit // 8] ^= np.uint8(1 << (bit % 8))
+            t0 = time.perf_counter()
+            for b, c in zip(part, canon):
+                d1[b] = O.block_digest(c, w.seed)
+            t_digest += time.perf_counter() - t0
+            for b in part:  # a changed block's d0 is already its real pre-flip digest
+                if b not in changed:
+                    d0[b] = d1[b]
+    t_gen = time.perf_counter() - t_gen - t_digest
     op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
     op.offload(batch, d0)
     op.restore(batch, faults.load_failed)
@@ -71,22 +97,29 @@ def cpu_baseline(w, batch, faults, sample_blocks: int):
     t0 = time.perf_counter()
     out = op.check(batch, d1)
     t_claims = time.perf_counter() - t0
-    per_byte = t_digest / (len(blocks) * g.block_bytes)
+    ev = op.events()
+    per_byte = t_digest / (n_sample * g.block_bytes)
     t_check = per_byte * uniq.size * g.block_bytes + t_claims
     gbps = uniq.size * g.block_bytes / t_check / 1e9
+    whole = n_sample == uniq.size
+    real = np.union1d(blocks, np.array(sorted(changed | set(int(b) for b in faults.load_failed)),
+                                       dtype=np.int64)).astype(np.int64)
+    sample = (f"single-threaded oracle: digest of the restored bytes of "
+              f"{'all ' if whole else ''}{n_sample} of {uniq.size} unique blocks "
+              f"({n_sample * g.block_bytes / 1e9:.2f} GB) timed in {t_digest:.2f} s"
+              + ("" if whole else " and extrapolated per byte to the whole unique set")
+              + f"; claim stage on all {batch.num_claims} claims timed in {t_claims:.3f} s; "
+              f"content generated untimed on {threads} host threads in {t_gen:.1f} s")
     return {
         "value": round(gbps, 4),
         "unit": "GB/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": (f"single-threaded oracle: digest of {len(blocks)} of {uniq.size} unique blocks "
-                   f"({len(blocks) * g.block_bytes / 1e9:.2f} GB) timed in {t_digest:.2f} s and "
-                   f"extrapolated per byte to all {uniq.size}; claim stage on all "
-                   f"{batch.num_claims} claims timed in {t_claims:.2f} s"),
+        "sample": sample,
         "claims_per_s": round(batch.num_claims / t_check, 2),
         "host_cpus": os.cpu_count(),
         "host_cpu_model": _cpu_model(),
-    }, out
+    }, out, ev, d0, d1, real
 
 
 def _cpu_model() -> str:
@@ -106,7 +139,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3-8b")
-    ap.add_argument("--cpu-sample-blocks", type=int, default=512)
+    ap.add_argument("--cpu-sample-gb", type=float, default=20.0,
+                    help="block bytes the oracle digests for the CPU baseline (whole unique set "
+                         "if it is smaller)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--round-trip", action="store_true",
                     help="offload through pinned host staging, drop the device copy, restore from "
@@ -239,6 +274,7 @@ def main() -> int:
     t1 = time.perf_counter()
     stages = pool.timing()
     out, ev = pool.read()
+    state = pool.block_state()
 
     # spread of single checks, in a separate pass after the timed region:
     # hipEvents on the pool stream around each check
@@ -335,11 +371,21 @@ def main() -> int:
     if round_trip is not None:
         line["round_trip"] = round_trip
     if not args.no_cpu_baseline:
-        base, want = cpu_baseline(w, batch, faults, args.cpu_sample_blocks)
+        base, want, want_ev, d0, d1, real = cpu_baseline(w, batch, faults, args.cpu_sample_gb)
         line["cpu_baseline"] = base
-        line["verified_against_oracle"] = bool(np.array_equal(out["code"], want["code"]) and
-                                               np.array_equal(out["first_failing_block"],
-                                                              want["first_failing_block"]))
+        # the last timed check against the oracle: every outcome field, that
+        # check's events, and the digests of every block the oracle digested
+        same_out = all(np.array_equal(out[f], want[f]) for f in want.dtype.names)
+        k = len(want_ev)
+        last = ev[len(ev) - k:]
+        same_ev = len(ev) == k * (steps + warm) and all(
+            np.array_equal(last[f], want_ev[f])
+            for f in ("claim_id", "aux", "kind", "block_index", "phys_block"))
+        same_d = bool(np.array_equal(state["d_off"][real], d0[real]) and
+                      np.array_equal(state["d_res"][real], d1[real]))
+        line["verified_against_oracle"] = bool(same_out and same_ev and same_d)
+        line["oracle_comparison"] = {"outcome_fields": bool(same_out), "events": bool(same_ev),
+                                     "block_digests": same_d, "blocks_with_real_digests": int(real.size)}
     print(json.dumps(line), flush=True)
     return 0
 

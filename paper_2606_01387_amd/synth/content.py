@@ -30,7 +30,7 @@ HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-shared", "-std=c++17",
 def build() -> None:
     """Compile the host generator (gcc) and the GPU fill (hipcc, gfx950)."""
     tmp = HOST_LIB + ".tmp"
-    subprocess.run(["gcc", "-O2", "-std=c99", "-shared", "-fPIC", HOST_SRC, "-o", tmp], check=True)
+    subprocess.run(["gcc", "-O3", "-std=c99", "-shared", "-fPIC", HOST_SRC, "-o", tmp], check=True)
     os.replace(tmp, HOST_LIB)
     tmp = FILL_LIB + ".tmp"
     subprocess.run([HIPCC, *HIP_FLAGS, FILL_SRC, "-o", tmp], check=True)
