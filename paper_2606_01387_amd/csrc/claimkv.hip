@@ -29,8 +29,10 @@
 //  * Claims.  A group of W lanes (W = 2..64, from the batch's mean claim
 //    length) owns one claim: lanes take block positions j = j0 + lane.  A
 //    window first issues every load that depends only on j (block id,
-//    accepted block and identity, the block's tokens), then the per-block
-//    state, which stays in flight while the serial chain
+//    accepted block and identity, the block's tokens), then the block's
+//    status byte (offload record, reported failure, digest mismatch, all
+//    three decided when the check combines the block's digest), which
+//    stays in flight while the serial chain
 //    h_j = splitmix64(h_{j-1} ^ M_j) walks the window (on the scalar unit
 //    when W = 64); the checks (footprint, identity, missing entry, offload
 //    record, reported failure, digest mismatch, predicate) follow.  The
@@ -645,18 +647,28 @@ __global__ void __launch_bounds__(kThreads) k_digest(const u32x2* __restrict__ p
   }
 }
 
+// Per-block status byte of a check (bstat): the three facts the claim stage
+// needs about a block, so that it loads one byte per block position.
+constexpr uint32_t kBsRecord = 1, kBsLoadFailed = 2, kBsMismatch = 4;
+
 // Add each unique block's piece-group partials.  One wave per block, lanes
 // over piece groups.
 //   mode 0 (offload): d_off, valid_off = 1, load_failed = 0, slot_of
-//   mode 1 (check):   d_res
+//   mode 1 (check):   d_res, and bstat = record | reported failure |
+//                     (d_res != d_off); every block a check's claims can
+//                     find with an offload record is one of its unique
+//                     blocks, so the claim stage reads bstat only for
+//                     blocks written here (others keep 0 = no record)
 __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restrict__ uniq,
                                                        const Counters* __restrict__ ctr,
                                                        const uint64_t* __restrict__ partial,
                                                        uint32_t pgs, uint32_t groups, int mode,
                                                        int staged, uint64_t* __restrict__ d_out,
+                                                       const uint64_t* __restrict__ d_off,
                                                        uint8_t* __restrict__ valid_off,
                                                        uint8_t* __restrict__ load_failed,
-                                                       uint32_t* __restrict__ slot_of) {
+                                                       uint32_t* __restrict__ slot_of,
+                                                       uint8_t* __restrict__ bstat) {
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t U = ctr->uniq_count;
   const uint32_t NW = (U + groups - 1) / groups;
@@ -674,6 +686,9 @@ __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restric
         valid_off[b] = 1;
         load_failed[b] = 0;
         slot_of[b] = staged ? u : kNone;
+      } else {
+        bstat[b] = (uint8_t)(kBsRecord | (load_failed[b] ? kBsLoadFailed : 0u) |
+                             (sum != d_off[b] ? kBsMismatch : 0u));
       }
     }
   }
@@ -860,8 +875,7 @@ __global__ void __launch_bounds__(kThreads) k_restore_claims(BatchDev b, RegDev 
 struct CheckState {
   const uint64_t* d_off;
   const uint64_t* d_res;
-  const uint8_t* valid_off;
-  const uint8_t* load_failed;
+  const uint8_t* bstat;
 };
 
 template <int W>
@@ -984,15 +998,12 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     // lane without a pool block) so that it is in flight while the identity
     // step runs; the empty asm keeps every use, and so the wait, after it
     const uint32_t sb = (j < n && blk < nb) ? blk : 0u;
-    uint32_t rec = st.valid_off[sb];
-    uint32_t lfb = st.load_failed[sb];
-    uint64_t d_res = st.d_res[sb];
-    uint64_t d_off = st.d_off[sb];
+    uint32_t bst = st.bstat[sb];
     // the cache identity of block j, from the accepted h_{j-1}
     const uint64_t up = lane_read64(acc_h, gl == 0 ? gbase : gbase + gl - 1);
     const uint64_t hh = splitmix_step((gl == 0 ? carry : up) ^ m_sum);
     carry = lane_read64(acc_h, gbase + W - 1);
-    asm volatile("" : "+v"(rec), "+v"(lfb), "+v"(d_res), "+v"(d_off));
+    asm volatile("" : "+v"(bst));
     const bool mism = j < id_pos && hh != acc_h;
 
     uint64_t my_key = kNoKey;
@@ -1004,12 +1015,12 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       if (blk >= nb) {
         reasons |= CLAIM_R_MISSING_ENTRY;
         my_key = j < my_key ? j : my_key;
-      } else if (!rec) {
+      } else if (!(bst & kBsRecord)) {
         reasons |= CLAIM_R_NO_OFFLOAD_RECORD;
         my_key = j < my_key ? j : my_key;
       } else {
-        const bool lf = lfb != 0;
-        const bool mm = d_res != d_off;
+        const bool lf = (bst & kBsLoadFailed) != 0;
+        const bool mm = (bst & kBsMismatch) != 0;
         if ((lf || mm) && j < intact) intact = j;
         if (j >= pred) {
           // past the predicate: the claimed prefix is still intact
@@ -1397,6 +1408,7 @@ struct claim_pool {
 
   uint64_t *d_off = nullptr, *d_res = nullptr, *partial = nullptr;
   uint8_t *valid_off = nullptr, *load_failed = nullptr, *mark = nullptr;
+  uint8_t* bstat = nullptr;  // per-block status of the last check (kBs* bits)
   uint32_t *uniq = nullptr, *slot_of = nullptr;
 
   uint64_t reg_mask = 0, max_claims = 0;
@@ -1657,7 +1669,8 @@ int launch_finalize(claim_pool* P, int mode, int staged) {
   const uint32_t grid = P->nb / 4 + 1 < 8192 ? P->nb / 4 + 1 : 8192;
   hipLaunchKernelGGL(k_finalize, dim3(grid), dim3(kThreads), 0, P->stream, P->uniq, P->ctr,
                      P->partial, P->pgs, P->groups, mode, staged,
-                     mode == 0 ? P->d_off : P->d_res, P->valid_off, P->load_failed, P->slot_of);
+                     mode == 0 ? P->d_off : P->d_res, P->d_off, P->valid_off, P->load_failed,
+                     P->slot_of, P->bstat);
   return hip_status(hipGetLastError());
 }
 
@@ -1752,7 +1765,7 @@ int choose_digest_shape(claim_pool* P) {
 
 void free_pool(claim_pool* P) {
   if (!P) return;
-  void* ptrs[] = {P->d_off,    P->d_res,    P->partial, P->valid_off, P->load_failed,
+  void* ptrs[] = {P->d_off,    P->d_res,    P->partial, P->valid_off, P->load_failed, P->bstat,
                   P->mark,     P->uniq,     P->slot_of, P->reg,       P->fp_store,
                   P->log,      P->ctr,      P->outcomes, P->cnt,      P->pend,
                   P->tsum,     P->dup_table, P->f_blocks, P->f_bits,   P->idn_store,
@@ -1860,7 +1873,8 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     if ((rc = dalloc(&P->d_off, nb)) || (rc = dalloc(&P->d_res, nb)) ||
         (rc = dalloc(&P->partial, (uint64_t)P->pgs * (nb + P->groups))) ||
         (rc = dalloc(&P->valid_off, nb)) ||
-        (rc = dalloc(&P->load_failed, nb)) || (rc = dalloc(&P->mark, (nb + 15) / 16 * 16)) ||
+        (rc = dalloc(&P->load_failed, nb)) || (rc = dalloc(&P->bstat, nb)) ||
+        (rc = dalloc(&P->mark, (nb + 15) / 16 * 16)) ||
         (rc = dalloc(&P->uniq, nb)) || (rc = dalloc(&P->slot_of, nb)))
       break;
     P->max_claims = d->max_claims;
@@ -1891,6 +1905,7 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     }
     if ((rc = fill<uint64_t>(P, P->d_off, nb, 0)) || (rc = fill<uint64_t>(P, P->d_res, nb, 0)) ||
         (rc = fill<uint8_t>(P, P->valid_off, nb, 0)) || (rc = fill<uint8_t>(P, P->load_failed, nb, 0)) ||
+        (rc = fill<uint8_t>(P, P->bstat, nb, 0)) ||
         (rc = fill<uint8_t>(P, P->mark, (nb + 15) / 16 * 16, 0)) || (rc = fill<uint32_t>(P, P->slot_of, nb, kNone)) ||
         (rc = fill<uint64_t>(P, (uint64_t*)P->reg, cap * (sizeof(RegEntry) / 8), 0)) ||
         (rc = fill_strided_u64(P, (uint64_t*)P->reg, cap, sizeof(RegEntry) / 8, kEmptyId)))
@@ -2063,8 +2078,7 @@ int claim_check(claim_pool* P, const claim_batch* b) {
     CheckState st;
     st.d_off = P->d_off;
     st.d_res = P->d_res;
-    st.valid_off = P->valid_off;
-    st.load_failed = P->load_failed;
+    st.bstat = P->bstat;
     LAUNCH_GROUPED(k_check, P, b, batch_dev(b), reg_dev(P), st, P->nb, P->bs, P->seed, P->outcomes,
                    P->cnt, P->pend);
   }
