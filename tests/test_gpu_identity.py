@@ -321,3 +321,46 @@ def test_identity_positions(torch, ck, W):
     assert out["code"][names.index("same")] == ck.MATERIALIZED
     del kv
     free_gpu(torch)
+
+
+def test_chain_reproduces_published_outputs_on_gpu(torch, ck):
+    """The library's chain against values published outside this project:
+    on a pool with seed 0 and 16-token blocks, the token blocks of
+    tests/golden/chain_splitmix_tokens.txt chain to the four published
+    SplitMix64 outputs for seed 0.  Checked in acceptance (ACCEPTED carries
+    the chain hash), in the check (outcome chain hash, per-position identity)
+    and in the lookup (chain hash at the hit, for every prefix length)."""
+    from tests.test_oracle_hash import GOLD, chain_fixture
+
+    note("chain against published SplitMix64 outputs")
+    toks = chain_fixture()
+    g = Geometry(1, 2, 16, 1, 8, 2, 16)
+    kv = torch.zeros(g.pool_bytes, dtype=torch.uint8, device="cuda")
+    blocks = [3, 5, 7, 9]
+    claim = from_claims([(0x5EED, blocks, toks)])
+    changed = toks.copy()
+    changed[40] += 1  # a token of block 2
+    reqs = from_claims([(0x100 + k, [], toks[: 16 * k]) for k in range(1, 5)])
+    with ck.Pool(g, 0, kv, max_claims=64, max_footprint=256, event_capacity=256) as pool:
+        db = ck.DeviceBatch(claim)
+        pool.offload(db)
+        _, ev_acc = pool.read(max_outcomes=1)
+        pool.restore(db)
+        pool.check(db)
+        out, _ = pool.read()
+        lk = pool.lookup(ck.DeviceBatch(reqs))
+        pool.check(ck.DeviceBatch(from_claims([(0x5EED, blocks, changed)])))
+        out_changed, _ = pool.read()
+    acc = ev_acc[ev_acc["kind"] == ck.EV_ACCEPTED]
+    assert acc["aux"].tolist() == [GOLD[3]]
+    assert out["code"].tolist() == [ck.MATERIALIZED]
+    assert int(out[0]["chain_hash"]) == GOLD[3]
+    assert lk["hit_blocks"].tolist() == [1, 2, 3, 4]
+    assert lk["last_block"].tolist() == blocks
+    assert lk["chain_hash_at_hit"].tolist() == GOLD
+    # identities h_0, h_1 still match; block 2 is the first that differs
+    assert out_changed["code"].tolist() == [ck.UNKNOWN]
+    assert int(out_changed[0]["first_failing_block"]) == 2
+    assert int(out_changed[0]["reasons"]) & ck.R_TOKEN_MISMATCH
+    del kv
+    free_gpu(torch)

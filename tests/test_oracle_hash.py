@@ -181,6 +181,30 @@ def test_chain_first_step_on_zero_tokens_is_published_output():
     assert O.chain_hash(np.zeros(0, np.uint32), 16, 12345) == 12345
 
 
+def chain_fixture():
+    """Token blocks (block size 16, pool seed 0) whose chain is the published
+    SplitMix64 stream (tests/golden/make_chain_tokens.py)."""
+    return np.array([int(t) for row in golden_lines("chain_splitmix_tokens.txt") for t in row],
+                    np.uint32)
+
+
+def test_chain_reproduces_published_outputs():
+    # block 0 is zero tokens and block j has M_j = out_{j-1} xor j*gamma, so
+    # h_j = splitmix64(h_{j-1} xor M_j) = mix64((j+1) gamma) = out_j: the
+    # whole chain (xor with the previous hash, added gamma, block index of
+    # M_j, start value S = 0) against the four published outputs
+    toks = chain_fixture()
+    assert toks.size == 4 * 16
+    assert [int(h) for h in O.chain(toks, 16, 0)] == GOLD
+    for k in range(1, 5):
+        assert O.chain_hash(toks[: 16 * k], 16, 0) == GOLD[k - 1]
+    # the same tokens in another block order, or under another seed, leave
+    # the stream
+    swapped = np.concatenate([toks[:16], toks[32:48], toks[16:32], toks[48:]])
+    assert [int(h) for h in O.chain(swapped, 16, 0)][1:] != GOLD[1:]
+    assert [int(h) for h in O.chain(toks, 16, 1)] != GOLD
+
+
 def test_chain_is_prefix_closed_and_shared_prefixes_collide():
     rng = np.random.default_rng(7)
     bs, seed = 16, 1002
