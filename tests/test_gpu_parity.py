@@ -530,3 +530,30 @@ def test_full_size_parity(torch, ck, name):
         assert (out["intact_blocks"] <= out["num_blocks"]).all()
     del kv, db
     free_gpu(torch)
+
+
+def test_digest_of_unit_words_is_published_key(torch, ck):
+    """The library's digest against published values: with pool seed 0, a
+    block whose only non-zero canonical word is w_i = 1 digests to
+    k_i = splitmix64(0, i) | 1, the i-th published SplitMix64 output with
+    its low bit set; w_i = 2^b gives 2^b k_i.  Blocks 0..3 carry the unit
+    word at canonical index 0..3 (plane 0); block 4 carries 2^63 at index 1."""
+    from tests.test_oracle_hash import GOLD
+
+    note("digest of unit words against published outputs")
+    g = Geometry(1, 2, 16, 1, 8, 2, 8)  # 256-byte chunks, 2 planes
+    kv = torch.zeros(g.pool_bytes, dtype=torch.uint8, device="cuda")
+    words = kv.view(torch.int64)
+    chunk_words = g.chunk_bytes // 8
+    for b in range(4):  # plane 0, block b, word b of its chunk
+        words[b * chunk_words + b] = 1
+    words[4 * chunk_words + 1] = -(1 << 63)  # bit 63 of word 1 of block 4
+    claim = from_claims([(0xD1, [0, 1, 2, 3, 4], np.arange(5 * 16, dtype=np.uint32))])
+    with ck.Pool(g, 0, kv, max_claims=16, max_footprint=64, event_capacity=64) as pool:
+        pool.offload(ck.DeviceBatch(claim))
+        st = pool.block_state()
+    assert [int(x) for x in st["d_off"][:4]] == [x | 1 for x in GOLD]
+    assert int(st["d_off"][4]) == ((GOLD[1] | 1) << 63) & ((1 << 64) - 1)
+    assert int(st["d_off"][5]) == 0 and not st["valid_off"][5]
+    del kv
+    free_gpu(torch)
