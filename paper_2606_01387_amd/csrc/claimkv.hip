@@ -142,6 +142,45 @@ __device__ __forceinline__ uint64_t group_min64(uint64_t v) {
   return v;
 }
 
+// Mask of the calling lane's group (W lanes) whose predicate holds: bit i
+// is group lane i.  One ballot instead of a shuffle reduction.
+template <int W>
+__device__ __forceinline__ uint64_t group_ballot(bool pred) {
+  const uint64_t m = __ballot(pred);
+  if constexpr (W == 64) {
+    return m;
+  } else {
+    const uint32_t gbase = (threadIdx.x & 63) & ~(uint32_t)(W - 1);
+    return (m >> gbase) & ((1ull << W) - 1);
+  }
+}
+
+// First group lane whose predicate holds, W if none.
+template <int W>
+__device__ __forceinline__ uint32_t group_first(bool pred) {
+  const uint64_t m = group_ballot<W>(pred);
+  return m ? (uint32_t)__builtin_ctzll(m) : (uint32_t)W;
+}
+
+// Value of group lane i.  With one group per wave i is wave-uniform and a
+// readlane serves; narrower groups read through the LDS crossbar.
+template <int W>
+__device__ __forceinline__ uint64_t group_read64(uint64_t v, uint32_t gbase, uint32_t i) {
+  if constexpr (W == 64) {
+    return uniform_read64(v, i);
+  } else {
+    return lane_read64(v, gbase + i);
+  }
+}
+
+// The previous lane's value (lane 0 gets 0): a DPP shift of the whole wave
+// by one lane, which callers override at the first lane of each group.
+__device__ __forceinline__ uint64_t prev_lane64(uint64_t v) {
+  const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)v, 0x138, 0xf, 0xf, false);
+  const uint32_t hi = __builtin_amdgcn_update_dpp(0u, (uint32_t)(v >> 32), 0x138, 0xf, 0xf, false);
+  return ((uint64_t)hi << 32) | lo;
+}
+
 template <int W>
 __device__ __forceinline__ uint32_t group_or(uint32_t v) {
   const uint32_t lane = threadIdx.x & 63;
@@ -193,9 +232,19 @@ struct IdEntry {
   uint32_t flags;  // kIdUsed | kIdAmbiguous
 };
 
+// Where the first claim that registered an identity keeps its accepted
+// identities: the identity store index of the identity itself, and one past
+// that claim's last accepted identity.  A lookup that reaches the identity
+// follows that claim's identities to confirm many positions at once.
+struct IdSrc {
+  uint64_t at;
+  uint64_t end;
+};
+
 struct IdDev {
   uint64_t mask;
   IdEntry* e;  // mask + 2 entries
+  IdSrc* src;  // mask + 2 entries, parallel to e
 };
 
 struct Pend {  // events a claim will append (0..2), written before the scan
@@ -273,15 +322,22 @@ __device__ IdEntry* id_claim_slot(const IdDev& t, uint64_t key) {
 
 // Register (key -> block).  Order-independent: the first registration sets
 // the block, any later one with another block marks the identity ambiguous.
-__device__ void id_register(const IdDev& t, uint64_t key, uint32_t block,
-                            Counters* __restrict__ ctr) {
+// The first registration also records where its claim keeps its accepted
+// identities (at, end); lookups only read it in a later kernel.
+__device__ void id_register(const IdDev& t, uint64_t key, uint32_t block, uint64_t at,
+                            uint64_t end, Counters* __restrict__ ctr) {
   IdEntry* e = id_claim_slot(t, key);
   if (!e) return;
   if (!(atomicOr(&e->flags, kIdUsed) & kIdUsed))
     atomicAdd((unsigned long long*)&ctr->id_entries, 1ull);
   const uint32_t prev = atomicCAS(&e->block, kNone, block);
-  if (prev != kNone && prev != block && !(atomicOr(&e->flags, kIdAmbiguous) & kIdAmbiguous))
+  if (prev == kNone) {
+    IdSrc& src = t.src[e - t.e];
+    src.at = at;
+    src.end = end;
+  } else if (prev != block && !(atomicOr(&e->flags, kIdAmbiguous) & kIdAmbiguous)) {
     atomicAdd((unsigned long long*)&ctr->id_ambiguous, 1ull);
+  }
 }
 
 __device__ __forceinline__ const IdEntry* id_find(const IdDev& t, uint64_t key) {
@@ -760,7 +816,9 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
     const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
     if (j < npos) {
       reg.idn[fp_base + r.bo0 + j] = my_h;
-      if (offloaded) id_register(ids, my_h, b.bi[(uint64_t)r.bo0 + j], ctr);
+      if (offloaded)
+        id_register(ids, my_h, b.bi[(uint64_t)r.bo0 + j], fp_base + r.bo0 + j,
+                    fp_base + r.bo0 + npos, ctr);
     }
   }
   if (gl != 0) return;
@@ -1149,12 +1207,75 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
 
 // ------------------------------------------------------------------ lookup
 
-// Reuse lookup: one group of W lanes per request.  Lanes hash one token
-// block each, the chain runs through the group, then every lane probes the
-// identity table for its h_j; the group stops at the first block that is
-// not a plain hit (absent, or registered but ambiguous).
+// A lookup probe issued ahead of its use: the whole 16-byte entry at the
+// identity's home slot (key, block, flags), so that one load answers the
+// common case; id_probe_resolve finishes it.
+__device__ __forceinline__ u32x4 id_probe_issue(const IdDev& t, uint64_t key) {
+  const IdEntry* e = key == 0 ? t.e + t.mask + 1 : t.e + slot_of_id(key, t.mask);
+  return *(const u32x4*)e;
+}
+
+// The entry index of identity `key` (-1: not registered) from its home
+// entry; when the home slot holds another identity the probe continues from
+// the next slot (linear probing; the table is at most half full).
+__device__ __forceinline__ int64_t id_probe_resolve(const IdDev& t, uint64_t key, u32x4 home) {
+  const uint64_t k = ((uint64_t)home.y << 32) | home.x;
+  if (key == 0) return (home.w & kIdUsed) ? (int64_t)(t.mask + 1) : -1;
+  if (k == key) return (int64_t)slot_of_id(key, t.mask);
+  if (k == 0) return -1;
+  const IdEntry* e = id_find(t, key);
+  return e ? (int64_t)(e - t.e) : -1;
+}
+
+// First 16-token chunk of a block, loaded ahead (count < 16: not loaded;
+// the block's multilinear then loads its tokens itself).
+__device__ __forceinline__ void prefetch_chunk(uint32_t (&ch)[16], const uint32_t* __restrict__ tok,
+                                               uint64_t first, uint64_t count) {
+  if (count >= 16) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) ch[k] = tok[first + k];
+  }
+}
+
+// Token multilinear of a block whose first 16-token chunk, if it has one,
+// was loaded ahead into ch.
+__device__ __forceinline__ uint64_t multilinear_prefetched(const uint32_t (&ch)[16],
+                                                          const uint32_t* __restrict__ tok,
+                                                          uint64_t first, uint64_t count,
+                                                          const uint64_t* tkey) {
+  if (count < 16) return block_multilinear<0>(tok, first, count, tkey);
+  uint64_t m_sum = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) m_sum += (uint64_t)ch[k] * tkey[k];
+  if (count > 16) m_sum += block_multilinear<0>(tok, first + 16, count - 16, tkey + 16);
+  return m_sum;
+}
+
+// Reuse lookup: one group of W lanes per request; the group stops at the
+// first token block whose identity is not a plain hit (absent, or
+// registered but ambiguous).
+//
+// Narrow groups (requests of a few blocks) hash one token block per lane,
+// run the chain through the group and probe every lane's h_j.
+//
+// Wide groups (long requests) confirm positions without the serial chain.
+// When h_j of the request is a registered identity, the claim that first
+// registered it (IdSrc) has the same chain up to j and keeps its accepted
+// identities acc_j, acc_{j+1}, ...  Lane i of a window computes
+// hh = splitmix64(acc_{i-1} xor M_i) (h_prev for lane 0) and compares it
+// with acc_i.  By induction from the window's start, below the first lane q
+// whose hh differs (or that has no acc) the request's h equals acc, and at q
+// it equals hh, so the window yields the request's h for lanes 0..q exactly,
+// with no assumption about hash collisions.  Those lanes are probed in
+// parallel; the first that is not a plain hit stops the lookup.  If none
+// stops, a wholly confirmed window keeps the source, and otherwise lane q's
+// own identity (a plain hit) gives the next source.  Without a source (the
+// first position, or past the source claim's end) a window decides only its
+// first position, which is the serial chain's step.  The outputs are the
+// serial chain's.
 template <int W>
-__global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids, uint32_t bs,
+__global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids,
+                                                     const uint64_t* __restrict__ idn, uint32_t bs,
                                                      uint64_t seed,
                                                      claim_lookup_result* __restrict__ out) {
   __shared__ uint64_t tkey[kMaxBlockSize];
@@ -1169,34 +1290,102 @@ __global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids, uint
   const uint64_t ntok = bad ? 0 : to1 - to0;
   const uint64_t nt = (ntok + bs - 1) / bs;
 
-  uint64_t h = seed;
   uint64_t stop = kNoKey;  // (j << 1) | plain_miss of the first block that did not hit
   uint64_t h_at = seed;    // h_{hit - 1}
-  for (uint64_t j0 = 0; j0 < nt && stop == kNoKey; j0 += W) {
-    const uint64_t j = j0 + gl;
-    uint64_t m_sum = 0;
-    if (j < nt) {
-      const uint64_t first = j * bs;
-      const uint64_t count = ntok - first < bs ? ntok - first : bs;
-      m_sum = block_multilinear<(W >= 16 ? 2 : 0)>(b.tok, to0 + first, count, tkey);
+  if constexpr (W >= 16) {
+    uint64_t j = 0, h_prev = seed;  // next position to decide, and h_{j-1}
+    bool have_src = false;
+    uint64_t a = 0, a_end = 0;  // idn[a] is the source's identity at position j
+    // A window's first token chunk and accepted identity are loaded while
+    // the previous window's probes are in flight (speculatively: as if that
+    // window is confirmed whole; a window that is not discards them).
+    auto count_of = [&](uint64_t p) { return ntok - p * bs < bs ? ntok - p * bs : (uint64_t)bs; };
+    uint32_t ch[16];
+    if ((uint64_t)gl < nt) prefetch_chunk(ch, b.tok, to0 + (uint64_t)gl * bs, count_of(gl));
+    bool pre = true;        // ch holds the chunk of position j + gl
+    uint64_t pre_acc = 0;   // idn[a + gl], when pre_has
+    bool pre_has = false;
+    while (j < nt) {
+      const uint64_t jj = j + gl;
+      uint64_t m_sum = 0;
+      if (jj < nt) {
+        const uint64_t first = to0 + jj * bs;
+        m_sum = pre ? multilinear_prefetched(ch, b.tok, first, count_of(jj), tkey)
+                    : block_multilinear<0>(b.tok, first, count_of(jj), tkey);
+      }
+      const bool has_acc = have_src && jj < nt && a + gl < a_end;
+      const uint64_t acc = has_acc ? (pre_has ? pre_acc : idn[a + gl]) : 0;
+      const uint64_t up = prev_lane64(acc);  // group lane gl-1's acc
+      const uint64_t hh = splitmix_step((gl == 0 ? h_prev : up) ^ m_sum);
+      // first lane the source does not confirm (W: every lane up to nt)
+      const uint32_t q = group_first<W>(!(jj >= nt || (has_acc && hh == acc)));
+      const uint32_t known =
+          q < (uint32_t)W ? q : (uint32_t)(nt - j < (uint64_t)W ? nt - j : (uint64_t)W) - 1;
+      const uint64_t my_h = gl < q ? acc : hh;
+      const bool probe = gl <= known;
+      const u32x4 home = probe ? id_probe_issue(ids, my_h) : u32x4{0u, 0u, 0u, 0u};
+      // the next window, if this one is confirmed whole
+      const uint64_t jn = jj + W;
+      pre = q == (uint32_t)W;
+      pre_has = pre && have_src && jn < nt && a + W + gl < a_end;
+      if (pre && jn < nt) prefetch_chunk(ch, b.tok, to0 + jn * bs, count_of(jn));
+      if (pre_has) pre_acc = idn[a + W + gl];
+      int64_t my_e = -1;
+      bool amb = false;
+      if (probe) {
+        my_e = id_probe_resolve(ids, my_h, home);
+        const uint64_t home_slot = my_h == 0 ? ids.mask + 1 : slot_of_id(my_h, ids.mask);
+        amb = my_e >= 0 &&
+              (((uint64_t)my_e == home_slot ? home.w : ids.e[my_e].flags) & kIdAmbiguous);
+      }
+      const uint64_t miss = group_ballot<W>(probe && my_e < 0);
+      const uint64_t stops = miss | group_ballot<W>(amb);
+      if (stops) {  // the first position that is not a plain hit
+        const uint32_t p = (uint32_t)__builtin_ctzll(stops);
+        stop = ((j + p) << 1) | ((miss >> p) & 1u);
+        h_at = p > 0 ? group_read64<W>(my_h, gbase, p - 1) : h_prev;
+        break;
+      }
+      h_prev = group_read64<W>(my_h, gbase, known);
+      if (q == (uint32_t)W) {
+        a += known + 1;  // the whole window confirmed: keep following the source
+      } else {
+        const IdSrc src = ids.src[group_read64<W>((uint64_t)my_e, gbase, q)];
+        have_src = true;
+        a = src.at + 1;
+        a_end = src.end;
+      }
+      j += known + 1;
     }
-    const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
-    const uint64_t h_before = h;
-    const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
-    uint64_t my_stop = kNoKey;
-    if (j < nt) {
-      const IdEntry* e = id_find(ids, my_h);
-      if (!e)
-        my_stop = (j << 1) | 1u;
-      else if (e->flags & kIdAmbiguous)
-        my_stop = j << 1;
-    }
-    stop = group_min64<W>(my_stop);
-    if (stop == kNoKey) {
-      h_at = h;  // the whole window hit
-    } else {
-      const uint64_t js = stop >> 1;
-      h_at = js > j0 ? lane_read64(my_h, gbase + (uint32_t)(js - 1 - j0)) : h_before;
+    if (stop == kNoKey) h_at = h_prev;
+  } else {
+    uint64_t h = seed;
+    for (uint64_t j0 = 0; j0 < nt && stop == kNoKey; j0 += W) {
+      const uint64_t j = j0 + gl;
+      uint64_t m_sum = 0;
+      if (j < nt) {
+        const uint64_t first = j * bs;
+        const uint64_t count = ntok - first < bs ? ntok - first : bs;
+        m_sum = block_multilinear<0>(b.tok, to0 + first, count, tkey);
+      }
+      const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
+      const uint64_t h_before = h;
+      const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
+      uint64_t my_stop = kNoKey;
+      if (j < nt) {
+        const IdEntry* e = id_find(ids, my_h);
+        if (!e)
+          my_stop = (j << 1) | 1u;
+        else if (e->flags & kIdAmbiguous)
+          my_stop = j << 1;
+      }
+      stop = group_min64<W>(my_stop);
+      if (stop == kNoKey) {
+        h_at = h;  // the whole window hit
+      } else {
+        const uint64_t js = stop >> 1;
+        h_at = js > j0 ? lane_read64(my_h, gbase + (uint32_t)(js - 1 - j0)) : h_before;
+      }
     }
   }
   if (gl != 0) return;
@@ -1427,6 +1616,7 @@ struct claim_pool {
   uint64_t* idn_store = nullptr;  // accepted identities, parallel to fp_store
   uint64_t max_fp = 0, fp_used = 0;
   IdEntry* id_table = nullptr;
+  IdSrc* id_src = nullptr;  // parallel to id_table
   uint64_t id_mask = 0;
   uint64_t staged_blocks = 0;  // blocks written by the last staged offload
   uint64_t reg_used_ub = 0;  // upper bound on registered claims
@@ -1552,6 +1742,7 @@ IdDev id_dev(claim_pool* P) {
   IdDev t;
   t.mask = P->id_mask;
   t.e = P->id_table;
+  t.src = P->id_src;
   return t;
 }
 
@@ -1779,7 +1970,7 @@ void free_pool(claim_pool* P) {
                   P->mark,     P->uniq,     P->slot_of, P->reg,       P->fp_store,
                   P->log,      P->ctr,      P->outcomes, P->cnt,      P->pend,
                   P->tsum,     P->dup_table, P->f_blocks, P->f_bits,   P->idn_store,
-                  P->id_table};
+                  P->id_table, P->id_src};
   for (void* p : ptrs)
     if (p) dfree(p);
   if (P->host_ctr) (void)hipHostFree(P->host_ctr);
@@ -1897,7 +2088,7 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     // every registered identity is a footprint position: at most half full
     const uint64_t id_cap = next_pow2(2 * d->max_footprint < 64 ? 64 : 2 * d->max_footprint);
     P->id_mask = id_cap - 1;
-    if ((rc = dalloc(&P->id_table, id_cap + 1))) break;
+    if ((rc = dalloc(&P->id_table, id_cap + 1)) || (rc = dalloc(&P->id_src, id_cap + 1))) break;
     P->ev_cap = d->event_capacity;
     if ((rc = dalloc(&P->log, d->event_capacity))) break;
     if ((rc = dalloc(&P->ctr, 1))) break;
@@ -1922,7 +2113,8 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
       break;
     // identity table: key 0 (empty), block kNone, flags 0
     if ((rc = fill<uint64_t>(P, (uint64_t*)P->id_table, 2 * (P->id_mask + 2), 0)) ||
-        (rc = fill_strided_u64(P, (uint64_t*)P->id_table + 1, P->id_mask + 2, 2, (uint64_t)kNone)))
+        (rc = fill_strided_u64(P, (uint64_t*)P->id_table + 1, P->id_mask + 2, 2, (uint64_t)kNone)) ||
+        (rc = fill<uint64_t>(P, (uint64_t*)P->id_src, 2 * (P->id_mask + 2), 0)))
       break;
     if ((rc = fill<uint64_t>(P, (uint64_t*)P->ctr, sizeof(Counters) / 8, 0))) break;
     if (hipStreamSynchronize(P->stream) != hipSuccess) { rc = CLAIM_EHIP; break; }
@@ -2114,8 +2306,8 @@ int claim_lookup(claim_pool* P, const claim_batch* b, claim_lookup_result* out,
   if (out_cap < b->num_claims) return CLAIM_ENOSPC;
   if (b->num_claims == 0) return CLAIM_OK;
   HIP_TRY(hipSetDevice(P->device));
-  LAUNCH_GROUPED_W(k_lookup, P, b, lookup_group_width(b, P->bs), batch_dev(b), id_dev(P), P->bs,
-                   P->seed, out);
+  LAUNCH_GROUPED_W(k_lookup, P, b, lookup_group_width(b, P->bs), batch_dev(b), id_dev(P),
+                   P->idn_store, P->bs, P->seed, out);
   return CLAIM_OK;
 }
 
