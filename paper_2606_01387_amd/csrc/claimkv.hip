@@ -1058,9 +1058,9 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     const uint32_t sb = (j < n && blk < nb) ? blk : 0u;
     uint32_t bst = st.bstat[sb];
     // the cache identity of block j, from the accepted h_{j-1}
-    const uint64_t up = lane_read64(acc_h, gl == 0 ? gbase : gbase + gl - 1);
+    const uint64_t up = prev_lane64(acc_h);  // group lane gl-1's accepted identity
     const uint64_t hh = splitmix_step((gl == 0 ? carry : up) ^ m_sum);
-    carry = lane_read64(acc_h, gbase + W - 1);
+    carry = group_read64<W>(acc_h, gbase, W - 1);
     asm volatile("" : "+v"(bst));
     const bool mism = j < id_pos && hh != acc_h;
 
@@ -1098,19 +1098,26 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       if (j < intact) intact = j;
     }
     if (q == kNoKey) {  // windows ascend: the first window with a mismatch holds q
-      const uint64_t qk = group_min64<W>(mism ? j : kNoKey);
-      if (qk != kNoKey) {
-        q = qk;
-        h_qv = lane_read64(hh, gbase + (uint32_t)(qk - j0));
+      const uint32_t qi = group_first<W>(mism);
+      if (qi < (uint32_t)W) {
+        q = j0 + qi;
+        h_qv = group_read64<W>(hh, gbase, qi);
       }
     }
-    const uint64_t rk = group_min64<W>(my_key);
-    if (rk < best_pos) {
-      best_pos = rk;
-      acc_at_best = lane_read64(acc_h, gbase + (uint32_t)((rk & 0xFFFFFFFFull) - j0));
+    // the window's smallest key: positions ascend with the lane, so it is
+    // the first lane's with a class-0 key, else the first lane's with any
+    const uint64_t c0 = group_ballot<W>(my_key < (1ull << 32));
+    const uint64_t c_any = group_ballot<W>(my_key != kNoKey);
+    if (c_any) {
+      const uint32_t li = (uint32_t)__builtin_ctzll(c0 ? c0 : c_any);
+      const uint64_t rk = (c0 ? 0ull : (1ull << 32)) | (j0 + li);
+      if (rk < best_pos) {
+        best_pos = rk;
+        acc_at_best = group_read64<W>(acc_h, gbase, li);
+      }
     }
-    if (qmin >= j0 && qmin < j0 + W) acc_at_qmin = lane_read64(acc_h, gbase + (uint32_t)(qmin - j0));
-    if (last >= j0 && last < j0 + W) acc_at_last = lane_read64(acc_h, gbase + (uint32_t)(last - j0));
+    if (qmin >= j0 && qmin < j0 + W) acc_at_qmin = group_read64<W>(acc_h, gbase, (uint32_t)(qmin - j0));
+    if (last >= j0 && last < j0 + W) acc_at_last = group_read64<W>(acc_h, gbase, (uint32_t)(last - j0));
   }
 
   // the presented h at the positions the outcome reports: the winning key's
