@@ -403,6 +403,32 @@ __device__ __forceinline__ uint64_t block_multilinear(const uint32_t* __restrict
   return m_sum;
 }
 
+// First 16-token chunk of a block, loaded ahead (count < 16: not loaded;
+// the block's multilinear then loads its tokens itself).
+__device__ __forceinline__ void prefetch_chunk(uint32_t (&ch)[16], const uint32_t* __restrict__ tok,
+                                               uint64_t first, uint64_t count) {
+  if (count >= 16) {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) ch[k] = tok[first + k];
+  }
+}
+
+// Token multilinear of a block whose first 16-token chunk, if it has one,
+// was loaded ahead into ch; the rest of a longer block is summed with
+// block_multilinear<kTail>.
+template <int kTail>
+__device__ __forceinline__ uint64_t multilinear_prefetched(const uint32_t (&ch)[16],
+                                                          const uint32_t* __restrict__ tok,
+                                                          uint64_t first, uint64_t count,
+                                                          const uint64_t* tkey) {
+  if (count < 16) return block_multilinear<0>(tok, first, count, tkey);
+  uint64_t m_sum = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) m_sum += (uint64_t)ch[k] * tkey[k];
+  if (count > 16) m_sum += block_multilinear<kTail>(tok, first + 16, count - 16, tkey + 16);
+  return m_sum;
+}
+
 // Put the wave-uniform value `val` into lane `lane` of `old` (v_writelane;
 // the lane select goes through M0, written by a scalar move, so the
 // instruction reads one scalar register besides it).
@@ -1037,26 +1063,51 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   uint64_t carry = seed;           // accepted h just before the window
   uint64_t intact = n < qmin ? n : qmin;  // first position with any problem (lane-local, then group min)
   const uint64_t L = n > nt ? n : nt;
+  // Wide groups (long claims, many windows) load a window's position loads
+  // and first token chunk during the previous window, so that a window
+  // waits for one round trip (its status bytes) instead of two.
+  constexpr bool kAhead = W >= 16;
+  auto count_of = [&](uint64_t p) { return r.ntok - p * bs < bs ? r.ntok - p * bs : (uint64_t)bs; };
+  uint32_t nx_blk = kNone, nx_acc_blk = kNone;
+  uint64_t nx_acc_h = 0;
+  uint32_t nx_ch[kAhead ? 16 : 1];
+  if constexpr (kAhead) {
+    const uint64_t j = gl;
+    if (j < n) nx_blk = b.bi[(uint64_t)r.bo0 + j];
+    if (found && j < common) nx_acc_blk = reg.fp[fpo + j];
+    if (j < id_pos) nx_acc_h = reg.idn[fpo + j];
+    if (j < nt) prefetch_chunk(nx_ch, b.tok, r.to0 + j * bs, count_of(j));
+  }
   for (uint64_t j0 = 0; j0 < L; j0 += W) {
     const uint64_t j = j0 + gl;
     // the window's loads that depend only on j, issued together
     uint32_t blk = kNone, acc_blk = kNone;
     uint64_t acc_h = 0;
-    if (j < n) blk = b.bi[(uint64_t)r.bo0 + j];
-    if (found && j < common) acc_blk = reg.fp[fpo + j];
-    if (j < id_pos) acc_h = reg.idn[fpo + j];
-    // the token loads go out first (they do not wait for blk)
     uint64_t m_sum = 0;
-    if (j < nt) {
-      const uint64_t first = j * bs;
-      const uint64_t count = r.ntok - first < bs ? r.ntok - first : bs;
-      m_sum = block_multilinear<(W >= 16 ? 2 : 1)>(b.tok, r.to0 + first, count, tkey);
+    if constexpr (kAhead) {
+      blk = nx_blk;
+      acc_blk = nx_acc_blk;
+      acc_h = nx_acc_h;
+      if (j < nt) m_sum = multilinear_prefetched<1>(nx_ch, b.tok, r.to0 + j * bs, count_of(j), tkey);
+    } else {
+      if (j < n) blk = b.bi[(uint64_t)r.bo0 + j];
+      if (found && j < common) acc_blk = reg.fp[fpo + j];
+      if (j < id_pos) acc_h = reg.idn[fpo + j];
+      // the token loads go out first (they do not wait for blk)
+      if (j < nt) m_sum = block_multilinear<1>(b.tok, r.to0 + j * bs, count_of(j), tkey);
     }
     // per-block state, loaded unconditionally (block 0 stands in for a
     // lane without a pool block) so that it is in flight while the identity
     // step runs; the empty asm keeps every use, and so the wait, after it
     const uint32_t sb = (j < n && blk < nb) ? blk : 0u;
     uint32_t bst = st.bstat[sb];
+    if constexpr (kAhead) {  // the next window's loads, issued after the status byte's
+      const uint64_t jn = j + W;
+      nx_blk = jn < n ? b.bi[(uint64_t)r.bo0 + jn] : kNone;
+      nx_acc_blk = found && jn < common ? reg.fp[fpo + jn] : kNone;
+      nx_acc_h = jn < id_pos ? reg.idn[fpo + jn] : 0;
+      if (jn < nt) prefetch_chunk(nx_ch, b.tok, r.to0 + jn * bs, count_of(jn));
+    }
     // the cache identity of block j, from the accepted h_{j-1}
     const uint64_t up = prev_lane64(acc_h);  // group lane gl-1's accepted identity
     const uint64_t hh = splitmix_step((gl == 0 ? carry : up) ^ m_sum);
@@ -1234,30 +1285,6 @@ __device__ __forceinline__ int64_t id_probe_resolve(const IdDev& t, uint64_t key
   return e ? (int64_t)(e - t.e) : -1;
 }
 
-// First 16-token chunk of a block, loaded ahead (count < 16: not loaded;
-// the block's multilinear then loads its tokens itself).
-__device__ __forceinline__ void prefetch_chunk(uint32_t (&ch)[16], const uint32_t* __restrict__ tok,
-                                               uint64_t first, uint64_t count) {
-  if (count >= 16) {
-#pragma unroll
-    for (int k = 0; k < 16; ++k) ch[k] = tok[first + k];
-  }
-}
-
-// Token multilinear of a block whose first 16-token chunk, if it has one,
-// was loaded ahead into ch.
-__device__ __forceinline__ uint64_t multilinear_prefetched(const uint32_t (&ch)[16],
-                                                          const uint32_t* __restrict__ tok,
-                                                          uint64_t first, uint64_t count,
-                                                          const uint64_t* tkey) {
-  if (count < 16) return block_multilinear<0>(tok, first, count, tkey);
-  uint64_t m_sum = 0;
-#pragma unroll
-  for (int k = 0; k < 16; ++k) m_sum += (uint64_t)ch[k] * tkey[k];
-  if (count > 16) m_sum += block_multilinear<0>(tok, first + 16, count - 16, tkey + 16);
-  return m_sum;
-}
-
 // Reuse lookup: one group of W lanes per request; the group stops at the
 // first token block whose identity is not a plain hit (absent, or
 // registered but ambiguous).
@@ -1317,7 +1344,7 @@ __global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids,
       uint64_t m_sum = 0;
       if (jj < nt) {
         const uint64_t first = to0 + jj * bs;
-        m_sum = pre ? multilinear_prefetched(ch, b.tok, first, count_of(jj), tkey)
+        m_sum = pre ? multilinear_prefetched<0>(ch, b.tok, first, count_of(jj), tkey)
                     : block_multilinear<0>(b.tok, first, count_of(jj), tkey);
       }
       const bool has_acc = have_src && jj < nt && a + gl < a_end;
