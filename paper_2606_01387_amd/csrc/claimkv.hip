@@ -733,8 +733,7 @@ __global__ void __launch_bounds__(kThreads) k_digest(const u32x2* __restrict__ p
 // needs about a block, so that it loads one byte per block position.
 constexpr uint32_t kBsRecord = 1, kBsLoadFailed = 2, kBsMismatch = 4;
 
-// Add each unique block's piece-group partials.  One wave per block, lanes
-// over piece groups.
+// Add each unique block's piece-group partials.
 //   mode 0 (offload): d_off, valid_off = 1, load_failed = 0, slot_of
 //   mode 1 (check):   d_res, and bstat = record | reported failure |
 //                     (d_res != d_off); every block a check's claims can
@@ -751,27 +750,39 @@ __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restric
                                                        uint8_t* __restrict__ load_failed,
                                                        uint32_t* __restrict__ slot_of,
                                                        uint8_t* __restrict__ bstat) {
-  const uint32_t lane = threadIdx.x & 63;
+  // One lane per unique block.  Unique index u = n * groups + g was digested
+  // by the workgroups of group g, which wrote its partials at
+  // partial[(pg * groups + g) * NW + n]; slot t = g * NW + n puts
+  // consecutive n of one group in consecutive lanes, so each piece group's
+  // partials are read as one contiguous run per wave.
   const uint32_t U = ctr->uniq_count;
   const uint32_t NW = (U + groups - 1) / groups;
-  const uint32_t waves = gridDim.x * (kThreads / 64);
-  for (uint32_t u = blockIdx.x * (kThreads / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-       u < U; u += waves) {
-    const uint32_t g = u % groups, n = u / groups;
+  const uint64_t slots = (uint64_t)groups * NW;
+  const uint64_t stride = (uint64_t)gridDim.x * kThreads;
+  for (uint64_t t = (uint64_t)blockIdx.x * kThreads + threadIdx.x; t < slots; t += stride) {
+    const uint32_t g = (uint32_t)(t / NW), n = (uint32_t)(t % NW);
+    const uint32_t u = n * groups + g;
+    if (u >= U) continue;
+    // partials in batches of 32 loads issued together
+    const uint64_t* src = partial + (uint64_t)g * NW + n;
+    const uint64_t pstride = (uint64_t)groups * NW;
     uint64_t sum = 0;
-    for (uint32_t pg = lane; pg < pgs; pg += 64) sum += partial[((uint64_t)pg * groups + g) * NW + n];
-    sum = dpp_wave_sum64(sum);
-    if (lane == 0) {
-      const uint32_t b = uniq[u];
-      d_out[b] = sum;
-      if (mode == 0) {
-        valid_off[b] = 1;
-        load_failed[b] = 0;
-        slot_of[b] = staged ? u : kNone;
-      } else {
-        bstat[b] = (uint8_t)(kBsRecord | (load_failed[b] ? kBsLoadFailed : 0u) |
-                             (sum != d_off[b] ? kBsMismatch : 0u));
-      }
+    for (uint32_t pg0 = 0; pg0 < pgs; pg0 += 32) {
+      uint64_t v[32];
+#pragma unroll
+      for (uint32_t k = 0; k < 32; ++k) v[k] = pg0 + k < pgs ? src[(uint64_t)(pg0 + k) * pstride] : 0ull;
+#pragma unroll
+      for (uint32_t k = 0; k < 32; ++k) sum += v[k];
+    }
+    const uint32_t b = uniq[u];
+    d_out[b] = sum;
+    if (mode == 0) {
+      valid_off[b] = 1;
+      load_failed[b] = 0;
+      slot_of[b] = staged ? u : kNone;
+    } else {
+      bstat[b] = (uint8_t)(kBsRecord | (load_failed[b] ? kBsLoadFailed : 0u) |
+                           (sum != d_off[b] ? kBsMismatch : 0u));
     }
   }
 }
@@ -1901,7 +1912,7 @@ int launch_digest(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_
 }
 
 int launch_finalize(claim_pool* P, int mode, int staged) {
-  const uint32_t grid = P->nb / 4 + 1 < 8192 ? P->nb / 4 + 1 : 8192;
+  const uint32_t grid = grid_for((uint64_t)P->nb + P->groups);  // slots <= U + groups
   hipLaunchKernelGGL(k_finalize, dim3(grid), dim3(kThreads), 0, P->stream, P->uniq, P->ctr,
                      P->partial, P->pgs, P->groups, mode, staged,
                      mode == 0 ? P->d_off : P->d_res, P->d_off, P->valid_off, P->load_failed,
