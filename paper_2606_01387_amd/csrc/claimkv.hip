@@ -1464,12 +1464,14 @@ __global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids,
 
 // ------------------------------------------------------------ event append
 
-// Batches of up to kSmallEvents claims: one workgroup scans the per-claim
-// event counts, appends the events and advances the log, in one launch.
-// The claims are spread over all 1024 threads (per = ceil(C / 1024) each),
-// and a thread issues the loads of all its claims before it writes.
-constexpr uint32_t kSmallPer = 4;
-constexpr uint64_t kSmallEvents = 1024ull * kSmallPer;
+// Batches of up to kSmallEvents claims: one workgroup of 1024 threads
+// appends the events and advances the log, in one launch.  It takes the
+// claims in rounds of 1024, one per thread: coalesced loads of the counts,
+// pending records and ids, a scan of the counts, the round's events built in
+// LDS and copied to the log as contiguous 8-byte words.  (Four claims per
+// thread with each thread storing its own events took 15.6 us for 4096
+// claims.)
+constexpr uint64_t kSmallEvents = 4096;
 
 __global__ void __launch_bounds__(1024) k_events_small(const uint32_t* __restrict__ cnt,
                                                        const Pend* __restrict__ pend,
@@ -1477,48 +1479,41 @@ __global__ void __launch_bounds__(1024) k_events_small(const uint32_t* __restric
                                                        Counters* __restrict__ ctr,
                                                        claim_event* __restrict__ log) {
   __shared__ uint32_t lds[17];
-  __shared__ uint64_t base_pos, base_seq;
-  if (threadIdx.x == 0) {
-    base_pos = ctr->log_count;
-    base_seq = ctr->seq_next;
-  }
-  const uint32_t per = (uint32_t)((C + 1023) / 1024);  // <= kSmallPer
-  const uint64_t first = (uint64_t)threadIdx.x * per;
-  uint32_t v[kSmallPer];
-  Pend pe[kSmallPer];
-  uint64_t cid[kSmallPer];
-  uint32_t sum = 0;
-#pragma unroll
-  for (uint32_t k = 0; k < kSmallPer; ++k) {
-    const bool mine = k < per && first + k < C;
-    v[k] = mine ? cnt[first + k] : 0;
-    sum += v[k];
-  }
-#pragma unroll
-  for (uint32_t k = 0; k < kSmallPer; ++k)
-    if (v[k]) {
-      pe[k] = pend[first + k];
-      cid[k] = ids[first + k];
+  __shared__ claim_event s_ev[2 * 1024];
+  const uint64_t base_pos = ctr->log_count, base_seq = ctr->seq_next;
+  uint64_t run = 0;
+  for (uint64_t c0 = 0; c0 < C; c0 += 1024) {
+    const uint64_t c = c0 + threadIdx.x;
+    const uint32_t v = c < C ? cnt[c] : 0u;
+    Pend pe;
+    uint64_t cid = 0;
+    if (v) {
+      pe = pend[c];
+      cid = ids[c];
     }
-  uint32_t total;
-  uint64_t pos = block_exclusive_scan_1024(sum, &total, lds);  // also orders base_* reads
-#pragma unroll
-  for (uint32_t k = 0; k < kSmallPer; ++k) {
-    for (uint32_t e = 0; e < v[k]; ++e, ++pos) {
+    uint32_t total;
+    uint32_t at = block_exclusive_scan_1024(v, &total, lds);  // also orders the LDS reuse
+    for (uint32_t e = 0; e < v; ++e, ++at) {
       claim_event ev;
-      ev.seq = base_seq + pos;
-      ev.claim_id = cid[k];
-      ev.aux = e == 0 ? pe[k].aux0 : pe[k].aux1;
-      ev.kind = (pe[k].kinds >> (8 * e)) & 0xFFu;
-      ev.block_index = pe[k].j;
-      ev.phys_block = pe[k].phys;
+      ev.seq = base_seq + run + at;
+      ev.claim_id = cid;
+      ev.aux = e == 0 ? pe.aux0 : pe.aux1;
+      ev.kind = (pe.kinds >> (8 * e)) & 0xFFu;
+      ev.block_index = pe.j;
+      ev.phys_block = pe.phys;
       ev.reserved = 0;
-      log[base_pos + pos] = ev;
+      s_ev[at] = ev;
     }
+    __syncthreads();
+    const uint64_t* src = (const uint64_t*)s_ev;
+    uint64_t* dst = (uint64_t*)(log + base_pos + run);
+    for (uint32_t i = threadIdx.x; i < total * (sizeof(claim_event) / 8); i += 1024) dst[i] = src[i];
+    run += total;
+    __syncthreads();  // s_ev is reused by the next round
   }
   if (threadIdx.x == 0) {
-    ctr->log_count = base_pos + total;
-    ctr->seq_next = base_seq + total;
+    ctr->log_count = base_pos + run;
+    ctr->seq_next = base_seq + run;
   }
 }
 
