@@ -307,37 +307,59 @@ __device__ __forceinline__ int64_t reg_find(const RegDev& r, uint64_t id) {
   return -1;
 }
 
-// Slot of identity `key`, inserting the key if it is absent.
-__device__ IdEntry* id_claim_slot(const IdDev& t, uint64_t key) {
-  if (key == 0) return t.e + t.mask + 1;
-  uint64_t s = slot_of_id(key, t.mask);
-  for (uint64_t probe = 0; probe <= t.mask; ++probe) {
-    const unsigned long long old =
-        atomicCAS((unsigned long long*)&t.e[s].key, 0ull, (unsigned long long)key);
-    if (old == 0ull || old == key) return t.e + s;
-    s = (s + 1) & t.mask;
+// Registration of an identity happens in two passes, so that a position
+// whose identity is already present costs no atomic and a new identity one.
+//
+// Pass 1 (id_insert, during acceptance): find the identity's slot, reading
+// before writing; only an empty slot is claimed, with one CAS on the key.
+// The CAS winner stores the block and where its claim keeps its accepted
+// identities (IdSrc) with plain stores.  The identity 0 lives in the extra
+// entry e[mask + 1], claimed by setting kIdUsed.
+//
+// Pass 2 (k_register_owners, after acceptance): every registering position
+// compares its block with the stored one; a different block is duplicate
+// ownership and marks the identity ambiguous for good.  Among racing first
+// registrants the stored block and source depend on the order, but they
+// are read only for identities that are not ambiguous, so every output is
+// order-independent.
+//
+// Returns kRegNewEntry if this call inserted the identity.
+constexpr uint32_t kRegNewEntry = 1;
+
+__device__ uint32_t id_insert(const IdDev& t, uint64_t key, uint32_t block, uint64_t at,
+                              uint64_t end) {
+  uint64_t s;
+  if (key == 0) {
+    s = t.mask + 1;
+    if (atomicOr(&t.e[s].flags, kIdUsed) & kIdUsed) return 0;
+  } else {
+    s = slot_of_id(key, t.mask);
+    for (uint64_t probe = 0;; ++probe) {
+      if (probe > t.mask) return 0;  // unreachable: the table is at most half full
+      // keys only ever go from 0 to their final value, so a non-zero read is
+      // final; a stale 0 only costs a CAS that reports the real key
+      uint64_t k = t.e[s].key;
+      if (k == 0)
+        k = atomicCAS((unsigned long long*)&t.e[s].key, 0ull, (unsigned long long)key);
+      if (k == 0) break;         // inserted here
+      if (k == key) return 0;    // present
+      s = (s + 1) & t.mask;      // another identity: keep probing
+    }
   }
-  return nullptr;  // unreachable: the table is at most half full
+  t.e[s].block = block;
+  t.src[s].at = at;
+  t.src[s].end = end;
+  return kRegNewEntry;
 }
 
-// Register (key -> block).  Order-independent: the first registration sets
-// the block, any later one with another block marks the identity ambiguous.
-// The first registration also records where its claim keeps its accepted
-// identities (at, end); lookups only read it in a later kernel.
-__device__ void id_register(const IdDev& t, uint64_t key, uint32_t block, uint64_t at,
-                            uint64_t end, Counters* __restrict__ ctr) {
-  IdEntry* e = id_claim_slot(t, key);
-  if (!e) return;
-  if (!(atomicOr(&e->flags, kIdUsed) & kIdUsed))
-    atomicAdd((unsigned long long*)&ctr->id_entries, 1ull);
-  const uint32_t prev = atomicCAS(&e->block, kNone, block);
-  if (prev == kNone) {
-    IdSrc& src = t.src[e - t.e];
-    src.at = at;
-    src.end = end;
-  } else if (prev != block && !(atomicOr(&e->flags, kIdAmbiguous) & kIdAmbiguous)) {
-    atomicAdd((unsigned long long*)&ctr->id_ambiguous, 1ull);
-  }
+// Adds the active lanes whose predicate holds to *counter with one atomic
+// per wave (many lanes adding 1 to one address serialize on it).  Every
+// active lane must call it at the same point.
+__device__ __forceinline__ void wave_count(uint64_t* counter, bool pred) {
+  const uint64_t m = __ballot(pred);
+  const uint64_t active = __ballot(true);
+  if (m && (threadIdx.x & 63) == (uint32_t)__builtin_ctzll(active))
+    atomicAdd((unsigned long long*)counter, (unsigned long long)__builtin_popcountll(m));
 }
 
 __device__ __forceinline__ const IdEntry* id_find(const IdDev& t, uint64_t key) {
@@ -851,12 +873,14 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
     }
     const uint64_t steps = nt - j0 < (uint64_t)W ? nt - j0 : (uint64_t)W;
     const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
+    uint32_t res = 0;
     if (j < npos) {
       reg.idn[fp_base + r.bo0 + j] = my_h;
       if (offloaded)
-        id_register(ids, my_h, b.bi[(uint64_t)r.bo0 + j], fp_base + r.bo0 + j,
-                    fp_base + r.bo0 + npos, ctr);
+        res = id_insert(ids, my_h, b.bi[(uint64_t)r.bo0 + j], fp_base + r.bo0 + j,
+                        fp_base + r.bo0 + npos);
     }
+    wave_count(&ctr->id_entries, res & kRegNewEntry);
   }
   if (gl != 0) return;
   if (r.malformed) {
@@ -892,7 +916,7 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
     if (kb < r.n) pred = (uint32_t)kb;
   }
   e.pred = pred;
-  atomicAdd((unsigned long long*)&ctr->reg_count, 1ull);
+  wave_count(&ctr->reg_count, true);  // the group leaders that got here
   Pend pe;
   pe.aux0 = h;
   pe.aux1 = r.n;
@@ -905,6 +929,40 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
 }
 
 // ----------------------------------------------------------------- restore
+
+// Registration pass 2: duplicate ownership.  Every position an offloaded
+// claim of the batch registered compares its block with the block stored
+// for its identity; a different one makes the identity ambiguous (counted
+// once, by the call that sets the flag).
+template <int W>
+__global__ void __launch_bounds__(kThreads) k_register_owners(BatchDev b, RegDev reg, IdDev ids,
+                                                              uint32_t nb, uint32_t bs,
+                                                              uint64_t fp_base,
+                                                              Counters* __restrict__ ctr) {
+  const uint64_t c = group_claim<W>();
+  if (c >= b.C) return;
+  const uint32_t gl = (threadIdx.x & 63) & (W - 1);
+  const Row r = read_row(b, c);
+  const uint64_t nt = (r.ntok + bs - 1) / bs;
+  uint32_t missing = 0;
+  for (uint64_t j = gl; j < r.n; j += W)
+    if (b.bi[(uint64_t)r.bo0 + j] >= nb) missing = 1;
+  missing = group_or<W>(missing);
+  const bool offloaded = !r.malformed && r.n > 0 && !missing && (uint64_t)r.n == nt;
+  if (!offloaded) return;
+  for (uint64_t j0 = 0; j0 < r.n; j0 += W) {
+    const uint64_t j = j0 + gl;
+    uint32_t amb = 0;
+    if (j < r.n) {
+      const uint64_t key = reg.idn[fp_base + r.bo0 + j];
+      const IdEntry* e = id_find(ids, key);
+      if (e && e->block != b.bi[(uint64_t)r.bo0 + j] &&
+          !(atomicOr((uint32_t*)&e->flags, kIdAmbiguous) & kIdAmbiguous))
+        amb = 1;
+    }
+    wave_count(&ctr->id_ambiguous, amb);
+  }
+}
 
 __global__ void __launch_bounds__(kThreads) k_flips(uint32_t* __restrict__ pool32, uint32_t nb,
                                                     uint64_t chunk_bytes, uint32_t n,
@@ -2208,6 +2266,7 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
     HIP_TRY(hipGetLastError());
     LAUNCH_GROUPED(k_accept, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->seed, P->fp_used, P->ctr,
                    P->cnt, P->pend);
+    LAUNCH_GROUPED(k_register_owners, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->fp_used, P->ctr);
     TRY(append_events(P, b));
   }
   // offload record; a staged offload replaces every earlier staging slot
