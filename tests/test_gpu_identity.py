@@ -364,3 +364,44 @@ def test_chain_reproduces_published_outputs_on_gpu(torch, ck):
     assert int(out_changed[0]["reasons"]) & ck.R_TOKEN_MISMATCH
     del kv
     free_gpu(torch)
+
+
+def test_same_batch_duplicate_ownership(torch, ck):
+    """Registrants of one identity racing inside one offload batch: pairs of
+    claims with the same tokens, half of them with a different first block
+    (duplicate ownership of h_0, so h_0 is ambiguous; their later identities
+    have the same blocks and stay plain), half with identical blocks (stored
+    once).  The GPU registers concurrently, the oracle in batch order; the
+    identity counts and every lookup must agree."""
+    note("same-batch duplicate ownership")
+    w = TINY
+    g = w.geometry
+    bs = g.block_size
+    rng = np.random.default_rng(17)
+    parts, reqs = [], []
+    for i in range(100):
+        nblk = int(rng.integers(2, 5))
+        t = rng.integers(1, 32000, size=nblk * bs - int(rng.integers(0, bs)), dtype=np.uint32)
+        blocks = [int(x) for x in rng.integers(0, g.num_blocks, size=nblk)]
+        other = list(blocks)
+        if i % 2 == 0:
+            other[0] = (blocks[0] + 1 + int(rng.integers(0, g.num_blocks - 1))) % g.num_blocks
+        parts += [(1000 + 2 * i, blocks, t), (1001 + 2 * i, other, t.copy())]
+        reqs += [t, t[: bs], np.concatenate([t, rng.integers(1, 32000, size=bs, dtype=np.uint32)])]
+    order = rng.permutation(len(parts))
+    batch = from_claims([parts[k] for k in order])
+    rb = from_claims([(5000 + i, [], r) for i, r in enumerate(reqs)])
+    kv = gpu_pool_tensor(torch, w)
+    op = O.OraclePool(g.num_blocks, bs, w.seed)
+    zero = np.zeros(g.num_blocks, np.uint64)
+    with ck.Pool(g, w.seed, kv, max_claims=512, max_footprint=2048, event_capacity=2048) as pool:
+        pool.offload(ck.DeviceBatch(batch))
+        assert op.offload(batch, zero) == O.OK
+        stats = pool.identity_stats()
+        got = pool.lookup(ck.DeviceBatch(rb))
+    assert stats == op.identity_stats()
+    assert stats[1] == 50  # h_0 of every pair with a different first block
+    same_lookups(got, op.lookup(rb))
+    assert (got["status"] == ck.LOOKUP_UNKNOWN).sum() >= 100
+    del kv
+    free_gpu(torch)
