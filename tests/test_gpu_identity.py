@@ -405,3 +405,73 @@ def test_same_batch_duplicate_ownership(torch, ck):
     assert (got["status"] == ck.LOOKUP_UNKNOWN).sum() >= 100
     del kv
     free_gpu(torch)
+
+
+@pytest.mark.parametrize("batches", [1, 3])
+def test_lookup_source_switching(torch, ck, batches):
+    """Long requests (wide groups) that leave one accepted claim's identities
+    for another's: a tree of claims that share prefixes of different lengths
+    (offloaded in one batch, or in three), and requests that follow one
+    branch, switch branches at a divergence, run past a shorter claim's end
+    onto a longer one, or leave every claim.  Every lookup field against the
+    oracle."""
+    note(f"lookup source switching, {batches} offload batches")
+    w = TINY
+    g = w.geometry
+    bs = g.block_size
+    rng = np.random.default_rng(23 + batches)
+
+    def toks(nblk):
+        return rng.integers(1, 32000, size=nblk * bs, dtype=np.uint32)
+
+    root = toks(90)
+    branches = [root]
+    for cut in (7, 20, 33, 64, 80):  # branches diverging from earlier ones at block `cut`
+        base = branches[int(rng.integers(0, len(branches)))]
+        cut = min(cut, base.size // bs - 1)
+        branches.append(np.concatenate([base[: cut * bs], toks(int(rng.integers(10, 70)))]))
+    short = root[: 30 * bs].copy()  # a shorter claim inside the root
+    claims = branches + [short]
+    parts = []
+    for i, t in enumerate(claims):
+        nblk = t.size // bs
+        parts.append((700 + i, [int(x) for x in rng.integers(0, g.num_blocks, size=nblk)], t))
+    # shared prefixes keep the same physical blocks as the claim they copy
+    by_tokens = {}
+    for k, (cid, blks, t) in enumerate(parts):
+        for j in range(len(blks)):
+            key = t[: (j + 1) * bs].tobytes()
+            if key in by_tokens:
+                blks[j] = by_tokens[key]
+            else:
+                by_tokens[key] = blks[j]
+    reqs = []
+    for t in claims:
+        reqs.append(t)
+        reqs.append(np.concatenate([t, toks(3)]))
+        cut = int(rng.integers(1, t.size))
+        reqs.append(t[:cut])
+        changed = t.copy()
+        changed[int(rng.integers(0, t.size))] += 1
+        reqs.append(changed)
+    # follow the short claim, then continue along the root past its end
+    reqs.append(root[: 60 * bs])
+    rb = from_claims([(9000 + i, [], r) for i, r in enumerate(reqs)])
+    assert rb.num_tokens // rb.num_claims >= 16 * bs  # wide lookup groups
+    groups = np.array_split(rng.permutation(len(parts)), batches)
+    kv = gpu_pool_tensor(torch, w)
+    op = O.OraclePool(g.num_blocks, bs, w.seed)
+    zero = np.zeros(g.num_blocks, np.uint64)
+    with ck.Pool(g, w.seed, kv, max_claims=64, max_footprint=4096, event_capacity=512) as pool:
+        for grp in groups:
+            bt = from_claims([parts[k] for k in grp])
+            pool.offload(ck.DeviceBatch(bt))
+            assert op.offload(bt, zero) == O.OK
+        got = pool.lookup(ck.DeviceBatch(rb))
+        stats = pool.identity_stats()
+    want = op.lookup(rb)
+    same_lookups(got, want)
+    assert stats == op.identity_stats()
+    assert (got["status"] == ck.LOOKUP_HIT).sum() >= len(claims)
+    del kv
+    free_gpu(torch)
