@@ -54,7 +54,10 @@
  *     claim_offload (for its acceptance verdict and to settle its counts),
  *     claim_restore (to read the host fault lists), outcomes_read,
  *     claim_block_state_read, claim_timing_read, claim_identity_stats and
- *     claim_pool_destroy wait for the stream;
+ *     claim_pool_destroy wait for the stream, and claim_check waits, then
+ *     allocates, only when its batch has more claims than any earlier call
+ *     of the pool (the per-claim scratch grows to at least 1024 claims and
+ *     is kept until claim_pool_destroy);
  *   - device arrays passed in a claim_batch must stay valid and unchanged
  *     until the queued work that reads them has completed;
  *   - calls on one pool must not overlap from several host threads.
