@@ -207,6 +207,7 @@ def main() -> int:
                    event_capacity=2 * C * (steps + warm + 2) + 4 * C, timing=True,
                    stage_timing=args.stages)
     round_trip = None
+    lifecycle = None
     if args.round_trip:
         # the host-link leg of the lifecycle: gather + digest straight into
         # pinned host memory, lose the device copy, scatter back from host
@@ -257,8 +258,20 @@ def main() -> int:
         }
         del staging
     else:
+        # the lifecycle steps before the checks, timed once (whole calls,
+        # including their waits on the stream); not part of the check's value
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
         pool.offload(db)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
         pool.restore(db, faults=faults)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        lifecycle = {"offload_ms": round((t1 - t0) * 1e3, 3), "restore_ms": round((t2 - t1) * 1e3, 3),
+                     "note": "claim_offload (acceptance, identity registration, offload digest) and "
+                             "claim_restore (faults, RESTORE_REQUIRED) on the device-resident pool, "
+                             "wall time of one call each, including the offload's host waits"}
     pool.read(max_outcomes=1)
 
     for _ in range(warm):
@@ -370,6 +383,8 @@ def main() -> int:
     }
     if round_trip is not None:
         line["round_trip"] = round_trip
+    if lifecycle is not None:
+        line["lifecycle"] = lifecycle
     if not args.no_cpu_baseline:
         base, want, want_ev, d0, d1, real = cpu_baseline(w, batch, faults, args.cpu_sample_gb)
         line["cpu_baseline"] = base
