@@ -51,10 +51,14 @@
  *
  * Parity pins (checked by the CPU tests): the published SplitMix64 outputs
  * for seed 0; D(0) = 0, D(e_i) = k_i, additivity, the exact single-bit-flip
- * delta +-2^beta * k_i; exhaustive single flips on a small block; shared
- * token prefixes give equal chain hashes; outcome enumeration over every
- * ok/failed/missing assignment of short claims; memcmp brute force of the
- * failing set on the tiny pool; the paper's event-order templates.
+ * delta +-2^beta * k_i; exhaustive single flips on a small block; four
+ * token blocks whose chain h_0 .. h_3 is the published SplitMix64 stream
+ * for seed 0; shared token prefixes give equal chain hashes; outcome
+ * enumeration over every ok/failed/missing assignment of short claims, with
+ * every predicate length; memcmp brute force of the failing set on the tiny
+ * pool; brute-force walks over token-prefix tuples for the identity table
+ * and the lookup; the paper's event-order templates and its 448-token and
+ * 17-token examples.
  */
 
 #include <cstdint>
