@@ -40,6 +40,38 @@ def test_mix64_fixes_zero_and_is_injective_on_sample():
     assert len({O.mix64(x) for x in xs}) == len(set(xs))
 
 
+def _unxorshift(y: int, s: int) -> int:
+    """Inverse of y = x ^ (x >> s) on 64-bit words: recover x from its top
+    bits down, s bits at a time."""
+    x = y
+    for _ in range(64 // s + 1):
+        x = y ^ (x >> s)
+    return x & M64
+
+
+def _mix64_inverse(z: int) -> int:
+    """The SplitMix64 finaliser run backwards: each step is a bijection (xor
+    with a right shift, multiplication by an odd constant mod 2^64)."""
+    c1, c2 = 0xBF58476D1CE4E5B9, 0x94D049BB133111EB
+    z = _unxorshift(z, 31)
+    z = z * pow(c2, -1, 1 << 64) & M64
+    z = _unxorshift(z, 27)
+    z = z * pow(c1, -1, 1 << 64) & M64
+    return _unxorshift(z, 30)
+
+
+def test_mix64_is_the_published_bijection():
+    # the oracle's finaliser undone step by step by the inverse of the
+    # published steps: a changed shift, constant or step order breaks it
+    rng = np.random.default_rng(3)
+    xs = [0, 1, M64, GAMMA] + [int(v) for v in rng.integers(0, 2**64, size=300, dtype=np.uint64)]
+    for x in xs:
+        assert _mix64_inverse(O.mix64(x)) == x
+    # and the published outputs come from the states (i+1) * gamma
+    for i, g in enumerate(GOLD):
+        assert _mix64_inverse(g) == (i + 1) * GAMMA & M64
+
+
 def test_key_schedules_are_odd_stream_outputs():
     for i, g in enumerate(GOLD):
         assert O.kv_key(0, i) == g | 1
