@@ -27,7 +27,7 @@ import pytest
 from oracle import oracle as O
 from paper_2606_01387_amd.synth import (FULL, MISSING, TINY, FaultSpec, Geometry, Workload, content,
                                         from_claims, make_batch, make_faults, make_requests, scaled)
-from tests.helpers import apply_flips, digests, modeled_digests
+from tests.helpers import apply_flips, digests, modeled_digests, validate_lifecycle
 
 pytestmark = pytest.mark.gpu
 
@@ -505,6 +505,7 @@ def test_full_size_parity(torch, ck, name):
     same_events(ev_pre, want_pre)
     same_outcomes(out, want)
     same_events(ev, op.events())
+    validate_lifecycle(batch, ev_pre, ev, out)  # the paper's lifecycle order, from the paper alone
     want_lk = op.lookup(reqs)
     for f in want_lk.dtype.names:
         if f != "pad":

@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 
 from oracle import oracle as O
-from paper_2606_01387_amd.synth import MISSING, TINY, FaultSpec, from_claims, make_batch, make_faults
+from paper_2606_01387_amd.synth import FULL, MISSING, TINY, FaultSpec, from_claims, make_batch, make_faults, scaled
 from tests.conftest import golden_lines
 from tests.helpers import NONE32, apply_flips, digests, expected_by_scan, host_pool, modeled_digests, oracle_lifecycle
 
@@ -492,3 +492,27 @@ def test_modeled_digests_reproduce_real_digest_outcomes():
     out_mod = op.check(b, m1)
     assert np.array_equal(out_real, out_mod)
     assert np.array_equal(ev_real, op.events())
+
+
+@pytest.mark.parametrize("w", [TINY, scaled(FULL["llama3-70b"], 24, 40, missing_claim_rate=0.1),
+                               scaled(FULL["small-claim-stress"], 256, 30000)],
+                         ids=lambda w: w.name)
+def test_event_log_follows_the_lifecycle_at_scale(w):
+    """The oracle's event log over a whole workload, checked against the
+    paper's lifecycle order by a validator written from the paper alone
+    (tests.helpers.validate_lifecycle): consecutive sequence numbers,
+    ACCEPTED (+ OFFLOADED) in batch order, RESTORE_REQUIRED for the
+    offloaded claims, one terminal outcome per claim that agrees with its
+    code, the claim itself as the blocking id."""
+    from tests.helpers import modeled_digests, validate_lifecycle
+
+    b = make_batch(w)
+    f = make_faults(w, b)
+    d0, d1 = modeled_digests(w, f, [])
+    op = O.OraclePool(w.geometry.num_blocks, w.geometry.block_size, w.seed)
+    assert op.offload(b, d0) == O.OK
+    assert op.restore(b, f.load_failed) == O.OK
+    pre = op.events(clear=True)
+    out = op.check(b, d1)
+    validate_lifecycle(b, pre, op.events(), out)
+    assert len(set(out["code"].tolist())) >= 2
