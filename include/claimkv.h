@@ -251,7 +251,8 @@ typedef struct claim_timing {
  * Allocates the pool's device state: offload and restored digests, offload
  * records, reported-failure flags, the claim registry (ids, state, token
  * count, chain hash, footprint, per-position accepted identities), the
- * cache-identity table (16 bytes per entry, next_pow2(2 * max_footprint)
+ * cache-identity table (32 bytes per entry: the entry and where its first
+ * registrant keeps its accepted identities; next_pow2(2 * max_footprint)
  * entries), the event log and scratch.  Returns EINVAL for a bad
  * description, ENOMEM / EHIP on allocation failure. */
 int claim_pool_create(const claim_pool_desc* desc, claim_pool** out);
