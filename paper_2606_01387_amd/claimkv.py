@@ -227,12 +227,17 @@ class Pool:
             _check(lib().claim_pool_create(ctypes.byref(d), ctypes.byref(h)), "claim_pool_create")
         self._h = h
         self.event_capacity = event_capacity
+        # device arrays of calls still queued on the pool's stream: the C ABI
+        # needs them alive until that work completes, which the next call
+        # that waits for the stream guarantees
+        self._inflight = []
 
     def close(self) -> None:
         h = getattr(self, "_h", None)
         if h is not None and h.value:
             _check(lib().claim_pool_destroy(h), "claim_pool_destroy")
         self._h = None
+        self._inflight = []
 
     def __del__(self):
         try:
@@ -250,6 +255,7 @@ class Pool:
     def offload(self, batch: DeviceBatch, staging=None, staging_bytes: int | None = None) -> None:
         ptr, nbytes = _staging_args(staging, staging_bytes)
         _check(lib().claim_offload(self._h, ctypes.byref(batch.struct), ptr, nbytes), "claim_offload")
+        self._inflight = []  # claim_offload ends by waiting for the stream
 
     def restore(self, batch: DeviceBatch, staging=None, faults=None,
                 staging_bytes: int | None = None) -> None:
@@ -267,10 +273,12 @@ class Pool:
                          load_failed_blocks=lf.ctypes.data if lf.size else None)
         _check(lib().claim_restore(self._h, ctypes.byref(batch.struct), ptr, nbytes,
                                    ctypes.byref(fs) if fs is not None else None), "claim_restore")
-        del keep
+        del keep  # host fault lists: read before claim_restore returns
+        self._inflight += [batch, staging]
 
     def check(self, batch: DeviceBatch) -> None:
         _check(lib().claim_check(self._h, ctypes.byref(batch.struct)), "claim_check")
+        self._inflight.append(batch)
 
     def lookup_async(self, batch: DeviceBatch, out=None):
         """Queue a reuse lookup of the batch's token rows on the pool stream;
@@ -283,12 +291,14 @@ class Pool:
         cap = out.numel() // LOOKUP_DTYPE.itemsize
         _check(lib().claim_lookup(self._h, ctypes.byref(batch.struct), out.data_ptr(), cap),
                "claim_lookup")
+        self._inflight += [batch, out]
         return out
 
     def lookup(self, batch: DeviceBatch) -> np.ndarray:
         """Reuse lookup of the batch's token rows, read back to the host."""
         out = self.lookup_async(batch)
         self.stream.synchronize()
+        self._inflight = []
         return out.cpu().numpy().view(LOOKUP_DTYPE)[: batch.num_claims].copy()
 
     def identity_stats(self) -> tuple[int, int]:
@@ -296,6 +306,7 @@ class Pool:
         e, a = ctypes.c_uint64(), ctypes.c_uint64()
         _check(lib().claim_identity_stats(self._h, ctypes.byref(e), ctypes.byref(a)),
                "claim_identity_stats")
+        self._inflight = []  # waited for the stream
         return int(e.value), int(a.value)
 
     def read(self, max_outcomes: int = 1 << 22, max_events: int | None = None):
@@ -308,6 +319,7 @@ class Pool:
         n_ev = ctypes.c_uint64()
         _check(lib().outcomes_read(self._h, out.ctypes.data, out.size, ctypes.byref(n_out),
                                    ev.ctypes.data, ev.size, ctypes.byref(n_ev)), "outcomes_read")
+        self._inflight = []  # waited for the stream
         return out[: n_out.value].copy(), ev[: n_ev.value].copy()
 
     def block_state(self, first: int = 0, count: int | None = None) -> dict:
@@ -321,6 +333,7 @@ class Pool:
         _check(lib().claim_block_state_read(self._h, first, count, d_off.ctypes.data,
                                             d_res.ctypes.data, valid.ctypes.data,
                                             failed.ctypes.data), "claim_block_state_read")
+        self._inflight = []  # waited for the stream
         return {"d_off": d_off, "d_res": d_res, "valid_off": valid, "load_failed": failed}
 
     def timing(self) -> dict:

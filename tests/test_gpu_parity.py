@@ -217,14 +217,15 @@ class Mirror:
     """The same lifecycle steps on the GPU library and on the oracle (tiny
     pool, real bytes on both sides)."""
 
-    def __init__(self, torch, ck, event_capacity=4096):
-        self.w = TINY
+    def __init__(self, torch, ck, event_capacity=4096, w=TINY, stream=None, max_claims=256,
+                 max_footprint=8192):
+        self.w = w
         g = self.w.geometry
         self.torch, self.ck = torch, ck
         self.kv = gpu_pool_tensor(torch, self.w)
         self.host = content.pool_host(g, self.w.content_seed)
-        self.pool = ck.Pool(g, self.w.seed, self.kv, max_claims=256, max_footprint=8192,
-                            event_capacity=event_capacity)
+        self.pool = ck.Pool(g, self.w.seed, self.kv, stream=stream, max_claims=max_claims,
+                            max_footprint=max_footprint, event_capacity=event_capacity)
         self.op = O.OraclePool(g.num_blocks, g.block_size, self.w.seed)
 
     def offload(self, batch):
@@ -241,13 +242,14 @@ class Mirror:
         f = FaultSpec(np.array([b for b, _ in flips], np.uint32),
                       np.array([bit for _, bit in flips], np.uint64),
                       np.array(load_failed, np.uint32))
+        # a temporary batch: the pool keeps its device arrays alive until
+        # the work queued on its stream (which may not be torch's) is done
         self.pool.restore(self.ck.DeviceBatch(batch), faults=f)
         self.host = apply_flips(self.host, self.w, f)
         assert self.op.restore(batch, f.load_failed) == O.OK
 
     def check(self, batch):
-        db = self.ck.DeviceBatch(batch)
-        self.pool.check(db)
+        self.pool.check(self.ck.DeviceBatch(batch))
         want = self.op.check(batch, digests(self.host, self.w))
         got, ev = self.pool.read()
         same_outcomes(got, want)
@@ -346,6 +348,47 @@ def test_controls_mirrored(torch, ck):
     m.check(empty)
     m.finish()
     del m
+    free_gpu(torch)
+
+
+def test_scratch_growth_and_two_pools(torch, ck):
+    """Two pools with different content and seeds, one on torch's stream and
+    one on a stream of its own, driven in turn; pool A sees batches of 20,
+    3000 and 20 claims (its per-claim scratch, sized for 1024 claims at
+    first, grows in the middle of its life) and checks a small batch again
+    after the large one.  Each pool against its own oracle."""
+    note("scratch growth and two pools")
+    wa = replace(TINY, name="pool-a")
+    wb = replace(TINY, name="pool-b", seed=4242, content_seed=4343)
+    caps = dict(event_capacity=40000, max_claims=8192, max_footprint=65536)
+    side = torch.cuda.Stream()
+    a = Mirror(torch, ck, w=wa, **caps)
+    b = Mirror(torch, ck, w=wb, stream=side, **caps)
+    torch.cuda.synchronize()  # pool content filled on torch's stream before pool B's stream reads it
+    small1 = make_batch(replace(wa, num_claims=20, gen_seed=301))
+    large = make_batch(replace(wa, num_claims=3000, gen_seed=302))
+    small2 = make_batch(replace(wa, num_claims=20, gen_seed=303))
+    other = make_batch(replace(wb, num_claims=50, gen_seed=304))
+    flips = [(3, 77), (40, 131071)]
+    a.offload(small1)
+    b.offload(other)
+    a.restore(small1, flips=flips)
+    b.restore(other, flips=[(5, 1)], load_failed=[9])
+    a.check(small1)
+    b.check(other)
+    a.offload(large)
+    a.restore(large)
+    got = a.check(large)
+    assert len(got) == 3000
+    b.check(other)
+    a.offload(small2)
+    a.restore(small2, load_failed=[12])
+    a.check(small2)
+    a.check(small1)  # the first batch again, after the scratch grew
+    b.check(other)
+    side.synchronize()
+    a.finish()
+    b.finish()
     free_gpu(torch)
 
 
