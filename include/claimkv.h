@@ -147,7 +147,10 @@ typedef struct claim_pool_desc {
  * block_offsets[c+1]) (CLAIM_NONE = missing entry) and token ids
  * tokens[token_offsets[c] .. token_offsets[c+1]).  Rows whose offsets run
  * backwards or past num_refs / num_tokens, or whose id is
- * CLAIM_RESERVED_ID, are malformed: never accepted, UNKNOWN at check.
+ * CLAIM_RESERVED_ID, are malformed: never accepted, UNKNOWN at check.  Rows
+ * after a backwards row may share entries with earlier rows: each
+ * well-formed row is still a claim of its own (claim_offload then stores
+ * each claim's footprint separately, one extra wait for the stream). 
  * Claim ids are stable and distinct from request ids (Table 5).
  *
  * predicate_tokens gives each claim's materialization predicate
@@ -281,8 +284,10 @@ int claim_pool_destroy(claim_pool* pool);
  * host memory from hipHostMalloc, 16-byte aligned, else EINVAL), one block
  * after another in ascending block-id order; staging_bytes must cover them
  * (else ENOSPC).  A staged offload replaces the previous one.  Waits twice
- * for the stream to read the acceptance verdict.  ENOSPC if the registry,
- * footprint store or event log could overflow. */
+ * for the stream to read the acceptance verdict (three times when a block
+ * row runs backwards).  ENOSPC if the registry, footprint store or event
+ * log could overflow; the footprint store takes num_refs entries, or, when
+ * rows share entries, the sum of the well-formed rows' lengths. */
 int claim_offload(claim_pool* pool, const claim_batch* batch, void* staging,
                   uint64_t staging_bytes);
 

@@ -257,7 +257,7 @@ struct Pend {  // events a claim will append (0..2), written before the scan
 
 struct Counters {  // device-resident counters of one pool (64 bytes)
   uint32_t uniq_count;
-  uint32_t dup_flag;
+  uint32_t dup_flag;      // kFlagDupId | kFlagBackwardRow
   uint64_t log_count;     // events held in the log
   uint64_t seq_next;      // next global sequence number
   uint64_t call_pos;      // log position of the current call's first event
@@ -268,6 +268,19 @@ struct Counters {  // device-resident counters of one pool (64 bytes)
 };
 
 static_assert(sizeof(Counters) == 64, "Counters layout");
+
+// dup_flag bits set by k_dupcheck: a claim id occurs twice or is already
+// registered (the batch is refused); some block row runs backwards, so the
+// rows after it may share block-table entries with earlier rows.
+constexpr uint32_t kFlagDupId = 1, kFlagBackwardRow = 2;
+
+// Where claim c's accepted footprint and identities start in the stores:
+// at its own block-table offset when the batch's rows are disjoint, else
+// at the offset k_footprint_offsets gave it.
+__device__ __forceinline__ uint64_t store_at(const uint64_t* fpo, uint64_t fp_base, uint64_t c,
+                                             uint32_t bo0) {
+  return fpo ? fpo[c] : fp_base + bo0;
+}
 static_assert(sizeof(IdEntry) == 16, "IdEntry layout");
 static_assert(sizeof(claim_lookup_result) == 40, "claim_lookup_result layout");
 static_assert(sizeof(claim_outcome) == 64, "claim_outcome layout");
@@ -505,13 +518,6 @@ __global__ void __launch_bounds__(kThreads) k_fill_strided(uint64_t* p, uint64_t
   const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
   for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
     p[i * stride_words] = v;
-}
-
-__global__ void __launch_bounds__(kThreads) k_copy_u32(uint32_t* dst, const uint32_t* src,
-                                                       uint64_t n) {
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
-    dst[i] = src[i];
 }
 
 // Mark the in-range blocks referenced by well-formed claims (filtered by
@@ -812,16 +818,18 @@ __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restric
 // ----------------------------------------------------------------- offload
 
 // Duplicate ownership: a non-reserved id occurring twice in the batch or
-// already registered sets dup_flag.  table is a cleared scratch hash set.
+// already registered sets kFlagDupId; a block row that runs backwards sets
+// kFlagBackwardRow.  table is a cleared scratch hash set.
 __global__ void __launch_bounds__(kThreads) k_dupcheck(BatchDev b, RegDev reg,
                                                        unsigned long long* table, uint64_t tmask,
                                                        Counters* ctr) {
   const uint64_t c = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
   if (c >= b.C) return;
+  if (b.bo[c + 1] < b.bo[c]) atomicOr(&ctr->dup_flag, kFlagBackwardRow);
   const uint64_t id = b.ids[c];
   if (id == kEmptyId) return;
   if (reg_find(reg, id) >= 0) {
-    atomicOr(&ctr->dup_flag, 1u);
+    atomicOr(&ctr->dup_flag, kFlagDupId);
     return;
   }
   uint64_t s = slot_of_id(id, tmask);
@@ -830,19 +838,53 @@ __global__ void __launch_bounds__(kThreads) k_dupcheck(BatchDev b, RegDev reg,
                                              (unsigned long long)id);
     if (old == kEmptyId) return;
     if (old == id) {
-      atomicOr(&ctr->dup_flag, 1u);
+      atomicOr(&ctr->dup_flag, kFlagDupId);
       return;
     }
     s = (s + 1) & tmask;
   }
 }
 
-// Acceptance: chain hash of the claim's tokens, presence of its footprint,
-// registration, and the ACCEPTED (+ OFFLOADED) events.
+// Store offsets for a batch whose block rows may share entries (some row
+// runs backwards): each well-formed claim gets a run of its own in the
+// footprint and identity stores, at fp_base plus the exclusive prefix sum of
+// the row lengths in claim order (a malformed row takes none); fpo[C] is the
+// total.  One workgroup; only such batches pay for it.
+__global__ void __launch_bounds__(1024) k_footprint_offsets(BatchDev b, uint64_t fp_base,
+                                                            uint64_t* __restrict__ fpo) {
+  __shared__ uint64_t s_sum[1024];
+  const uint32_t t = threadIdx.x;
+  const uint64_t per = (b.C + 1023) / 1024;
+  const uint64_t c0 = (uint64_t)t * per < b.C ? (uint64_t)t * per : b.C;
+  const uint64_t c1 = c0 + per < b.C ? c0 + per : b.C;
+  uint64_t mine = 0;
+  for (uint64_t c = c0; c < c1; ++c) mine += read_row(b, c).n;
+  s_sum[t] = mine;
+  __syncthreads();
+  for (uint32_t d = 1; d < 1024; d <<= 1) {  // inclusive scan of the 1024 sums
+    const uint64_t v = t >= d ? s_sum[t - d] : 0;
+    __syncthreads();
+    s_sum[t] += v;
+    __syncthreads();
+  }
+  uint64_t at = fp_base + s_sum[t] - mine;
+  for (uint64_t c = c0; c < c1; ++c) {
+    fpo[c] = at;
+    at += read_row(b, c).n;
+  }
+  if (t == 1023) fpo[b.C] = s_sum[1023];
+}
+
+// Acceptance: chain hash of the claim's tokens, presence of its footprint
+// (stored as the accepted footprint), its accepted identities and their
+// registration, and the record of its ACCEPTED (+ OFFLOADED) events.
 template <int W>
 __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdDev ids,
                                                      uint32_t nb, uint32_t bs, uint64_t seed,
-                                                     uint64_t fp_base, Counters* __restrict__ ctr,
+                                                     uint64_t fp_base,
+                                                     const uint64_t* __restrict__ fpo,
+                                                     uint32_t* __restrict__ fp_out,
+                                                     Counters* __restrict__ ctr,
                                                      uint32_t* __restrict__ cnt,
                                                      Pend* __restrict__ pend) {
   __shared__ uint64_t tkey[kMaxBlockSize];
@@ -854,10 +896,14 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
   const Row r = read_row(b, c);
   const uint64_t nt = (r.ntok + bs - 1) / bs;
 
+  const uint64_t at0 = r.malformed ? 0 : store_at(fpo, fp_base, c, r.bo0);
   // presence first: only an offloaded claim registers its identities
   uint32_t missing = 0;
-  for (uint64_t j = gl; j < r.n; j += W)
-    if (b.bi[(uint64_t)r.bo0 + j] >= nb) missing = 1;
+  for (uint64_t j = gl; j < r.n; j += W) {
+    const uint32_t blk = b.bi[(uint64_t)r.bo0 + j];
+    fp_out[at0 + j] = blk;  // the accepted footprint
+    if (blk >= nb) missing = 1;
+  }
   missing = group_or<W>(missing);
   const bool offloaded = !r.malformed && r.n > 0 && !missing && (uint64_t)r.n == nt;
   const uint64_t npos = (uint64_t)r.n < nt ? (uint64_t)r.n : nt;  // positions with block and tokens
@@ -875,10 +921,8 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
     const uint64_t my_h = chain_window<W>(h, m_sum, gl, gbase, steps);
     uint32_t res = 0;
     if (j < npos) {
-      reg.idn[fp_base + r.bo0 + j] = my_h;
-      if (offloaded)
-        res = id_insert(ids, my_h, b.bi[(uint64_t)r.bo0 + j], fp_base + r.bo0 + j,
-                        fp_base + r.bo0 + npos);
+      reg.idn[at0 + j] = my_h;
+      if (offloaded) res = id_insert(ids, my_h, b.bi[(uint64_t)r.bo0 + j], at0 + j, at0 + npos);
     }
     wave_count(&ctr->id_entries, res & kRegNewEntry);
   }
@@ -887,36 +931,8 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
     cnt[c] = 0;
     return;
   }
-  uint64_t s = slot_of_id(r.id, reg.mask);
-  bool inserted = false;
-  for (uint64_t probe = 0; probe <= reg.mask && !inserted; ++probe) {
-    const unsigned long long old = atomicCAS((unsigned long long*)&reg.e[s].key,
-                                             (unsigned long long)kEmptyId,
-                                             (unsigned long long)r.id);
-    if (old == kEmptyId)
-      inserted = true;
-    else
-      s = (s + 1) & reg.mask;
-  }
-  if (!inserted) {  // unreachable: the host keeps the table at most half full
-    cnt[c] = 0;
-    return;
-  }
-  RegEntry& e = reg.e[s];
-  e.state = kStAccepted | (offloaded ? kStOffloaded : 0u);
-  e.nblk = r.n;
-  e.ntok = r.ntok;
-  e.chain = h;
-  e.fpoff = fp_base + r.bo0;
-  // leading_prefix_at_least(k): the blocks holding the first k tokens
-  uint32_t pred = r.n;
-  if (b.pred) {
-    const uint64_t k = b.pred[c];
-    const uint64_t kb = k / bs + (k % bs != 0);
-    if (kb < r.n) pred = (uint32_t)kb;
-  }
-  e.pred = pred;
-  wave_count(&ctr->reg_count, true);  // the group leaders that got here
+  // the claim is registered by k_register_claims, one lane per claim, from
+  // this record (its chain hash and whether it was offloaded)
   Pend pe;
   pe.aux0 = h;
   pe.aux1 = r.n;
@@ -926,6 +942,57 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
   pe.pad = 0;
   pend[c] = pe;
   cnt[c] = offloaded ? 2 : 1;
+}
+
+// Registration of the batch's claims in the registry, one lane per claim,
+// after acceptance: a read of each probed slot first, then one CAS on the
+// key of an empty one (the batch's ids are distinct and none is registered,
+// which the duplicate check established, so a lost CAS only means another
+// claim took the slot).  Kept out of the claim-group kernel so that each
+// wave waits on its atomics once, for 64 claims.
+__global__ void __launch_bounds__(kThreads) k_register_claims(BatchDev b, RegDev reg, uint32_t bs,
+                                                              uint64_t fp_base,
+                                                              const uint64_t* __restrict__ fpo,
+                                                              const Pend* __restrict__ pend,
+                                                              Counters* __restrict__ ctr) {
+  const uint64_t c = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+  bool inserted = false;
+  if (c < b.C) {
+    const Row r = read_row(b, c);
+    if (!r.malformed) {
+      const Pend pe = pend[c];
+      uint64_t s = slot_of_id(r.id, reg.mask);
+      for (uint64_t probe = 0; probe <= reg.mask; ++probe) {
+        uint64_t k = reg.e[s].key;
+        if (k == kEmptyId)
+          k = atomicCAS((unsigned long long*)&reg.e[s].key, (unsigned long long)kEmptyId,
+                        (unsigned long long)r.id);
+        if (k == kEmptyId) {
+          inserted = true;
+          break;
+        }
+        s = (s + 1) & reg.mask;
+      }
+      // not inserted: unreachable, the host keeps the table at most half full
+      if (inserted) {
+        RegEntry& e = reg.e[s];
+        e.state = kStAccepted | ((pe.kinds >> 8) == CLAIM_EV_OFFLOADED ? kStOffloaded : 0u);
+        e.nblk = r.n;
+        e.ntok = r.ntok;
+        e.chain = pe.aux0;
+        e.fpoff = store_at(fpo, fp_base, c, r.bo0);
+        // leading_prefix_at_least(k): the blocks holding the first k tokens
+        uint32_t pred = r.n;
+        if (b.pred) {
+          const uint64_t k = b.pred[c];
+          const uint64_t kb = k / bs + (k % bs != 0);
+          if (kb < r.n) pred = (uint32_t)kb;
+        }
+        e.pred = pred;
+      }
+    }
+  }
+  wave_count(&ctr->reg_count, inserted);
 }
 
 // ----------------------------------------------------------------- restore
@@ -938,6 +1005,7 @@ template <int W>
 __global__ void __launch_bounds__(kThreads) k_register_owners(BatchDev b, RegDev reg, IdDev ids,
                                                               uint32_t nb, uint32_t bs,
                                                               uint64_t fp_base,
+                                                              const uint64_t* __restrict__ fpo,
                                                               Counters* __restrict__ ctr) {
   const uint64_t c = group_claim<W>();
   if (c >= b.C) return;
@@ -950,11 +1018,12 @@ __global__ void __launch_bounds__(kThreads) k_register_owners(BatchDev b, RegDev
   missing = group_or<W>(missing);
   const bool offloaded = !r.malformed && r.n > 0 && !missing && (uint64_t)r.n == nt;
   if (!offloaded) return;
+  const uint64_t at0 = store_at(fpo, fp_base, c, r.bo0);
   for (uint64_t j0 = 0; j0 < r.n; j0 += W) {
     const uint64_t j = j0 + gl;
     uint32_t amb = 0;
     if (j < r.n) {
-      const uint64_t key = reg.idn[fp_base + r.bo0 + j];
+      const uint64_t key = reg.idn[at0 + j];
       const IdEntry* e = id_find(ids, key);
       if (e && e->block != b.bi[(uint64_t)r.bo0 + j] &&
           !(atomicOr((uint32_t*)&e->flags, kIdAmbiguous) & kIdAmbiguous))
@@ -1730,6 +1799,7 @@ struct claim_pool {
   uint32_t* cnt = nullptr;
   Pend* pend = nullptr;
   uint32_t* tsum = nullptr;
+  uint64_t* fpo = nullptr;  // per-claim store offsets of a batch whose rows may share entries
   unsigned long long* dup_table = nullptr;
   uint64_t dup_cap = 0;
   uint64_t last_check_claims = 0;
@@ -1881,15 +1951,18 @@ int ensure_claim_scratch(claim_pool* P, uint64_t C, bool for_check) {
   dfree(P->pend);
   dfree(P->tsum);
   dfree(P->dup_table);
+  dfree(P->fpo);
   P->cnt = nullptr;
   P->pend = nullptr;
   P->tsum = nullptr;
   P->dup_table = nullptr;
+  P->fpo = nullptr;
   P->scratch_claims = 0;
   const uint64_t cap = C < 1024 ? 1024 : C;
   TRY(dalloc(&P->cnt, cap));
   TRY(dalloc(&P->pend, cap));
   TRY(dalloc(&P->tsum, (cap + kTile - 1) / kTile));
+  TRY(dalloc(&P->fpo, cap + 1));
   P->dup_cap = next_pow2(2 * cap);
   TRY(dalloc(&P->dup_table, P->dup_cap));
   P->scratch_claims = cap;
@@ -2068,7 +2141,7 @@ void free_pool(claim_pool* P) {
                   P->mark,     P->uniq,     P->slot_of, P->reg,       P->fp_store,
                   P->log,      P->ctr,      P->outcomes, P->cnt,      P->pend,
                   P->tsum,     P->dup_table, P->f_blocks, P->f_bits,   P->idn_store,
-                  P->id_table, P->id_src};
+                  P->id_table, P->id_src,    P->fpo};
   for (void* p : ptrs)
     if (p) dfree(p);
   if (P->host_ctr) (void)hipHostFree(P->host_ctr);
@@ -2238,9 +2311,7 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
   TRY(check_batch(P, b));
   HIP_TRY(hipSetDevice(P->device));
   const uint64_t C = b->num_claims;
-  if (P->reg_used_ub + C > P->max_claims || P->fp_used + b->num_refs > P->max_fp ||
-      P->log_ub + 2 * C > P->ev_cap)
-    return CLAIM_ENOSPC;
+  if (P->reg_used_ub + C > P->max_claims || P->log_ub + 2 * C > P->ev_cap) return CLAIM_ENOSPC;
   TRY(ensure_claim_scratch(P, C, false));
 
   // verdict: duplicates and the staged size, before any state changes
@@ -2255,18 +2326,33 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
   }
   TRY(select_blocks(P, b, kMarkAny));
   TRY(read_counters(P));
-  if (P->host_ctr->dup_flag) return CLAIM_EDUP;
+  if (P->host_ctr->dup_flag & kFlagDupId) return CLAIM_EDUP;
   const uint64_t U = P->host_ctr->uniq_count;
   if (staging && staging_bytes < U * P->block_bytes) return CLAIM_ENOSPC;  // nothing changed
+  // footprint and identity storage: the rows' own offsets when they are
+  // disjoint (no row runs backwards), else a run per claim
+  const uint64_t* fpo = nullptr;
+  uint64_t fp_need = b->num_refs;
+  if (P->host_ctr->dup_flag & kFlagBackwardRow) {
+    hipLaunchKernelGGL(k_footprint_offsets, dim3(1), dim3(1024), 0, P->stream, bd, P->fp_used,
+                       P->fpo);
+    HIP_TRY(hipGetLastError());
+    HIP_TRY(hipMemcpyAsync(&fp_need, P->fpo + C, sizeof(uint64_t), hipMemcpyDeviceToHost,
+                           P->stream));
+    HIP_TRY(hipStreamSynchronize(P->stream));
+    fpo = P->fpo;
+  }
+  if (P->fp_used + fp_need > P->max_fp) return CLAIM_ENOSPC;  // nothing changed
 
   // acceptance
   if (C) {
-    hipLaunchKernelGGL(k_copy_u32, dim3(grid_for(b->num_refs, 4096)), dim3(kThreads), 0, P->stream,
-                       P->fp_store + P->fp_used, b->block_ids, b->num_refs);
+    LAUNCH_GROUPED(k_accept, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->seed, P->fp_used, fpo,
+                   P->fp_store, P->ctr, P->cnt, P->pend);
+    hipLaunchKernelGGL(k_register_claims, dim3(grid_for(C, 0x7FFFFFFFu)), dim3(kThreads), 0,
+                       P->stream, bd, rd, P->bs, P->fp_used, fpo, P->pend, P->ctr);
     HIP_TRY(hipGetLastError());
-    LAUNCH_GROUPED(k_accept, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->seed, P->fp_used, P->ctr,
-                   P->cnt, P->pend);
-    LAUNCH_GROUPED(k_register_owners, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->fp_used, P->ctr);
+    LAUNCH_GROUPED(k_register_owners, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->fp_used, fpo,
+                   P->ctr);
     TRY(append_events(P, b));
   }
   // offload record; a staged offload replaces every earlier staging slot
@@ -2274,7 +2360,7 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
   TRY(launch_digest(P, P->partial, staging));
   TRY(launch_finalize(P, 0, staging != nullptr));
   TRY(read_counters(P));
-  P->fp_used += b->num_refs;
+  P->fp_used += fp_need;
   if (staging) P->staged_blocks = U;
   P->reg_used_ub = P->host_ctr->reg_count;
   P->log_ub = P->host_ctr->log_count;

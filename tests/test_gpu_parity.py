@@ -25,7 +25,7 @@ import numpy as np
 import pytest
 
 from oracle import oracle as O
-from paper_2606_01387_amd.synth import (FULL, MISSING, TINY, FaultSpec, Geometry, Workload, content,
+from paper_2606_01387_amd.synth import (FULL, MISSING, TINY, Batch, FaultSpec, Geometry, Workload, content,
                                         from_claims, make_batch, make_faults, make_requests, scaled)
 from tests.helpers import apply_flips, digests, modeled_digests, validate_lifecycle
 
@@ -348,6 +348,45 @@ def test_controls_mirrored(torch, ck):
     m.check(empty)
     m.finish()
     del m
+    free_gpu(torch)
+
+
+def test_rows_sharing_entries(torch, ck):
+    """Block rows that share block-table entries, which compressed rows
+    allow only around a row whose offsets run backwards (itself malformed):
+    each well-formed claim keeps its own accepted footprint and identities,
+    as the oracle does, through offload, restore, check and lookup."""
+    note("rows sharing block-table entries")
+    m = Mirror(torch, ck)
+    tA, tC, tE = toks(4), toks(3, 7), toks(3)
+    # A = entries [0, 4), B = [4, 1) malformed, C = [1, 4) (A's last three,
+    # other tokens), D = [4, 2) malformed, E = [2, 5) (shares two with A and C)
+    batch = Batch(claim_ids=np.array([0xA1, 0xB1, 0xC1, 0xD1, 0xE1], np.uint64),
+                  block_offsets=np.array([0, 4, 1, 4, 2, 5], np.uint32),
+                  block_ids=np.array([3, 9, 27, 30, 44], np.uint32),
+                  token_offsets=np.array([0, 64, 64, 64 + tC.size, 64 + tC.size,
+                                          64 + tC.size + tE.size], np.uint64),
+                  tokens=np.concatenate([tA, tC, tE]).astype(np.uint32))
+    m.offload(batch)
+    m.restore(batch, flips=[(44, 1000)])
+    out = m.check(batch)
+    assert out["code"].tolist() == [ck.MATERIALIZED, ck.UNKNOWN, ck.MATERIALIZED, ck.UNKNOWN,
+                                    ck.RESTORE_FAILED_FAIL_CLOSED]
+    assert int(out["first_failing_block"][4]) == 2
+    # the same claims presented as plain consecutive rows
+    out = m.check(from_claims([(0xA1, [3, 9, 27, 30], tA), (0xC1, [9, 27, 30], tC),
+                               (0xE1, [27, 30, 44], tE)]))
+    assert out["code"].tolist() == [ck.MATERIALIZED, ck.MATERIALIZED,
+                                    ck.RESTORE_FAILED_FAIL_CLOSED]
+    reqs = from_claims([(0x1, [], tA), (0x2, [], tC), (0x3, [], tE),
+                        (0x4, [], np.concatenate([tC[:32], tA[32:]]))])
+    want = m.op.lookup(reqs)
+    got = m.pool.lookup(ck.DeviceBatch(reqs))
+    for f in [n for n in O.LOOKUP_DTYPE.names if n != "pad"]:
+        assert np.array_equal(got[f], want[f]), (f, got[f].tolist(), want[f].tolist())
+    assert got["status"][:3].tolist() == [ck.LOOKUP_HIT] * 3
+    assert m.pool.identity_stats() == m.op.identity_stats()
+    m.finish()
     free_gpu(torch)
 
 
