@@ -475,3 +475,67 @@ def test_lookup_source_switching(torch, ck, batches):
     assert (got["status"] == ck.LOOKUP_HIT).sum() >= len(claims)
     del kv
     free_gpu(torch)
+
+
+@pytest.mark.parametrize("zero_at,nblocks", [(1, 3), (20, 40)])
+def test_identity_zero(torch, ck, zero_at, nblocks):
+    """A claim whose chain reaches the identity 0 at a chosen block (that
+    block's tokens solved on the lattice of the token keys, so that
+    h_{j-1} xor M_j = -gamma and h_j = mix64(0) = 0).  The library keeps that
+    identity in a table entry of its own; registration (new, then present),
+    lookups that hit, follow and stop at it (narrow and wide groups),
+    ambiguity from a second block and the check, against the oracle."""
+    from tests.chain_tokens import solve_block
+
+    note(f"identity 0 at block {zero_at} of {nblocks}")
+    m64, gamma = (1 << 64) - 1, 0x9E3779B97F4A7C15
+    w = TINY
+    g, seed, bs = w.geometry, w.seed, w.geometry.block_size
+    rng = np.random.default_rng(5000 + zero_at)
+    prefix = rng.integers(0, 32000, size=zero_at * bs, dtype=np.uint32)
+    h_prev = int(O.chain(prefix, bs, seed)[-1])
+    keys = [O.token_key(seed, k) for k in range(bs)]
+    zb = np.array(solve_block(h_prev ^ (-gamma & m64), keys, rng), np.uint32)
+    rest = rng.integers(0, 32000, size=(nblocks - zero_at - 1) * bs, dtype=np.uint32)
+    toks = np.concatenate([prefix, zb, rest])
+    assert int(O.chain(toks, bs, seed)[zero_at]) == 0
+    blocks = [int(b) for b in rng.permutation(g.num_blocks)[:nblocks]]
+    upto = (zero_at + 1) * bs
+    first = from_claims([(0x51, blocks, toks), (0x52, blocks[: zero_at + 1], toks[:upto])])
+    other = toks.copy()
+    other[upto + 3] ^= 1  # a token of the block after the identity 0
+    at_zero = toks.copy()
+    at_zero[upto - 2] ^= 1  # a token of the identity-0 block
+    reqs = from_claims([(0x101, [], toks), (0x102, [], toks[:upto]), (0x103, [], toks[: upto - 5]),
+                        (0x104, [], other), (0x105, [], at_zero), (0x106, [], toks[upto:])])
+    second = from_claims([(0x53, [(b + 1) % g.num_blocks for b in blocks[: zero_at + 1]],
+                           toks[:upto])])
+    kv = gpu_pool_tensor(torch, w)
+    host = __import__("paper_2606_01387_amd.synth", fromlist=["content"]).content.pool_host(
+        g, w.content_seed)
+    op = O.OraclePool(g.num_blocks, bs, seed)
+    with ck.Pool(g, seed, kv, max_claims=64, max_footprint=1024, event_capacity=1024) as pool:
+        pool.offload(ck.DeviceBatch(first))
+        assert op.offload(first, digests(host, w)) == O.OK
+        assert pool.identity_stats() == op.identity_stats() == (nblocks, 0)
+        got = pool.lookup(ck.DeviceBatch(reqs))
+        same_lookups(got, op.lookup(reqs))
+        assert got["status"][0] == ck.LOOKUP_HIT and int(got["chain_hash_at_hit"][1]) == 0
+        pool.restore(ck.DeviceBatch(first))
+        assert op.restore(first) == O.OK
+        pool.read(max_outcomes=1)
+        op.events(clear=True)
+        pool.check(ck.DeviceBatch(first))
+        out, ev = pool.read()
+        same_outcomes(out, op.check(first, digests(host, w)))
+        same_events(ev, op.events(clear=True))
+        assert out["code"].tolist() == [ck.MATERIALIZED] * 2
+        # the identity 0 (and the prefix before it) registered to other blocks
+        pool.offload(ck.DeviceBatch(second))
+        assert op.offload(second, digests(host, w)) == O.OK
+        assert pool.identity_stats() == op.identity_stats() == (nblocks, zero_at + 1)
+        got = pool.lookup(ck.DeviceBatch(reqs))
+        same_lookups(got, op.lookup(reqs))
+        assert got["status"][0] == ck.LOOKUP_UNKNOWN
+    del kv
+    free_gpu(torch)
