@@ -390,6 +390,48 @@ def test_rows_sharing_entries(torch, ck):
     free_gpu(torch)
 
 
+def with_shared_rows(base, first, count, rng):
+    """The base batch, then a row whose block offsets run backwards, then
+    `count` claims with fresh ids that reuse the block rows of base claims
+    first .. first+count-1 (sharing their block-table entries) and present
+    fresh tokens of the same lengths."""
+    C = base.num_claims
+    bo, to = base.block_offsets.astype(np.int64), base.token_offsets.astype(np.int64)
+    lens = to[first + 1: first + count + 1] - to[first: first + count]
+    fresh = rng.integers(0, 32000, size=int(lens.sum()), dtype=np.uint32)
+    ids = np.concatenate([base.claim_ids, [np.uint64(0xBAC0000000000000)],
+                          0xC1A0000000000000 + np.arange(count, dtype=np.uint64)]).astype(np.uint64)
+    new_bo = np.concatenate([bo, bo[first: first + count + 1]])
+    new_to = np.concatenate([to, [to[C]], to[C] + np.cumsum(lens)])
+    return Batch(claim_ids=ids, block_offsets=new_bo.astype(np.uint32), block_ids=base.block_ids,
+                 token_offsets=new_to.astype(np.uint64),
+                 tokens=np.concatenate([base.tokens, fresh]).astype(np.uint32))
+
+
+def test_shared_rows_at_scale(torch, ck):
+    """A scaled stress batch of 3000 claims followed by a backwards row and
+    500 claims that share block-table entries with 500 earlier claims but
+    present other tokens (3501 rows: several claims per thread in the
+    store-offset scan).  Whole lifecycle with real digests and lookups of
+    the shared-row claims' tokens, against the oracle."""
+    w = scaled(FULL["small-claim-stress"], 256, 3000, corrupt_rate=0.05, num_load_failed=2)
+    base = make_batch(w)
+    batch = with_shared_rows(base, 1000, 500, np.random.default_rng(7))
+    assert batch.block_offsets[3001] < batch.block_offsets[3000]  # the backwards row
+    faults = make_faults(w, batch)
+    note(f"shared rows at scale: {batch.num_claims} claims, {batch.num_refs} entries")
+    out, ev, st, want, want_ev, want_st, kv = run_both_real(torch, ck, w, batch, faults)
+    same_outcomes(out, want)
+    same_events(ev, want_ev)
+    for f in st:
+        assert np.array_equal(st[f], want_st[f]), f
+    codes = out["code"][3001:]
+    assert (codes == ck.MATERIALIZED).any() and (codes == ck.RESTORE_FAILED_FAIL_CLOSED).any()
+    assert out["code"][3000] == ck.UNKNOWN
+    del kv
+    free_gpu(torch)
+
+
 def test_scratch_growth_and_two_pools(torch, ck):
     """Two pools with different content and seeds, one on torch's stream and
     one on a stream of its own, driven in turn; pool A sees batches of 20,
