@@ -119,3 +119,88 @@ def test_attribution_and_controls(torch, ck, seed):
         if e["kind"] == ck.EV_RESTORATION_FAILED:
             assert int(e["claim_id"]) in failed_ids
     del kv
+
+
+MUTATIONS = ("none", "swap", "token", "missing", "unrecorded")
+
+
+def mutated(batch, unref, rng, bs):
+    """The claims of `batch` presented again at check time, claim c with
+    mutation c mod 5 at a seeded position (when its shape allows it):
+    two different block-table entries swapped, one token changed, one entry
+    replaced by the missing marker, or one entry replaced by a pool block
+    that was never offloaded.  Returns the presented batch and, from the
+    mutation alone, each claim's expected (code, first failing block): the
+    restore was clean, so a mutation at p makes the claim UNKNOWN at p
+    (swap: the first of the two positions; token: its token block)."""
+    from paper_2606_01387_amd.synth import MISSING, from_claims
+
+    parts, expected, kinds = [], [], []
+    for c in range(batch.num_claims):
+        cid, blks, tk = batch.claim(c)
+        blks, tk = blks.copy(), tk.copy()
+        kind, exp = MUTATIONS[c % len(MUTATIONS)], (1, 0xFFFFFFFF)  # MATERIALIZED
+        n = blks.size
+        if kind == "swap":
+            pairs = [(p, q) for p in range(n) for q in range(p + 1, n) if blks[p] != blks[q]]
+            if pairs:
+                p, q = pairs[int(rng.integers(len(pairs)))]
+                blks[p], blks[q] = blks[q], blks[p]
+                exp = (0, p)
+            else:
+                kind = "none"
+        elif kind == "token" and tk.size:
+            m = int(rng.integers(tk.size))
+            tk[m] = (int(tk[m]) + 1 + int(rng.integers(31999))) % 32000
+            exp = (0, m // bs)
+        elif kind in ("missing", "unrecorded") and n:
+            p = int(rng.integers(n))
+            blks[p] = MISSING if kind == "missing" else int(rng.choice(unref))
+            exp = (0, p)
+        else:
+            kind = "none"
+        parts.append((cid, blks, tk))
+        expected.append(exp)
+        kinds.append(kind)
+    return from_claims(parts), expected, kinds
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_mutation_controls(torch, ck, seed):
+    """Mutation controls: after a clean offload and restore, every claim is
+    checked again with one thing changed (footprint order, a token, a
+    missing entry, a block without an offload record).  Each mutated claim
+    must fail closed as UNKNOWN at the mutated position and every other
+    claim stay MATERIALIZED, with the GPU equal to the oracle bit for bit."""
+    w, batch, _ = seeded(100 + seed)
+    g = w.geometry
+    unref = np.setdiff1d(np.arange(g.num_blocks), batch.unique_blocks(g.num_blocks))
+    pres, expected, kinds = mutated(batch, unref, np.random.default_rng(seed), g.block_size)
+    print(f"mutation controls seed {seed}: " +
+          ", ".join(f"{k} {kinds.count(k)}" for k in MUTATIONS), flush=True)
+    kv = torch.empty(g.pool_bytes, dtype=torch.uint8, device="cuda")
+    content.fill_pool_gpu(kv.data_ptr(), kv.numel(), g, w.content_seed,
+                          torch.cuda.current_stream().cuda_stream)
+    db = ck.DeviceBatch(batch)
+    with ck.Pool(g, w.seed, kv, max_claims=256, max_footprint=4096, event_capacity=4096) as pool:
+        pool.offload(db)
+        pool.restore(db)
+        pool.read(max_outcomes=1)
+        pool.check(ck.DeviceBatch(pres))
+        out, ev = pool.read()
+    host = content.pool_host(g, w.content_seed)
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    op.offload(batch, digests(host, w))
+    op.restore(batch)
+    op.events(clear=True)
+    want = op.check(pres, digests(host, w))
+    for f in want.dtype.names:
+        if f != "pad":
+            assert np.array_equal(out[f], want[f]), f
+    assert [(int(a), int(b)) for a, b in zip(out["code"], out["first_failing_block"])] == expected
+    assert all(k != "none" for k, (code, _) in zip(kinds, expected) if code == 0)
+    assert sum(k != "none" for k in kinds) >= 0.7 * batch.num_claims
+    token = np.array([k == "token" for k in kinds])
+    assert (out["reasons"][token] & ck.R_TOKEN_MISMATCH).all()
+    assert len(ev) == batch.num_claims  # one terminal event each, none refused
+    del kv

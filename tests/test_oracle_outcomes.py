@@ -516,3 +516,25 @@ def test_event_log_follows_the_lifecycle_at_scale(w):
     out = op.check(b, d1)
     validate_lifecycle(b, pre, op.events(), out)
     assert len(set(out["code"].tolist())) >= 2
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_mutation_controls_oracle(seed):
+    """The oracle on the mutation controls (clean restore, then each claim
+    presented with its footprint order, a token, an entry or an offload
+    record changed): every outcome equals the one the mutation alone
+    predicts (UNKNOWN at the mutated position, else MATERIALIZED)."""
+    from paper_2606_01387_amd.synth import content
+    from tests.test_gpu_attribution import MUTATIONS, mutated, seeded
+
+    w, batch, _ = seeded(100 + seed)
+    g = w.geometry
+    unref = np.setdiff1d(np.arange(g.num_blocks), batch.unique_blocks(g.num_blocks))
+    pres, expected, kinds = mutated(batch, unref, np.random.default_rng(seed), g.block_size)
+    assert all(kinds.count(k) >= 10 for k in MUTATIONS)
+    host = content.pool_host(g, w.content_seed)
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    assert op.offload(batch, digests(host, w)) == O.OK
+    assert op.restore(batch) == O.OK
+    out = op.check(pres, digests(host, w))
+    assert [(int(a), int(b)) for a, b in zip(out["code"], out["first_failing_block"])] == expected
