@@ -51,7 +51,9 @@
  *
  * Parity pins (checked by the CPU tests): the published SplitMix64 outputs
  * for seed 0; D(0) = 0, D(e_i) = k_i, additivity, the exact single-bit-flip
- * delta +-2^beta * k_i; exhaustive single flips on a small block; four
+ * delta +-2^beta * k_i; exhaustive single flips on a small block; head-shard
+ * digests that add up to the block digest over a partition of the heads and
+ * equal the digest of the block with the other heads zeroed; four
  * token blocks whose chain h_0 .. h_3 is the published SplitMix64 stream
  * for seed 0; shared token prefixes give equal chain hashes; outcome
  * enumeration over every ok/failed/missing assignment of short claims, with
@@ -100,6 +102,32 @@ uint64_t le_word(const uint8_t* p) {
 uint64_t block_digest(const uint8_t* canon, uint64_t nbytes, uint64_t seed) {
   uint64_t d = 0;
   for (uint64_t i = 0; i < nbytes / 8; ++i) d += le_word(canon + 8 * i) * kv_key(seed, i);
+  return d;
+}
+
+/* Digest of a head shard of a block (a pool that holds KV heads
+ * [first_head, first_head + heads) of blocks whose full width is heads_total
+ * heads, as under tensor parallelism by KV head).  The full block's canonical
+ * bytes are its planes' chunks in order, each chunk [token][head][row_bytes];
+ * the shard's own canonical bytes are the same with only its heads.  Each
+ * shard word keeps the key of its position in the full block, so this is the
+ * full block's digest restricted to the shard's words, and the shards of a
+ * block add up to its digest.  row_bytes (one head's bytes of one token) is a
+ * multiple of 8. */
+uint64_t shard_digest(const uint8_t* canon, uint32_t planes, uint32_t block_size, uint32_t heads,
+                      uint32_t row_bytes, uint32_t heads_total, uint32_t first_head,
+                      uint64_t seed) {
+  const uint64_t row_words = row_bytes / 8;
+  uint64_t d = 0;
+  for (uint64_t p = 0; p < planes; ++p)
+    for (uint64_t t = 0; t < block_size; ++t)
+      for (uint64_t h = 0; h < heads; ++h)
+        for (uint64_t w = 0; w < row_words; ++w) {
+          const uint64_t local_word = ((p * block_size + t) * heads + h) * row_words + w;
+          const uint64_t full_word =
+              ((p * block_size + t) * heads_total + first_head + h) * row_words + w;
+          d += le_word(canon + 8 * local_word) * kv_key(seed, full_word);
+        }
   return d;
 }
 
@@ -293,6 +321,12 @@ uint64_t orc_token_key(uint64_t seed, uint64_t m) { return token_key(seed, m); }
 
 uint64_t orc_block_digest(const uint8_t* canon, uint64_t nbytes, uint64_t seed) {
   return block_digest(canon, nbytes, seed);
+}
+
+uint64_t orc_shard_digest(const uint8_t* canon, uint32_t planes, uint32_t block_size,
+                          uint32_t heads, uint32_t row_bytes, uint32_t heads_total,
+                          uint32_t first_head, uint64_t seed) {
+  return shard_digest(canon, planes, block_size, heads, row_bytes, heads_total, first_head, seed);
 }
 
 uint64_t orc_token_multilinear(const uint32_t* tok, uint64_t n, uint64_t seed) {

@@ -113,6 +113,7 @@ def lib() -> ctypes.CDLL:
             ("orc_kv_key", [u64, u64], u64),
             ("orc_token_key", [u64, u64], u64),
             ("orc_block_digest", [vp, u64, u64], u64),
+            ("orc_shard_digest", [vp, u32, u32, u32, u32, u32, u32, u64], u64),
             ("orc_token_multilinear", [vp, u64, u64], u64),
             ("orc_chain", [vp, u64, u32, u64, vp], u64),
             ("orc_canonical_block", [vp, u32, u32, u64, u32, vp], ctypes.c_int),
@@ -176,6 +177,18 @@ def block_digest(canon: np.ndarray, seed: int) -> int:
     c = _arr(canon, np.uint8)
     assert c.size % 8 == 0
     return lib().orc_block_digest(_ptr(c), c.size, seed)
+
+
+def shard_digest(canon: np.ndarray, seed: int, planes: int, block_size: int, heads: int,
+                 row_bytes: int, heads_total: int, first_head: int) -> int:
+    """Digest of a head shard of a block: its words with the keys of their
+    positions in the full block (``canon``: the shard's own canonical
+    bytes, planes chunks of [token][head][row_bytes])."""
+    c = _arr(canon, np.uint8)
+    assert c.size == planes * block_size * heads * row_bytes and row_bytes % 8 == 0
+    assert first_head + heads <= heads_total
+    return lib().orc_shard_digest(_ptr(c), planes, block_size, heads, row_bytes, heads_total,
+                                  first_head, seed)
 
 
 def token_multilinear(tokens, seed: int) -> int:

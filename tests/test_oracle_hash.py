@@ -159,6 +159,44 @@ def test_two_sign_bit_flips_can_cancel():
     assert O.block_digest(block, 5) == d0
 
 
+# ------------------------------------------------------------- head shards
+
+
+def _full_and_shard(full, first, heads):
+    """(full canonical bytes, the shard's own canonical bytes) of a block
+    given as [plane][token][head][row byte]."""
+    return full.reshape(-1), np.ascontiguousarray(full[:, :, first:first + heads, :]).reshape(-1)
+
+
+@pytest.mark.parametrize("heads", [1, 2, 4, 8])
+def test_head_shards_add_up_to_the_block_digest(heads):
+    """Under tensor parallelism by KV head each GPU holds a slice of every
+    block's heads.  Shard digests (each word keyed by its position in the
+    full block) over a partition of the heads add up to the full block's
+    digest, and each equals the full digest of the block with every other
+    head's bytes zeroed (linearity: zero words contribute nothing)."""
+    rng = np.random.default_rng(40 + heads)
+    planes, bs, total, row = 3, 4, 8, 24
+    seed = 777
+    full = rng.integers(0, 256, size=(planes, bs, total, row), dtype=np.uint8)
+    d_full = O.block_digest(full.reshape(-1), seed)
+    acc = 0
+    for first in range(0, total, heads):
+        _, shard = _full_and_shard(full, first, heads)
+        d = O.shard_digest(shard, seed, planes, bs, heads, row, total, first)
+        masked = np.zeros_like(full)
+        masked[:, :, first:first + heads, :] = full[:, :, first:first + heads, :]
+        assert d == O.block_digest(masked.reshape(-1), seed)
+        acc = (acc + d) & M64
+    assert acc == d_full
+
+
+def test_unsharded_shard_digest_is_the_block_digest():
+    rng = np.random.default_rng(48)
+    full = rng.integers(0, 256, size=(2, 16, 2, 128), dtype=np.uint8)
+    assert O.shard_digest(full.reshape(-1), 5, 2, 16, 2, 128, 2, 0) == O.block_digest(full.reshape(-1), 5)
+
+
 # ----------------------------------------------------------- canonical layout
 
 
