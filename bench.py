@@ -61,7 +61,7 @@ def cpu_baseline(w, batch, faults, sample_gb: float):
 
     from oracle import oracle as O
     from paper_2606_01387_amd.synth import content
-    from tests.helpers import modeled_digests
+    from tests.helpers import canon_digest, modeled_digests
 
     g = w.geometry
     uniq = batch.unique_blocks(g.num_blocks)
@@ -84,7 +84,7 @@ def cpu_baseline(w, batch, faults, sample_gb: float):
                     c[bit // 8] ^= np.uint8(1 << (bit % 8))
             t0 = time.perf_counter()
             for b, c in zip(part, canon):
-                d1[b] = O.block_digest(c, w.seed)
+                d1[b] = canon_digest(c, w)
             t_digest += time.perf_counter() - t0
             for b in part:  # a changed block's d0 is already its real pre-flip digest
                 if b not in changed:
@@ -161,9 +161,9 @@ def main() -> int:
     import torch
 
     from paper_2606_01387_amd import claimkv as ck
-    from paper_2606_01387_amd.synth import FULL, content, make_batch, make_faults, make_requests
+    from paper_2606_01387_amd.synth import FULL, SHARDS, content, make_batch, make_faults, make_requests
 
-    w = FULL[args.workload]
+    w = FULL[args.workload] if args.workload in FULL else SHARDS[args.workload]
     g = w.geometry
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -343,6 +343,8 @@ def main() -> int:
             "unique_blocks": U,
             "claims": C,
             "block_refs": batch.num_refs,
+            **({"kv_heads": f"{g.first_kv_head}..{g.first_kv_head + g.num_kv_heads - 1} of "
+                            f"{g.total_kv_heads} (head shard)"} if g.sharded else {}),
             "tokens": batch.num_tokens,
             "corrupted_blocks": int(faults.flip_blocks.size),
         },

@@ -123,7 +123,19 @@ typedef struct claim_pool claim_pool;
  * planes_per_layer = 2, p = layer for an MLA latent (planes_per_layer = 1);
  * a chunk is block_size x num_kv_heads x head_dim elements of elem_bytes
  * bytes in [token][head][dim] order, and must be a multiple of 16 bytes.
- * Element bytes are never interpreted (bf16 and fp8 are hashed as bytes). */
+ * Element bytes are never interpreted (bf16 and fp8 are hashed as bytes).
+ *
+ * A pool may hold a head shard of every block, as one GPU does under tensor
+ * parallelism by KV head: heads [first_kv_head, first_kv_head +
+ * num_kv_heads) of blocks whose full width is total_kv_heads heads (its
+ * chunks hold only its own heads, [token][head][dim] as above).  Each of its
+ * 64-bit words keeps the key of its position in the full block's canonical
+ * bytes, so a shard's block digest is the full digest's sum over the shard's
+ * words, and the digests of a block's shards add up, mod 2^64, to the
+ * digest of the whole block.  head_dim * elem_bytes must then be a multiple
+ * of 8.  total_kv_heads = 0 (or num_kv_heads, with first_kv_head = 0) is a
+ * pool of whole blocks; first_kv_head + num_kv_heads > total_kv_heads is
+ * EINVAL. */
 typedef struct claim_pool_desc {
   uint32_t num_layers;
   uint32_t planes_per_layer; /* 1 or 2 */
@@ -140,6 +152,8 @@ typedef struct claim_pool_desc {
   uint64_t max_claims;       /* registry capacity (claims ever accepted) */
   uint64_t max_footprint;    /* block-table entries ever accepted */
   uint64_t event_capacity;   /* event records held between outcomes_read calls */
+  uint32_t total_kv_heads;   /* head shard: KV heads of the full block (0: num_kv_heads) */
+  uint32_t first_kv_head;    /* head shard: full-block index of this pool's first head */
 } claim_pool_desc;
 
 /* A claim batch in compressed rows.  All arrays are device memory owned by

@@ -60,7 +60,8 @@ class PoolDesc(ctypes.Structure):
                 ("seed", ctypes.c_uint64), ("kv_base", ctypes.c_void_p),
                 ("kv_bytes", ctypes.c_uint64), ("stream", ctypes.c_void_p),
                 ("max_claims", ctypes.c_uint64), ("max_footprint", ctypes.c_uint64),
-                ("event_capacity", ctypes.c_uint64)]
+                ("event_capacity", ctypes.c_uint64), ("total_kv_heads", ctypes.c_uint32),
+                ("first_kv_head", ctypes.c_uint32)]
 
 
 class CBatch(ctypes.Structure):
@@ -84,7 +85,7 @@ class CTiming(ctypes.Structure):
                 ("claims_ms", ctypes.c_double), ("events_ms", ctypes.c_double)]
 
 
-assert ctypes.sizeof(PoolDesc) == 88 and ctypes.sizeof(CBatch) == 72
+assert ctypes.sizeof(PoolDesc) == 96 and ctypes.sizeof(CBatch) == 72
 assert OUTCOME_DTYPE.itemsize == 64 and EVENT_DTYPE.itemsize == 40 and LOOKUP_DTYPE.itemsize == 40
 
 
@@ -197,7 +198,8 @@ class Pool:
     """A claim pool over a caller-owned KV tensor on the current GPU.
 
     ``geometry`` has num_layers, planes_per_layer, block_size, num_kv_heads,
-    head_dim, elem_bytes and num_blocks (e.g. ``synth.Geometry``); ``kv`` is a
+    head_dim, elem_bytes and num_blocks, and for a head shard total_kv_heads
+    and first_kv_head (e.g. ``synth.Geometry``); ``kv`` is a
     contiguous CUDA tensor of at least planes x num_blocks x chunk bytes laid
     out [plane][block][chunk]."""
 
@@ -221,7 +223,9 @@ class Pool:
             flags=(POOL_TIMING if timing else 0) | (POOL_STAGE_TIMING if stage_timing else 0), seed=seed,
             kv_base=kv.data_ptr(), kv_bytes=kv.numel() * kv.element_size(),
             stream=stream.cuda_stream, max_claims=max_claims, max_footprint=max_footprint,
-            event_capacity=event_capacity)
+            event_capacity=event_capacity,
+            total_kv_heads=getattr(geometry, "total_kv_heads", 0),
+            first_kv_head=getattr(geometry, "first_kv_head", 0))
         h = ctypes.c_void_p()
         with torch.cuda.device(kv.device):
             _check(lib().claim_pool_create(ctypes.byref(d), ctypes.byref(h)), "claim_pool_create")

@@ -676,13 +676,34 @@ __device__ __forceinline__ uint64_t dpp_wave_sum64(uint64_t v) {
 
 // RAGGED: the chunk's last segment is partly past its end (masked slots).
 // STAGE: also copy the words to staging (offload with staging).
+// Position of a pool word in its block's full canonical bytes: the index of
+// its key.  A pool that holds every head has word q of plane p's chunk at
+// p * chunk_words + q.  A head shard (tensor parallel by KV head) holds heads
+// [first, first + heads) of blocks with `total` heads: its chunk is rows
+// r = t * heads + h ([token][head]) of row_words words, and row r sits at
+// row t * total + first + h of the full chunk.  So a shard's digest is the
+// full digest's sum over the shard's words, and shards add up to it.
+struct KeyMap {
+  uint32_t chunk_words;  // this pool's chunk
+  uint32_t row_words;    // one head's words of one token (shards only)
+  uint32_t heads, total, first;
+  __device__ __forceinline__ uint64_t at(uint32_t p, uint32_t q) const {
+    if (heads == total) return (uint64_t)p * chunk_words + q;
+    const uint32_t r = q / row_words, w = q - r * row_words;
+    const uint32_t t = r / heads, h = r - t * heads;
+    const uint64_t full_chunk = (uint64_t)(chunk_words / heads) * total;
+    return (uint64_t)p * full_chunk + ((uint64_t)t * total + first + h) * row_words + w;
+  }
+};
+
 template <int LPW, bool RAGGED, bool STAGE>
 __global__ void __launch_bounds__(kThreads) k_digest(const u32x2* __restrict__ pool, uint32_t nb,
                                                      uint32_t chunk_words, uint32_t planes,
                                                      uint32_t segs, uint32_t groups,
                                                      const uint32_t* __restrict__ uniq,
                                                      const Counters* __restrict__ ctr,
-                                                     uint64_t seed, uint64_t* __restrict__ partial,
+                                                     uint64_t seed, KeyMap km,
+                                                     uint64_t* __restrict__ partial,
                                                      u32x2* __restrict__ staging) {
   __shared__ uint64_t ring[kThreads / 64][kRing];
   const uint32_t lane = threadIdx.x & 63;
@@ -701,7 +722,7 @@ __global__ void __launch_bounds__(kThreads) k_digest(const u32x2* __restrict__ p
 #pragma unroll
   for (int k = 0; k < LPW; ++k) {
     const uint32_t q = q0 + 64u * k;
-    const uint64_t key = stream_output(seed, (uint64_t)p * chunk_words + q) | 1ull;
+    const uint64_t key = stream_output(seed, km.at(p, q)) | 1ull;
     const bool ok = !RAGGED || q < chunk_words;
     klo[k] = ok ? (uint32_t)key : 0u;  // a masked slot contributes 0
     khi[k] = ok ? (uint32_t)(key >> 32) : 0u;
@@ -1767,6 +1788,7 @@ struct claim_pool {
 
   uint32_t planes = 0, bs = 0, nb = 0;
   uint64_t chunk_bytes = 0, chunk_vecs = 0, block_bytes = 0, seed = 0;
+  KeyMap kmap{};  // key positions (head shards)
   void* kv = nullptr;
 
   int lpw = 32;
@@ -2013,7 +2035,7 @@ int launch_digest_lpw(claim_pool* P, uint64_t* partial, void* staging, int* wgs_
   const dim3 grid(P->pgs * P->groups), block(kThreads);
 #define GO(R, S)                                                                                \
   hipLaunchKernelGGL((k_digest<LPW, R, S>), grid, block, 0, P->stream, pool, P->nb, cw, P->planes, \
-                     P->segs, P->groups, P->uniq, P->ctr, P->seed, partial, st)
+                     P->segs, P->groups, P->uniq, P->ctr, P->seed, P->kmap, partial, st)
   if (ragged) {
     if (staging) GO(true, true); else GO(true, false);
   } else {
@@ -2213,6 +2235,13 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
   const uint64_t chunk = (uint64_t)d->block_size * d->num_kv_heads * d->head_dim * d->elem_bytes;
   if (chunk % 16 || planes > 0xFFFFFFFFull || chunk / 16 > 0xFFFFFFFFull) return CLAIM_EINVAL;
   if (d->max_claims > (1ull << 40) || d->max_footprint > (1ull << 40)) return CLAIM_EINVAL;
+  // a head shard: heads [first, first + num_kv_heads) of total_kv_heads,
+  // each head's row a whole number of 64-bit words
+  const uint32_t total_heads = d->total_kv_heads ? d->total_kv_heads : d->num_kv_heads;
+  const uint64_t row_bytes = (uint64_t)d->head_dim * d->elem_bytes;
+  if ((uint64_t)d->first_kv_head + d->num_kv_heads > total_heads) return CLAIM_EINVAL;
+  if (total_heads != d->num_kv_heads && row_bytes % 8) return CLAIM_EINVAL;
+  if ((uint64_t)d->block_size * total_heads * row_bytes / 8 > 0xFFFFFFFFull) return CLAIM_EINVAL;
   const long double need = (long double)planes * d->num_blocks * chunk;
   if (need > (long double)d->kv_bytes) return CLAIM_EINVAL;
 
@@ -2239,6 +2268,11 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     P->block_bytes = planes * chunk;
     P->seed = d->seed;
     P->kv = d->kv_base;
+    P->kmap.chunk_words = (uint32_t)(chunk / 8);
+    P->kmap.row_words = (uint32_t)(row_bytes / 8);
+    P->kmap.heads = d->num_kv_heads;
+    P->kmap.total = total_heads;
+    P->kmap.first = d->first_kv_head;
     if ((rc = choose_digest_shape(P))) break;
 
     const uint64_t nb = d->num_blocks;

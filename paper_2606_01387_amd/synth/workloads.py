@@ -28,6 +28,20 @@ class Geometry:
     head_dim: int  # latent width for MLA
     elem_bytes: int  # 2 = bf16, 1 = fp8 e4m3 (bytes are never interpreted)
     num_blocks: int
+    # a head shard (tensor parallel by KV head): this pool holds heads
+    # [first_kv_head, first_kv_head + num_kv_heads) of blocks that have
+    # total_kv_heads heads; 0 = whole blocks
+    total_kv_heads: int = 0
+    first_kv_head: int = 0
+
+    @property
+    def sharded(self) -> bool:
+        return self.total_kv_heads not in (0, self.num_kv_heads)
+
+    @property
+    def row_bytes(self) -> int:
+        """One head's bytes of one token."""
+        return self.head_dim * self.elem_bytes
 
     @property
     def planes(self) -> int:
@@ -141,6 +155,17 @@ MLA_FP8 = _w(
 )
 
 FULL = {w.name: w for w in (TINY, LLAMA3_8B, LLAMA3_70B, STRESS, MLA_FP8)}
+
+# One GPU's share of the 70B pool under tensor parallelism by KV head over 8
+# GPUs: the same blocks and claims, each block holding one of the 8 heads
+# (640 KiB per block, 4 KiB chunks, a 13.1 GB pool).  Its digests are the
+# head shard's part of the full blocks' digests.
+LLAMA3_70B_TP8 = replace(
+    LLAMA3_70B, name="llama3-70b-tp8-shard",
+    geometry=Geometry(80, 2, 16, 1, 128, 2, 20000, total_kv_heads=8, first_kv_head=0),
+    notes="one GPU's head shard of the 70B pool under 8-way tensor parallelism")
+
+SHARDS = {w.name: w for w in (LLAMA3_70B_TP8,)}
 
 
 def scaled(w: Workload, num_blocks: int, num_claims: int, **kw) -> Workload:

@@ -25,7 +25,7 @@ import numpy as np
 import pytest
 
 from oracle import oracle as O
-from paper_2606_01387_amd.synth import (FULL, MISSING, TINY, Batch, FaultSpec, Geometry, Workload, content,
+from paper_2606_01387_amd.synth import (FULL, MISSING, SHARDS, TINY, Batch, FaultSpec, Geometry, Workload, content,
                                         from_claims, make_batch, make_faults, make_requests, scaled)
 from tests.helpers import apply_flips, digests, modeled_digests, validate_lifecycle
 
@@ -158,6 +158,9 @@ SCALED = [
     MAX_BS_SHORT,
     MAX_BS_LONG,
     MIN_BS,
+    # one GPU's head shard of the 70B pool under 8-way tensor parallelism
+    scaled(SHARDS["llama3-70b-tp8-shard"], 24, 40, corrupt_rate=0.1, missing_claim_rate=0.1,
+           num_load_failed=1),
 ]
 
 
@@ -348,6 +351,44 @@ def test_controls_mirrored(torch, ck):
     m.check(empty)
     m.finish()
     del m
+    free_gpu(torch)
+
+
+@pytest.mark.parametrize("heads", [1, 2])
+def test_head_shards_add_up(torch, ck, heads):
+    """A pool of 4-head blocks cut into head shards of 1 or 2 heads (each
+    shard pool holding its heads' bytes of every block, as one GPU does
+    under tensor parallelism by KV head): every shard's offload digests
+    equal the oracle's shard digests, and for every block the shards'
+    digests add up, mod 2^64, to the digest the whole pool records."""
+    note(f"head shards of {heads}")
+    gf = Geometry(2, 2, 16, 4, 64, 2, 64)
+    wf = replace(TINY, name="four-heads", geometry=gf)
+    batch = make_batch(wf)
+    kv = gpu_pool_tensor(torch, wf)
+    host = content.pool_host(gf, wf.content_seed)
+    caps = capacities(batch)
+    with ck.Pool(gf, wf.seed, kv, **caps) as pool:
+        pool.offload(ck.DeviceBatch(batch))
+        whole = pool.block_state()["d_off"]
+    ref = batch.unique_blocks(gf.num_blocks)
+    assert np.array_equal(whole[ref], digests(host, wf)[ref])
+    view = kv.view(gf.planes, gf.num_blocks, gf.block_size, 4, gf.row_bytes)
+    host_view = host.reshape(gf.planes, gf.num_blocks, gf.block_size, 4, gf.row_bytes)
+    acc = np.zeros(gf.num_blocks, dtype=np.uint64)
+    for first in range(0, 4, heads):
+        gs = replace(gf, num_kv_heads=heads, total_kv_heads=4, first_kv_head=first)
+        ws = replace(wf, geometry=gs)
+        shard = view[:, :, :, first:first + heads, :].contiguous().view(-1)
+        with ck.Pool(gs, ws.seed, shard, **caps) as pool:
+            pool.offload(ck.DeviceBatch(batch))
+            d = pool.block_state()["d_off"]
+        host_shard = np.ascontiguousarray(host_view[:, :, :, first:first + heads, :]).reshape(-1)
+        assert np.array_equal(d[ref], digests(host_shard, ws)[ref]), first
+        acc += d  # wraps mod 2^64
+        del shard
+    assert np.array_equal(acc, whole)
+    del kv
     free_gpu(torch)
 
 
@@ -596,9 +637,10 @@ def test_staged_round_trip(torch, ck, w, where):
 # ----------------------------------------------------------- full-size workloads
 
 
-@pytest.mark.parametrize("name", ["llama3-8b", "llama3-70b", "small-claim-stress", "mla-fp8"])
+@pytest.mark.parametrize("name", ["llama3-8b", "llama3-70b", "small-claim-stress", "mla-fp8",
+                                  "llama3-70b-tp8-shard"])
 def test_full_size_parity(torch, ck, name):
-    w = FULL[name]
+    w = FULL[name] if name in FULL else SHARDS[name]
     g = w.geometry
     batch = make_batch(w)
     faults = make_faults(w, batch)
