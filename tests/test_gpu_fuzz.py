@@ -1,0 +1,76 @@
+"""Differential test of the library against the oracle over seeded
+irregular lifecycles (tests/fuzz_cases.py): four pool geometries (one a head
+shard), offload batches with empty, long, missing, out-of-range, malformed
+and entry-sharing rows, reserved ids and predicates, shared and
+duplicate-owned identities, faults, a partial restore, a check batch that
+presents the claims again reordered, repeated and changed, and lookups.
+Every status, outcome field, event, per-block digest, lookup field and
+identity count must equal the oracle's."""
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2606_01387_amd.synth import content
+from tests.fuzz_cases import SEEDS, make_case
+from tests.helpers import apply_flips, digests
+from tests.test_gpu_parity import free_gpu, gpu_pool_tensor, same_events, same_outcomes
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    return t
+
+
+@pytest.fixture(scope="module")
+def ck():
+    from paper_2606_01387_amd import claimkv
+
+    claimkv.lib()
+    return claimkv
+
+
+@pytest.mark.parametrize("seed", SEEDS)
+def test_fuzz_lifecycle(torch, ck, seed):
+    case = make_case(seed)
+    w = case.w
+    g = w.geometry
+    print(f"fuzz seed {seed}: heads {g.num_kv_heads}/{g.total_kv_heads or g.num_kv_heads}, "
+          f"offload {[b.num_claims for b in case.offload]}, check {case.check.num_claims}, "
+          f"lookup {case.lookup.num_claims}", flush=True)
+    host = content.pool_host(g, w.content_seed)
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    kv = gpu_pool_tensor(torch, w)
+    with ck.Pool(g, w.seed, kv, max_claims=256, max_footprint=4096, event_capacity=4096) as pool:
+        for b in case.offload:
+            want = op.offload(b, digests(host, w))
+            try:
+                pool.offload(ck.DeviceBatch(b))
+                got = ck.OK
+            except ck.ClaimError as e:
+                got = e.status
+            assert got == want
+        pool.restore(ck.DeviceBatch(case.restore), faults=case.faults)
+        assert op.restore(case.restore, case.faults.load_failed) == O.OK
+        _, ev_pre = pool.read(max_outcomes=1)
+        same_events(ev_pre, op.events(clear=True))
+        pool.check(ck.DeviceBatch(case.check))
+        out, ev = pool.read()
+        same_outcomes(out, op.check(case.check, digests(apply_flips(host, w, case.faults), w)))
+        same_events(ev, op.events(clear=True))
+        st = pool.block_state()
+        for f, v in op.block_state().items():
+            assert np.array_equal(st[f], v), f
+        got = pool.lookup(ck.DeviceBatch(case.lookup))
+        want = op.lookup(case.lookup)
+        for f in want.dtype.names:
+            if f != "pad":
+                assert np.array_equal(got[f], want[f]), f
+        assert pool.identity_stats() == op.identity_stats()
+    del kv
+    free_gpu(torch)

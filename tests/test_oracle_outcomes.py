@@ -538,3 +538,27 @@ def test_mutation_controls_oracle(seed):
     assert op.restore(batch) == O.OK
     out = op.check(pres, digests(host, w))
     assert [(int(a), int(b)) for a, b in zip(out["code"], out["first_failing_block"])] == expected
+
+
+def test_fuzz_cases_run_on_the_oracle():
+    """The irregular lifecycles the GPU differential test replays run on the
+    oracle with every offload accepted, and mix all three outcomes."""
+    from paper_2606_01387_amd.synth import content
+    from tests.fuzz_cases import SEEDS, make_case
+
+    codes = np.zeros(3, dtype=np.int64)
+    for seed in SEEDS:
+        case = make_case(seed)
+        w, g = case.w, case.w.geometry
+        host = content.pool_host(g, w.content_seed)
+        op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+        for b in case.offload:
+            assert op.offload(b, digests(host, w)) == O.OK
+        assert op.restore(case.restore, case.faults.load_failed) == O.OK
+        op.events(clear=True)
+        out = op.check(case.check, digests(apply_flips(host, w, case.faults), w))
+        assert out.size == case.check.num_claims
+        failed = int((out["code"] == O.RESTORE_FAILED_FAIL_CLOSED).sum())
+        assert op.events().size == out.size + failed
+        codes += np.bincount(out["code"], minlength=3)
+    assert (codes > 20).all(), codes
