@@ -28,6 +28,7 @@ GEOMETRIES = [
 @dataclass
 class Case:
     w: Workload
+    size: str
     offload: list  # batches offloaded in turn
     restore: Batch
     faults: FaultSpec
@@ -39,11 +40,14 @@ def _tokens(rng, n):
     return rng.integers(0, 32000, size=n, dtype=np.uint32)
 
 
-def _claims(rng, g, count, ids):
+SIZES = {"short": [0, 1, 1, 2, 3, 4, 6, 9], "long": [0, 3, 20, 40, 70, 120], "many": [0, 1, 1, 2, 3]}
+
+
+def _claims(rng, g, count, ids, size="short"):
     bs = g.block_size
     parts = []
     for cid in ids[:count]:
-        n = int(rng.choice([0, 1, 1, 2, 3, 4, 6, 9]))
+        n = int(rng.choice(SIZES[size]))
         blks = rng.integers(0, g.num_blocks, size=n).astype(np.int64)
         for j in range(n):
             u = rng.random()
@@ -75,7 +79,7 @@ def _bend(rng, b: Batch) -> Batch:
                  np.clip(to, 0, None).astype(np.uint64), b.tokens)
 
 
-def _present(rng, g, accepted, extra_ids):
+def _present(rng, g, accepted, extra_ids, size):
     """The claims again, reordered, some repeated, some changed (a token, an
     entry, a cut or an extension), plus claims never accepted."""
     parts = []
@@ -95,7 +99,7 @@ def _present(rng, g, accepted, extra_ids):
         parts.append((cid, blks, tk))
         if rng.random() < 0.1:
             parts.append((cid, blks, tk))  # the same claim presented twice
-    parts += _claims(rng, g, len(extra_ids), extra_ids)
+    parts += _claims(rng, g, len(extra_ids), extra_ids, size)
     return from_claims(parts)
 
 
@@ -105,11 +109,16 @@ def make_case(seed: int) -> Case:
     w = Workload(name=f"fuzz-{seed}", geometry=g, seed=int(rng.integers(0, 2**63)),
                  num_claims=0, length=TINY.length, sharing=TINY.sharing, corrupt_rate=0.0,
                  gen_seed=seed, content_seed=int(rng.integers(0, 2**31)))
-    ids = rng.permutation(np.arange(1, 400, dtype=np.uint64))
+    # most cases are short claims; some have long claims (the wide group
+    # paths) or thousands of claims (the tiled event scan)
+    size = {6: "long", 7: "many"}.get(seed % 8, "short")
+    n_first = {"short": int(rng.integers(0, 30)), "long": int(rng.integers(1, 12)),
+               "many": int(rng.integers(4200, 6000))}[size]
+    ids = rng.permutation(np.arange(1, 20000, dtype=np.uint64))
     if rng.random() < 0.3:
         ids[int(rng.integers(0, 10))] = RESERVED
-    first = _claims(rng, g, int(rng.integers(0, 30)), ids[:40])
-    second = _claims(rng, g, int(rng.integers(0, 12)), ids[40:60])
+    first = _claims(rng, g, n_first, ids[:n_first], size)
+    second = _claims(rng, g, int(rng.integers(0, 12)), ids[10000:10012], size)
     # a later claim with an earlier claim's tokens (shared identities; with
     # another block row, duplicate ownership)
     if first and rng.random() < 0.7:
@@ -117,7 +126,7 @@ def make_case(seed: int) -> Case:
         blks = src[1].copy()
         if blks.size and rng.random() < 0.5:
             blks[0] = int(rng.integers(0, g.num_blocks))
-        second.append((int(ids[60]), blks, src[2].copy()))
+        second.append((int(ids[10100]), blks, src[2].copy()))
     b1 = _bend(rng, from_claims(first))
     b1.predicate_tokens = (rng.integers(0, 80, size=b1.num_claims).astype(np.uint64)
                            if rng.random() < 0.4 else None)
@@ -129,11 +138,19 @@ def make_case(seed: int) -> Case:
                       rng.integers(0, g.num_blocks, size=int(rng.integers(0, 3))).astype(np.uint32))
     keep = len(accepted) if rng.random() < 0.8 else int(rng.integers(0, len(accepted) + 1))
     restore = from_claims(accepted[:keep])
-    check = _bend(rng, _present(rng, g, accepted, ids[100:104]))
+    check = _bend(rng, _present(rng, g, accepted, ids[10200:10204], size))
     reqs = [(int(i), [], p[2][: int(rng.integers(0, p[2].size + 1))] if rng.random() < 0.3 else p[2])
-            for i, p in zip(ids[200:], accepted)]
-    lookup = _bend(rng, from_claims(reqs + [(int(ids[300]), [], _tokens(rng, 3 * g.block_size))]))
-    return Case(w, [b1, b2], restore, flips, check, lookup)
+            for i, p in zip(ids[12000:], accepted)]
+    lookup = _bend(rng, from_claims(reqs + [(int(ids[10300]), [], _tokens(rng, 3 * g.block_size))]))
+    return Case(w, size, [b1, b2], restore, flips, check, lookup)
+
+
+
+def capacities(case: Case) -> dict:
+    claims = sum(b.num_claims for b in case.offload)
+    refs = sum(b.num_refs for b in case.offload)
+    return dict(max_claims=2 * claims + 64, max_footprint=4 * refs + 256,
+                event_capacity=4 * (claims + case.check.num_claims) + 1024)
 
 
 SEEDS = range(160)

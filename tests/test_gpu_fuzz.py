@@ -12,7 +12,7 @@ import pytest
 
 from oracle import oracle as O
 from paper_2606_01387_amd.synth import content
-from tests.fuzz_cases import SEEDS, make_case
+from tests.fuzz_cases import SEEDS, capacities, make_case
 from tests.helpers import apply_flips, digests
 from tests.test_gpu_parity import free_gpu, gpu_pool_tensor, same_events, same_outcomes
 
@@ -40,13 +40,13 @@ def test_fuzz_lifecycle(torch, ck, seed):
     case = make_case(seed)
     w = case.w
     g = w.geometry
-    print(f"fuzz seed {seed}: heads {g.num_kv_heads}/{g.total_kv_heads or g.num_kv_heads}, "
+    print(f"fuzz seed {seed} ({case.size}): heads {g.num_kv_heads}/{g.total_kv_heads or g.num_kv_heads}, "
           f"offload {[b.num_claims for b in case.offload]}, check {case.check.num_claims}, "
           f"lookup {case.lookup.num_claims}", flush=True)
     host = content.pool_host(g, w.content_seed)
     op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
     kv = gpu_pool_tensor(torch, w)
-    with ck.Pool(g, w.seed, kv, max_claims=256, max_footprint=4096, event_capacity=4096) as pool:
+    with ck.Pool(g, w.seed, kv, **capacities(case)) as pool:
         for b in case.offload:
             want = op.offload(b, digests(host, w))
             try:
