@@ -29,6 +29,7 @@ GEOMETRIES = [
 class Case:
     w: Workload
     size: str
+    staged: bool  # the second offload stages its blocks, the restore copies them back
     offload: list  # batches offloaded in turn
     restore: Batch
     faults: FaultSpec
@@ -142,8 +143,22 @@ def make_case(seed: int) -> Case:
     reqs = [(int(i), [], p[2][: int(rng.integers(0, p[2].size + 1))] if rng.random() < 0.3 else p[2])
             for i, p in zip(ids[12000:], accepted)]
     lookup = _bend(rng, from_claims(reqs + [(int(ids[10300]), [], _tokens(rng, 3 * g.block_size))]))
-    return Case(w, size, [b1, b2], restore, flips, check, lookup)
+    return Case(w, size, seed % 3 == 0, [b1, b2], restore, flips, check, lookup)
 
+
+
+def well_formed_blocks(b: Batch, num_blocks: int) -> np.ndarray:
+    """In-range blocks referenced by the batch's well-formed rows (the
+    blocks an offload stages and a restore copies back), ascending."""
+    bo, to = b.block_offsets.astype(np.int64), b.token_offsets.astype(np.int64)
+    out = []
+    for c in range(b.num_claims):
+        if (int(b.claim_ids[c]) == RESERVED or bo[c] > bo[c + 1] or bo[c + 1] > b.num_refs
+                or to[c] > to[c + 1] or to[c + 1] > b.num_tokens):
+            continue
+        blks = b.block_ids[bo[c]:bo[c + 1]]
+        out.append(blks[blks < num_blocks])
+    return np.unique(np.concatenate(out)) if out else np.zeros(0, np.uint32)
 
 
 def capacities(case: Case) -> dict:

@@ -2,17 +2,19 @@
 irregular lifecycles (tests/fuzz_cases.py): four pool geometries (one a head
 shard), offload batches with empty, long, missing, out-of-range, malformed
 and entry-sharing rows, reserved ids and predicates, shared and
-duplicate-owned identities, faults, a partial restore, a check batch that
-presents the claims again reordered, repeated and changed, and lookups.
-Every status, outcome field, event, per-block digest, lookup field and
-identity count must equal the oracle's."""
+duplicate-owned identities, faults, a partial restore (in a third of the
+cases from device staging written by the second offload, after the staged
+blocks' device copies are zeroed), a check batch that presents the claims
+again reordered, repeated and changed, and lookups.  The pool's bytes after
+the restore must equal the host model, and every status, outcome field,
+event, per-block digest, lookup field and identity count the oracle's."""
 
 import numpy as np
 import pytest
 
 from oracle import oracle as O
 from paper_2606_01387_amd.synth import content
-from tests.fuzz_cases import SEEDS, capacities, make_case
+from tests.fuzz_cases import SEEDS, capacities, make_case, well_formed_blocks
 from tests.helpers import apply_flips, digests
 from tests.test_gpu_parity import free_gpu, gpu_pool_tensor, same_events, same_outcomes
 
@@ -40,28 +42,45 @@ def test_fuzz_lifecycle(torch, ck, seed):
     case = make_case(seed)
     w = case.w
     g = w.geometry
-    print(f"fuzz seed {seed} ({case.size}): heads {g.num_kv_heads}/{g.total_kv_heads or g.num_kv_heads}, "
+    print(f"fuzz seed {seed} ({case.size}{', staged' if case.staged else ''}): heads {g.num_kv_heads}/{g.total_kv_heads or g.num_kv_heads}, "
           f"offload {[b.num_claims for b in case.offload]}, check {case.check.num_claims}, "
           f"lookup {case.lookup.num_claims}", flush=True)
     host = content.pool_host(g, w.content_seed)
     op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
     kv = gpu_pool_tensor(torch, w)
+    staging, restored = None, host.copy()
     with ck.Pool(g, w.seed, kv, **capacities(case)) as pool:
-        for b in case.offload:
+        for i, b in enumerate(case.offload):
             want = op.offload(b, digests(host, w))
+            if case.staged and i == len(case.offload) - 1:
+                staged = well_formed_blocks(b, g.num_blocks)
+                staging = torch.empty(max(1, staged.size) * g.block_bytes, dtype=torch.uint8,
+                                      device="cuda")
             try:
-                pool.offload(ck.DeviceBatch(b))
+                pool.offload(ck.DeviceBatch(b), staging=staging)
                 got = ck.OK
             except ck.ClaimError as e:
                 got = e.status
             assert got == want
-        pool.restore(ck.DeviceBatch(case.restore), faults=case.faults)
+        if case.staged:
+            # the staged blocks' device copies are gone; the restore copies
+            # back those its well-formed rows reference
+            pool.stream.synchronize()
+            idx = torch.as_tensor(staged.astype(np.int64), device="cuda")
+            kv.view(g.planes, g.num_blocks, g.chunk_bytes)[:, idx, :] = 0
+            torch.cuda.synchronize()
+            lost = np.setdiff1d(staged, well_formed_blocks(case.restore, g.num_blocks))
+            restored.reshape(g.planes, g.num_blocks, g.chunk_bytes)[:, lost, :] = 0
+        pool.restore(ck.DeviceBatch(case.restore), staging=staging, faults=case.faults)
         assert op.restore(case.restore, case.faults.load_failed) == O.OK
+        restored = apply_flips(restored, w, case.faults)
+        pool.stream.synchronize()
+        assert np.array_equal(kv.cpu().numpy(), restored)
         _, ev_pre = pool.read(max_outcomes=1)
         same_events(ev_pre, op.events(clear=True))
         pool.check(ck.DeviceBatch(case.check))
         out, ev = pool.read()
-        same_outcomes(out, op.check(case.check, digests(apply_flips(host, w, case.faults), w)))
+        same_outcomes(out, op.check(case.check, digests(restored, w)))
         same_events(ev, op.events(clear=True))
         st = pool.block_state()
         for f, v in op.block_state().items():
@@ -72,5 +91,5 @@ def test_fuzz_lifecycle(torch, ck, seed):
             if f != "pad":
                 assert np.array_equal(got[f], want[f]), f
         assert pool.identity_stats() == op.identity_stats()
-    del kv
+    del kv, staging
     free_gpu(torch)
