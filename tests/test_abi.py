@@ -93,12 +93,28 @@ def _desc(**kw):
     dict(num_kv_heads=0), dict(head_dim=0), dict(elem_bytes=0), dict(num_blocks=0),
     dict(num_blocks=0xFFFFFFFF), dict(kv_base=None), dict(kv_base=0x10008),
     dict(kv_bytes=(1 << 20) - 1), dict(max_claims=0), dict(event_capacity=0), dict(flags=0x80),
+    # head shards: past the full block's heads, or head rows that are not whole words
+    dict(total_kv_heads=4, first_kv_head=3), dict(first_kv_head=1), dict(total_kv_heads=1),
+    dict(head_dim=2, elem_bytes=1, total_kv_heads=4),
 ])
 def test_pool_create_rejects_bad_descriptions(L, bad):
     d = _desc(**bad)
     h = ctypes.c_void_p()
     rc = L.claim_pool_create(ctypes.byref(d), ctypes.byref(h))
     assert rc == ck.EINVAL and not h.value
+
+
+@pytest.mark.parametrize("ok", [dict(total_kv_heads=8, first_kv_head=6), dict(total_kv_heads=2),
+                                dict(total_kv_heads=0, first_kv_head=0)])
+def test_pool_create_accepts_head_shards(L, ok):
+    """Valid head-shard descriptions pass validation (without a GPU the
+    call then fails in the runtime, never with EINVAL)."""
+    d = _desc(**ok)
+    h = ctypes.c_void_p()
+    rc = L.claim_pool_create(ctypes.byref(d), ctypes.byref(h))
+    assert rc != ck.EINVAL
+    if rc == ck.OK:
+        L.claim_pool_destroy(h)
 
 
 def test_chunk_must_be_multiple_of_16_bytes(L):
