@@ -1100,8 +1100,13 @@ __global__ void __launch_bounds__(kThreads) k_restore_claims(BatchDev b, RegDev 
   cnt[c] = 0;
   if (r.malformed) return;
   const int64_t s = reg_find(reg, r.id);
-  if (s < 0 || !(reg.e[s].state & kStOffloaded)) return;
-  atomicOr(&reg.e[s].state, kStRestoreRequired);
+  if (s < 0) return;
+  const uint32_t state = reg.e[s].state;
+  if (!(state & kStOffloaded)) return;
+  // a plain store: every lane that finds this claim (a batch may present
+  // it twice) stores the same value, and nothing else changes the state
+  // while this kernel runs
+  if (!(state & kStRestoreRequired)) reg.e[s].state = state | kStRestoreRequired;
   Pend pe;
   pe.aux0 = reg.e[s].nblk;
   pe.aux1 = 0;
