@@ -9,6 +9,7 @@ computes the method's arithmetic."""
 
 from __future__ import annotations
 
+import os
 from dataclasses import dataclass
 
 import numpy as np
@@ -168,4 +169,5 @@ def capacities(case: Case) -> dict:
                 event_capacity=4 * (claims + case.check.num_claims) + 1024)
 
 
-SEEDS = range(160)
+# CLAIMKV_FUZZ_SEEDS widens a one-off run; the suite replays the first 160
+SEEDS = range(int(os.environ.get("CLAIMKV_FUZZ_SEEDS", "160")))
