@@ -139,6 +139,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama3-8b")
+    ap.add_argument("--geometry", default=None,
+                    help="layers,planes_per_layer,block_size,kv_heads,head_dim,elem_bytes,num_blocks: "
+                         "the workload's claims and faults over a pool of this geometry")
     ap.add_argument("--cpu-sample-gb", type=float, default=20.0,
                     help="block bytes the oracle digests for the CPU baseline (whole unique set "
                          "if it is smaller)")
@@ -164,6 +167,13 @@ def main() -> int:
     from paper_2606_01387_amd.synth import FULL, SHARDS, content, make_batch, make_faults, make_requests
 
     w = FULL[args.workload] if args.workload in FULL else SHARDS[args.workload]
+    if args.geometry:
+        from dataclasses import replace
+
+        from paper_2606_01387_amd.synth import Geometry
+
+        dims = [int(x) for x in args.geometry.split(",")]
+        w = replace(w, name=f"{w.name}-claims-on-{'x'.join(map(str, dims))}", geometry=Geometry(*dims))
     g = w.geometry
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
