@@ -23,8 +23,17 @@
  *        blocking_claim_ids (section 1 running example; section 7 event list
  *        E0..E14 and witness paths A and B);
  *      * only failures of the claim's own blocks count (section 7 path C,
- *        Table 9 last row); a reported load failure is not undone by later
- *        correct bytes (Table 9, fallback recompute row);
+ *        Table 9 last row);
+ *      * offload records are the claim's own: at acceptance a claim keeps the
+ *        digest of each of its blocks, and its check compares against those,
+ *        so another claim's later offload of a shared block neither satisfies
+ *        nor changes it (section 5 storage_restorability row: store and load
+ *        name the same claim; a recompute must not be relabelled as
+ *        restoration; Table 9 wrong-claim and fallback-recompute rows);
+ *      * a reported load failure fails every claim that recorded the block
+ *        before the report, and nothing clears it for them: a later offload
+ *        of the block (a recompute stored by another claim) is that claim's
+ *        own record (Table 9, fallback-recompute row);
  *      * ambiguity yields no claim outcome (Table 2, last rule; Table 5, last
  *        row): missing registry, unstable ids, cache-identity mismatch,
  *        partial streams and duplicate ownership all give UNKNOWN here.
@@ -44,10 +53,13 @@
  *    registers (h_j -> physical block) for every offloaded claim; equal
  *    registrations are stored once, and one identity registered to two
  *    different blocks is duplicate ownership, which makes the identity
- *    ambiguous.  A lookup reports the longest leading run of a request's
- *    token blocks whose identities are registered and unambiguous.  The
- *    check compares each h_j of the presented tokens with the one accepted
- *    for that position.
+ *    ambiguous.  A block holds the identity of its latest registration; an
+ *    identity whose block was since registered under another identity is
+ *    stale (the block no longer holds that prefix).  A lookup reports the
+ *    longest leading run of a request's token blocks whose identities are
+ *    registered, unambiguous and still held by their block.  The check
+ *    compares each h_j of the presented tokens with the one accepted for
+ *    that position.
  *
  * Parity pins (checked by the CPU tests): the published SplitMix64 outputs
  * for seed 0; D(0) = 0, D(e_i) = k_i, additivity, the exact single-bit-flip
@@ -58,9 +70,13 @@
  * for seed 0; shared token prefixes give equal chain hashes; outcome
  * enumeration over every ok/failed/missing assignment of short claims, with
  * every predicate length; memcmp brute force of the failing set on the tiny
- * pool; brute-force walks over token-prefix tuples for the identity table
- * and the lookup; the paper's event-order templates and its 448-token and
- * 17-token examples.
+ * pool; a claim ledger (each claim's own stored copy of its blocks, failures
+ * reported after it, compared by memcmp) over random lifecycles with several
+ * offloads, block rewrites and recomputes; brute-force walks over
+ * token-prefix tuples, with the prefix each block holds, for the identity
+ * table and the lookup; event payloads against values computed without the
+ * lifecycle (counts, reason bits, the exact single-flip digest delta); the
+ * paper's event-order templates and its 448-token and 17-token examples.
  */
 
 #include <cstdint>
@@ -251,6 +267,11 @@ struct Claim {
   uint64_t chain_hash;
   uint32_t pred_blocks; /* leading positions the predicate covers */
   std::vector<uint64_t> identity; /* accepted h_j for j < min(blocks, token blocks) */
+  /* the claim's own offload record: the digest of the block at each
+   * in-range footprint position when the claim was offloaded (0 where the
+   * entry is missing), and the generation of that offload */
+  std::vector<uint64_t> digest;
+  uint64_t generation;
 };
 
 /* One registered cache identity: the physical block that holds it, and
@@ -260,12 +281,20 @@ struct Identity {
   bool ambiguous;
 };
 
+/* Pool state.  Every offload and every restore call takes the next
+ * generation, so generations order the lifecycle calls.  Per block:
+ * d_off = the digest recorded by the block's latest offload, valid_off =
+ * some claim holds an offload record of it, d_res = its digest at the last
+ * check that re-digested it, fail_gen = the generation of its latest
+ * reported load failure (0 = none), holder = the identity of its latest
+ * registration (meaningful once the block has been registered). */
 struct Pool {
   uint32_t num_blocks;
   uint32_t block_size;
   uint64_t seed;
-  std::vector<uint64_t> d_off, d_res;
-  std::vector<uint8_t> valid_off, load_failed;
+  uint64_t generation;
+  std::vector<uint64_t> d_off, d_res, fail_gen, holder;
+  std::vector<uint8_t> valid_off;
   std::unordered_map<uint64_t, Claim> registry;
   std::unordered_map<uint64_t, Identity> identities;
   std::vector<orc_event> log;
@@ -376,10 +405,12 @@ void* orc_pool_new(uint32_t num_blocks, uint32_t block_size, uint64_t seed) {
   p->num_blocks = num_blocks;
   p->block_size = block_size;
   p->seed = seed;
+  p->generation = 0;
   p->d_off.assign(num_blocks, 0);
   p->d_res.assign(num_blocks, 0);
+  p->fail_gen.assign(num_blocks, 0);
+  p->holder.assign(num_blocks, 0);
   p->valid_off.assign(num_blocks, 0);
-  p->load_failed.assign(num_blocks, 0);
   p->next_seq = 0;
   return p;
 }
@@ -390,11 +421,13 @@ void orc_pool_free(void* handle) { delete static_cast<Pool*>(handle); }
  * current bytes (only entries referenced by the batch are read).
  *
  * The whole batch is refused (ORC_EDUP, nothing changes, no event) if a
- * non-reserved id occurs twice in it or is already registered.  Otherwise,
- * in batch order, each well-formed claim is registered (ACCEPTED), every
- * in-range block it references gets an offload record, and a claim whose
- * footprint is non-empty, fully present and consistent with its token count
- * is marked OFFLOADED. */
+ * non-reserved id occurs twice in it or is already registered.  Otherwise
+ * the call takes the next generation and, in batch order, each well-formed
+ * claim is registered (ACCEPTED) with its own offload record (the digest of
+ * every in-range block it references, and this generation), every such
+ * block is marked as recorded, and a claim whose footprint is non-empty,
+ * fully present and consistent with its token count is marked OFFLOADED
+ * and registers its identities. */
 int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num_tokens,
                 const uint64_t* ids, const uint32_t* blk_off, const uint32_t* blk_ids,
                 const uint64_t* tok_off, const uint32_t* tokens, const uint64_t* predicate_tokens,
@@ -410,6 +443,7 @@ int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
     seen[ids[c]] = 1;
   }
 
+  p->generation += 1;
   for (uint32_t c = 0; c < num_claims; ++c) {
     if (malformed(bt, c)) continue;
     uint32_t n = blk_off[c + 1] - blk_off[c];
@@ -419,6 +453,10 @@ int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
     Claim cl;
     cl.state = ST_ACCEPTED;
     cl.footprint.assign(fp, fp + n);
+    cl.generation = p->generation;
+    cl.digest.assign(n, 0);
+    for (uint32_t j = 0; j < n; ++j)
+      if (fp[j] < p->num_blocks) cl.digest[j] = digest_now[fp[j]];
     cl.n_tokens = ntok;
     std::vector<uint64_t> h;
     cl.chain_hash = chain(tokens + tok_off[c], ntok, p->block_size, p->seed, &h);
@@ -442,14 +480,13 @@ int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
       }
       p->d_off[b] = digest_now[b];
       p->valid_off[b] = 1;
-      p->load_failed[b] = 0;
     }
     if (all_present && n == ceil_div(ntok, p->block_size)) {
       p->registry[ids[c]].state |= ST_OFFLOADED;
       append_event(p, ids[c], EV_OFFLOADED, kNone, kNone, n);
       /* register h_j -> block for each position of the offloaded claim: an
        * equal registration is stored once; a different block for the same
-       * identity is duplicate ownership */
+       * identity is duplicate ownership; the block now holds h_j */
       for (uint32_t j = 0; j < n; ++j) {
         auto it = p->identities.find(h[j]);
         if (it == p->identities.end()) {
@@ -460,15 +497,17 @@ int orc_offload(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
         } else if (it->second.block != fp[j]) {
           it->second.ambiguous = true;
         }
+        p->holder[fp[j]] = h[j];
       }
     }
   }
   return ORC_OK;
 }
 
-/* Restore: mark the listed blocks as reported load failures, then, in batch
- * order, move every well-formed, registered and offloaded claim to
- * RESTORE_REQUIRED.  (Bit flips act on bytes, see orc_apply_flip.) */
+/* Restore: take the next generation and record it as the latest reported
+ * load failure of each listed block, then, in batch order, move every
+ * well-formed, registered and offloaded claim to RESTORE_REQUIRED.  (Bit
+ * flips act on bytes, see orc_apply_flip.) */
 int orc_restore(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num_tokens,
                 const uint64_t* ids, const uint32_t* blk_off, const uint32_t* blk_ids,
                 const uint64_t* tok_off, const uint32_t* tokens, uint32_t num_failed,
@@ -477,7 +516,8 @@ int orc_restore(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
   Batch bt = {num_claims, num_refs, num_tokens, ids, blk_off, blk_ids, tok_off, tokens};
   for (uint32_t f = 0; f < num_failed; ++f)
     if (failed_blocks[f] >= p->num_blocks) return ORC_EINVAL;
-  for (uint32_t f = 0; f < num_failed; ++f) p->load_failed[failed_blocks[f]] = 1;
+  p->generation += 1;
+  for (uint32_t f = 0; f < num_failed; ++f) p->fail_gen[failed_blocks[f]] = p->generation;
 
   for (uint32_t c = 0; c < num_claims; ++c) {
     if (malformed(bt, c)) continue;
@@ -491,10 +531,14 @@ int orc_restore(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t n
 
 /* Check: record restored digests, then decide each claim's outcome.
  *
- * The restored digest is refreshed for every in-range, offloaded block
- * listed anywhere in the batch's block table; only well-formed rows are
- * evaluated, so a malformed row can refresh a block's digest but never
- * contribute to an outcome.
+ * The restored digest is refreshed for every in-range block with an offload
+ * record that a well-formed row of the batch references.  Each position of
+ * a registered claim is judged against the claim's own offload record of
+ * the block at that position: a reported load failure later than the
+ * claim's offload, or a restored digest different from the claim's own
+ * offload digest, is a restoration failure there.  A position whose entry
+ * differs from the accepted one (or lies past the accepted footprint) holds
+ * no record of the claim.
  *
  * Every failure or ambiguity is a key (class << 32 | position); class 0 is
  * an ambiguity (no claim outcome), class 1 a restoration failure, and a
@@ -511,11 +555,13 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
   Pool* p = static_cast<Pool*>(handle);
   Batch bt = {num_claims, num_refs, num_tokens, ids, blk_off, blk_ids, tok_off, tokens};
 
-  /* restored digests of every offloaded block listed in the batch's block
-   * table (all num_refs entries, whichever rows hold them) */
-  for (uint64_t i = 0; i < num_refs; ++i) {
-    uint32_t b = blk_ids[i];
-    if (b < p->num_blocks && p->valid_off[b]) p->d_res[b] = digest_now[b];
+  /* restored digests of the recorded blocks the well-formed rows reference */
+  for (uint32_t c = 0; c < num_claims; ++c) {
+    if (malformed(bt, c)) continue;
+    for (uint32_t i = blk_off[c]; i < blk_off[c + 1]; ++i) {
+      uint32_t b = blk_ids[i];
+      if (b < p->num_blocks && p->valid_off[b]) p->d_res[b] = digest_now[b];
+    }
   }
 
   for (uint32_t c = 0; c < num_claims; ++c) {
@@ -542,6 +588,7 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
     uint64_t nt = h.size();
     uint32_t pred = n;       /* predicate coverage: accepted value, else the whole claim */
     uint32_t intact = n;     /* first position with any problem, else n */
+    const Claim* cl = nullptr;
 
     if (!(reasons & R_MALFORMED)) {
       auto it = p->registry.find(ids[c]);
@@ -549,43 +596,43 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
         reasons |= R_NOT_ACCEPTED;
         if (none_key < best) best = none_key;
       } else {
-        const Claim& cl = it->second;
-        pred = cl.pred_blocks < n ? cl.pred_blocks : n;
-        if (!(cl.state & ST_OFFLOADED)) {
+        cl = &it->second;
+        pred = cl->pred_blocks < n ? cl->pred_blocks : n;
+        if (!(cl->state & ST_OFFLOADED)) {
           reasons |= R_NOT_OFFLOADED;
           if (none_key < best) best = none_key;
         }
-        if (!(cl.state & ST_RESTORE_REQUIRED)) {
+        if (!(cl->state & ST_RESTORE_REQUIRED)) {
           reasons |= R_NO_RESTORE;
           if (none_key < best) best = none_key;
         }
         /* cache identity position by position: a token block whose chain
          * hash differs from the accepted one, and the block where the token
          * counts part; the whole-claim hash remains a claim-level check */
-        uint64_t npos = nt < cl.identity.size() ? nt : cl.identity.size();
+        uint64_t npos = nt < cl->identity.size() ? nt : cl->identity.size();
         for (uint64_t j = 0; j < npos; ++j) {
-          if (h[j] != cl.identity[j]) {
+          if (h[j] != cl->identity[j]) {
             reasons |= R_TOKEN_MISMATCH;
             uint64_t k = ((uint64_t)0 << 32) | j;
             if (k < best) best = k;
             if (j < intact) intact = (uint32_t)j;
           }
         }
-        if (cl.n_tokens != ntok) {
-          uint64_t q = (ntok < cl.n_tokens ? ntok : cl.n_tokens) / p->block_size;
+        if (cl->n_tokens != ntok) {
+          uint64_t q = (ntok < cl->n_tokens ? ntok : cl->n_tokens) / p->block_size;
           reasons |= R_TOKEN_MISMATCH;
           uint64_t k = ((uint64_t)0 << 32) | q;
           if (k < best) best = k;
           if (q < intact) intact = (uint32_t)q;
         }
-        if (cl.chain_hash != chain_hash) {
+        if (cl->chain_hash != chain_hash) {
           reasons |= R_TOKEN_MISMATCH;
           if (none_key < best) best = none_key;
         }
-        uint32_t na = (uint32_t)cl.footprint.size();
+        uint32_t na = (uint32_t)cl->footprint.size();
         uint32_t common = n < na ? n : na;
         for (uint32_t j = 0; j < common; ++j) {
-          if (fp[j] != cl.footprint[j]) {
+          if (fp[j] != cl->footprint[j]) {
             reasons |= R_FOOTPRINT_MISMATCH;
             uint64_t k = ((uint64_t)0 << 32) | j;
             if (k < best) best = k;
@@ -617,14 +664,20 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
           uint64_t k = ((uint64_t)0 << 32) | j;
           if (k < best) best = k;
           if (j < intact) intact = j;
-        } else if (!p->valid_off[b]) {
+        } else if (!cl) {
+          /* a claim that was never accepted holds no offload record
+           * (NOT_ACCEPTED already says so) */
+        } else if (j >= cl->footprint.size() || cl->footprint[j] != b) {
+          /* the claim recorded no offload of this block at this position */
           reasons |= R_NO_OFFLOAD_RECORD;
           uint64_t k = ((uint64_t)0 << 32) | j;
           if (k < best) best = k;
           if (j < intact) intact = j;
         } else {
-          bool lf = p->load_failed[b] != 0;
-          bool mm = p->d_res[b] != p->d_off[b];
+          /* the claim's own record: a failure reported after its offload,
+           * or restored bytes whose digest differs from its own */
+          bool lf = p->fail_gen[b] > cl->generation;
+          bool mm = p->d_res[b] != cl->digest[j];
           if ((lf || mm) && j < intact) intact = j;
           if (j >= pred) {
             /* beyond the predicate: the claimed prefix is intact */
@@ -659,7 +712,7 @@ int orc_check(void* handle, uint32_t num_claims, uint64_t num_refs, uint64_t num
       o.first_failing_block = j;
       o.phys_block = j < n ? fp[j] : kNone;
       if (cls == 1) {
-        o.expected_digest = p->d_off[fp[j]];
+        o.expected_digest = cl->digest[j];
         o.observed_digest = p->d_res[fp[j]];
       }
       if (j != kNone && j < nt) o.chain_hash_at_fail = h[j];
@@ -691,6 +744,9 @@ void orc_events(void* handle, orc_event* out) {
 /* Drop the events read so far (sequence numbers keep counting). */
 void orc_events_clear(void* handle) { static_cast<Pool*>(handle)->log.clear(); }
 
+/* Per-block state: the latest offload digest, the last restored digest,
+ * whether some claim recorded the block, and whether a load failure of it
+ * has ever been reported. */
 void orc_block_state(void* handle, uint64_t* d_off, uint64_t* d_res, uint8_t* valid_off,
                      uint8_t* load_failed) {
   Pool* p = static_cast<Pool*>(handle);
@@ -698,18 +754,16 @@ void orc_block_state(void* handle, uint64_t* d_off, uint64_t* d_res, uint8_t* va
     if (d_off) d_off[b] = p->d_off[b];
     if (d_res) d_res[b] = p->d_res[b];
     if (valid_off) valid_off[b] = p->valid_off[b];
-    if (load_failed) load_failed[b] = p->load_failed[b];
+    if (load_failed) load_failed[b] = p->fail_gen[b] != 0;
   }
 }
 
-/* Registry state of one claim id: returns the state bits, or 0 if the id is
- * not registered. */
-/* Predicate coverage (leading positions) recorded for a claim at
- * acceptance, or 0xFFFFFFFF if the id is not registered. */
 /* Lookup (the reuse lookup of section 7, E1, which reports how many of a
  * request's tokens hit offloaded claim footprints).  For each request row,
  * in order: the chain h_0 .. h_{nt-1} of its tokens; hit = the number of
- * leading token blocks whose identity is registered and unambiguous.  The
+ * leading token blocks whose identity is registered, unambiguous and still
+ * held by its block (a block registered since under another identity no
+ * longer holds this prefix: the identity is stale and does not hit).  The
  * lookup stops at the first block that is not; if that block's identity is
  * registered but ambiguous (duplicate ownership), the result is UNKNOWN
  * rather than a shorter hit, as is a malformed row (reserved id, or token
@@ -747,6 +801,7 @@ int orc_lookup(void* handle, uint32_t num_requests, uint64_t num_tokens, const u
         ambiguous = true;
         break;
       }
+      if (p->holder[it->second.block] != h[hit]) break; /* stale */
       ++hit;
     }
     r.hit_blocks = (uint32_t)hit;
@@ -777,12 +832,16 @@ void orc_identity_stats(void* handle, uint64_t* entries, uint64_t* ambiguous) {
   *ambiguous = a;
 }
 
+/* Predicate coverage (leading positions) recorded for a claim at
+ * acceptance, or 0xFFFFFFFF if the id is not registered. */
 uint32_t orc_claim_predicate(void* handle, uint64_t id) {
   Pool* p = static_cast<Pool*>(handle);
   auto it = p->registry.find(id);
   return it == p->registry.end() ? kNone : it->second.pred_blocks;
 }
 
+/* Registry state of one claim id: returns the state bits, or 0 if the id is
+ * not registered. */
 uint32_t orc_claim_state(void* handle, uint64_t id) {
   Pool* p = static_cast<Pool*>(handle);
   auto it = p->registry.find(id);

@@ -88,26 +88,37 @@ def test_identity_position_matches_token_comparison():
             assert out["intact_blocks"] == min(want, n)
 
 
-def registered_prefixes(claims):
+def registered_prefixes(claims, holders=None):
     """prefix (tuple of token blocks 0..j) -> set of physical blocks at j,
-    over the offloaded claims, by direct comparison."""
+    over the offloaded claims, by direct comparison.  With ``holders`` (a
+    dict), also record the prefix each physical block holds: that of its
+    latest registration, in offload order (claims in order, positions in
+    order)."""
     reg = {}
     for _, blks, tk in claims:
         tb = blocks_of(tk)
         for j in range(len(blks)):
             reg.setdefault(tuple(tb[: j + 1]), set()).add(int(blks[j]))
+            if holders is not None:
+                holders[int(blks[j])] = tuple(tb[: j + 1])
     return reg
 
 
-def brute_lookup(reg, tk):
+def brute_lookup(reg, tk, holders=None):
+    """Leading token blocks whose prefix is registered to exactly one block
+    that (with ``holders``) still holds that prefix; a prefix registered to
+    two blocks stops the walk as ambiguous."""
     tb = blocks_of(tk)
     hit = 0
     while hit < len(tb):
-        owners = reg.get(tuple(tb[: hit + 1]))
+        prefix = tuple(tb[: hit + 1])
+        owners = reg.get(prefix)
         if owners is None:
             return hit, None, False
         if len(owners) > 1:
             return hit, None, True
+        if holders is not None and holders[next(iter(owners))] != prefix:
+            return hit, None, False  # the block was registered since under another prefix
         hit += 1
     return hit, None, False
 
@@ -137,7 +148,8 @@ def test_lookup_matches_prefix_brute_force():
     claims = make_family_claims()
     op = O.OraclePool(NB, BS, SEED)
     assert op.offload(from_claims(claims), D0) == O.OK
-    reg = registered_prefixes(claims)
+    holders = {}
+    reg = registered_prefixes(claims, holders)
     entries, ambiguous = op.identity_stats()
     assert entries == len(reg)
     assert ambiguous == sum(1 for v in reg.values() if len(v) > 1) == 1
@@ -150,7 +162,7 @@ def test_lookup_matches_prefix_brute_force():
     batch = from_claims([(1000 + i, [], t) for i, t in enumerate(reqs)])
     got = op.lookup(batch)
     for i, t in enumerate(reqs):
-        hit, _, amb = brute_lookup(reg, t)
+        hit, _, amb = brute_lookup(reg, t, holders)
         r = got[i]
         assert r["request_id"] == 1000 + i
         assert r["hit_blocks"] == hit, (i, t.size)
@@ -227,3 +239,84 @@ def test_reuse_lookup_of_the_running_example_hits_448_tokens():
     longer = np.concatenate([tk, RNG.integers(1, 32000, size=37, dtype=np.uint32)])
     r = op.lookup(from_claims([(0x449, [], longer)]))[0]
     assert (r["status"], r["hit_tokens"]) == (O.LK_PARTIAL, 448)
+
+
+def test_reassigned_block_no_longer_hits_its_old_identity():
+    """Claim 1 offloads block 5 holding prefix P; claim 2 then offloads block
+    5 holding prefix Q.  Block 5 no longer holds P: a lookup of P must not
+    report a hit on it (section 7 E1 reports what is resident; Table 2, an
+    ambiguous or stale mapping must not be served), while Q hits.  A third
+    claim storing P in block 5 again makes P hit and Q stale."""
+    p_tok, q_tok = rand_tokens(BS), rand_tokens(BS)
+    op = O.OraclePool(NB, BS, SEED)
+    assert op.offload(from_claims([(1, [5], p_tok)]), D0) == O.OK
+    r = op.lookup(from_claims([(10, [], p_tok)]))[0]
+    assert (r["status"], r["hit_blocks"], r["last_block"]) == (O.LK_HIT, 1, 5)
+    assert op.offload(from_claims([(2, [5], q_tok)]), D0) == O.OK
+    assert op.identity_stats() == (2, 0)
+    got = op.lookup(from_claims([(10, [], p_tok), (11, [], q_tok)]))
+    assert (got[0]["status"], got[0]["hit_blocks"], got[0]["last_block"]) == (O.LK_MISS, 0, O.NONE32)
+    assert (got[1]["status"], got[1]["hit_blocks"], got[1]["last_block"]) == (O.LK_HIT, 1, 5)
+    # the same within one batch: the later row holds the block
+    op2 = O.OraclePool(NB, BS, SEED)
+    op2.offload(from_claims([(1, [5], p_tok), (2, [5], q_tok)]), D0)
+    got = op2.lookup(from_claims([(10, [], p_tok), (11, [], q_tok)]))
+    assert got["status"].tolist() == [O.LK_MISS, O.LK_HIT]
+    # P stored in block 5 again
+    assert op.offload(from_claims([(3, [5], p_tok.copy())]), D0) == O.OK
+    got = op.lookup(from_claims([(10, [], p_tok), (11, [], q_tok)]))
+    assert got["status"].tolist() == [O.LK_HIT, O.LK_MISS]
+    # a longer prefix through a reassigned block stops there
+    tk = rand_tokens(3 * BS)
+    op3 = O.OraclePool(NB, BS, SEED)
+    op3.offload(from_claims([(1, [0, 1, 2], tk)]), D0)
+    op3.offload(from_claims([(2, [1], rand_tokens(BS))]), D0)
+    r = op3.lookup(from_claims([(10, [], tk)]))[0]
+    assert (r["status"], r["hit_blocks"], r["last_block"]) == (O.LK_PARTIAL, 1, 0)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_lookup_with_block_reuse_matches_brute_force(seed):
+    """Claims drawn over only a few physical blocks, so that blocks are
+    registered under many prefixes, offloaded in one to three batches; every
+    lookup equals the brute-force walk over token-prefix tuples with block
+    holders (the latest registration of each block)."""
+    rng = np.random.default_rng(500 + seed)
+    nphys = 6
+    roots = [rand_tokens(int(rng.integers(1, 6 * BS))) for _ in range(3)]
+    claims = []
+    for k in range(14):
+        root = roots[int(rng.integers(len(roots)))]
+        cut = int(rng.integers(0, root.size + 1))
+        tk = np.concatenate([root[:cut], rand_tokens(int(rng.integers(0, 3 * BS)))])
+        if tk.size == 0:
+            tk = rand_tokens(1)
+        n = -(-tk.size // BS)
+        claims.append((300 + k, [int(x) for x in rng.integers(0, nphys, size=n)], tk))
+    cuts = sorted(rng.choice(np.arange(1, len(claims)), size=int(rng.integers(0, 3)), replace=False))
+    op = O.OraclePool(NB, BS, SEED)
+    start = 0
+    for end in list(cuts) + [len(claims)]:
+        assert op.offload(from_claims(claims[start:end]), D0) == O.OK
+        start = end
+    holders = {}
+    reg = registered_prefixes(claims, holders)
+    assert op.identity_stats() == (len(reg), sum(1 for v in reg.values() if len(v) > 1))
+    reqs = []
+    for _, _, tk in claims:
+        reqs.extend(variants(tk))
+    got = op.lookup(from_claims([(1000 + i, [], t) for i, t in enumerate(reqs)]))
+    stale_stops = 0
+    for i, t in enumerate(reqs):
+        hit, _, amb = brute_lookup(reg, t, holders)
+        r = got[i]
+        assert (int(r["hit_blocks"]), r["status"] == O.LK_UNKNOWN) == (hit, amb), (seed, i)
+        nt = -(-t.size // BS)
+        if not amb:
+            want = O.LK_HIT if hit == nt and hit > 0 else O.LK_MISS if hit == 0 else O.LK_PARTIAL
+            assert r["status"] == want
+        if hit:
+            assert r["last_block"] == next(iter(reg[tuple(blocks_of(t)[:hit])]))
+        plain_hit, _, plain_amb = brute_lookup(reg, t)
+        stale_stops += int(plain_hit > hit and not amb)
+    assert stale_stops > 0  # block reuse did stop some walks

@@ -170,22 +170,254 @@ def test_unclaimed_failure_gives_no_claim_outcome(pool):
 
 
 def test_fallback_recompute_does_not_restore_the_claim(pool, d0):
-    """A reported load failure stays a failure even if the bytes are later
-    rewritten correctly (fallback recompute is not restoration)."""
+    """A reported load failure stays a failure of the claim even if the bytes
+    are later rewritten correctly (Table 9, fallback-recompute row: a
+    recompute after a failed load is not evidence that the claim was
+    restored)."""
     b = from_claims([(9, [20, 21], toks(2))])
     op = fresh()
     op.offload(b, d0)
     op.restore(b, load_failed_blocks=[21])
     out = op.check(b, d0)[0]  # bytes equal to the original
     assert out["code"] == O.RESTORE_FAILED_FAIL_CLOSED and out["first_failing_block"] == 1
-    # only a fresh offload record clears it
+    # a second restore without a reported failure does not clear it either
+    op.restore(b)
+    out = op.check(b, d0)[0]
+    assert out["code"] == O.RESTORE_FAILED_FAIL_CLOSED and out["reasons"] == O.R_LOAD_FAILED
+
+
+def test_recompute_stored_by_another_claim_does_not_restore_the_first():
+    """Section 5 storage_restorability row (store and load name the same
+    claim; a hook must not relabel a fallback recompute as restoration) and
+    Table 9's fallback-recompute row.  Claim C = [5, 6, 7] is offloaded and
+    its restore reports block 6 lost; the block is recomputed (the same
+    bytes) and stored by an offload of another claim X = [6], which is then
+    restored.  C's reuse still fails closed at position 1; X, whose own
+    offload recorded the recomputed bytes, is materialized."""
+    d = np.arange(NB, dtype=np.uint64) * np.uint64(7919) + np.uint64(11)
+    c = from_claims([(0xC, [5, 6, 7], toks(3))])
+    x = from_claims([(0xA, [6], toks(1))])
+    op = fresh()
+    assert op.offload(c, d) == O.OK
+    assert op.restore(c, load_failed_blocks=[6]) == O.OK
+    first = op.check(c, d)[0]
+    assert (first["code"], first["first_failing_block"]) == (O.RESTORE_FAILED_FAIL_CLOSED, 1)
+    assert op.offload(x, d) == O.OK  # the recompute, stored under X
+    assert op.restore(x) == O.OK
+    op.events(clear=True)
+    out_c = op.check(c, d)[0]
+    assert (out_c["code"], out_c["first_failing_block"], out_c["phys_block"]) == \
+        (O.RESTORE_FAILED_FAIL_CLOSED, 1, 6)
+    assert out_c["reasons"] == O.R_LOAD_FAILED
+    assert kinds_for(op.events(), 0xC) == [O.EV_RESTORATION_FAILED, O.EV_ACTIVE_REQUEST_REFUSED]
+    out_x = op.check(x, d)[0]
+    assert out_x["code"] == O.MATERIALIZED and out_x["reasons"] == 0
+    # C restored again, after X's offload: still failed, never RESTORED
+    op.restore(c)
+    assert op.check(c, d)[0]["code"] == O.RESTORE_FAILED_FAIL_CLOSED
+    assert O.EV_RESTORED not in kinds_for(op.events(), 0xC)
+
+
+def test_another_claims_offload_record_does_not_satisfy_the_claim():
+    """Section 5 storage_restorability row (store and load name the same
+    claim) and Table 9's wrong-claim row.  Claim C = [5, 6, 7] is offloaded,
+    restored and materialized.  Block 6 then receives other bytes, which a
+    second claim X = [6] offloads.  C's next check compares block 6 with C's
+    own offload, not X's: it fails closed at position 1, with C's digest as
+    the expected one and the new bytes' digest as the observed one.  X is
+    materialized."""
+    d = np.arange(NB, dtype=np.uint64) * np.uint64(7919) + np.uint64(11)
+    c = from_claims([(0xC, [5, 6, 7], toks(3))])
+    x = from_claims([(0xA, [6], toks(1))])
+    op = fresh()
+    op.offload(c, d)
+    op.restore(c)
+    assert op.check(c, d)[0]["code"] == O.MATERIALIZED
+    d2 = d.copy()
+    d2[6] = np.uint64(0x5EED)  # block 6 now holds X's bytes
+    op.offload(x, d2)
+    op.restore(x)
+    out = op.check(c, d2)[0]
+    assert (out["code"], out["first_failing_block"], out["phys_block"]) == \
+        (O.RESTORE_FAILED_FAIL_CLOSED, 1, 6)
+    assert out["reasons"] == O.R_DIGEST_MISMATCH
+    assert (int(out["expected_digest"]), int(out["observed_digest"])) == (int(d[6]), 0x5EED)
+    assert op.check(x, d2)[0]["code"] == O.MATERIALIZED
+    # the block state keeps the latest offload's digest (X's): evidence only
+    assert int(op.block_state()["d_off"][6]) == 0x5EED
+
+
+def test_failure_reported_before_a_claim_is_not_its_failure():
+    """A load failure reported before a claim's offload belongs to the claims
+    that had recorded the block then; the later claim recorded the block's
+    bytes itself (section 7 path C: only the claim's own failure counts)."""
+    d = np.arange(NB, dtype=np.uint64) + np.uint64(5)
+    a = from_claims([(1, [3, 4], toks(2))])
+    b = from_claims([(2, [4, 8], toks(2))])
+    op = fresh()
+    op.offload(a, d)
+    op.restore(a, load_failed_blocks=[4])
+    op.offload(b, d)
+    op.restore(from_claims([(1, [3, 4], a.claim(0)[2]), (2, [4, 8], b.claim(0)[2])]))
+    out = op.check(from_claims([(1, [3, 4], a.claim(0)[2]), (2, [4, 8], b.claim(0)[2])]), d)
+    assert out["code"].tolist() == [O.RESTORE_FAILED_FAIL_CLOSED, O.MATERIALIZED]
+    # a failure reported after both offloads fails both
+    op.restore(from_claims([(2, [4, 8], b.claim(0)[2])]), load_failed_blocks=[4])
+    out = op.check(from_claims([(1, [3, 4], a.claim(0)[2]), (2, [4, 8], b.claim(0)[2])]), d)
+    assert out["code"].tolist() == [O.RESTORE_FAILED_FAIL_CLOSED] * 2
+    assert out["first_failing_block"].tolist() == [1, 0]
+    assert op.block_state()["load_failed"][4] == 1
+
+
+def _write_block(pool, g, b, canon):
+    """Put canonical bytes into block b of a host pool array ([plane][block][chunk])."""
+    flat = pool.reshape(-1)
+    for p in range(g.planes):
+        at = (p * g.num_blocks + b) * g.chunk_bytes
+        flat[at:at + g.chunk_bytes] = canon[p * g.chunk_bytes:(p + 1) * g.chunk_bytes]
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_multi_offload_lifecycles_match_a_claim_ledger(seed):
+    """Random lifecycles over a few shared blocks: offloads of new claims,
+    block rewrites between them (recomputes of earlier bytes, other bytes,
+    single-bit flips), restores with reported load failures, and checks.
+    The expectation is a ledger written from the paper with no digest: each
+    claim's offload stores a copy of its blocks' bytes (the claim's own
+    offload, section 5 storage_restorability); a check of a restored claim
+    fails closed at the first position whose current bytes differ from the
+    claim's own stored copy, or whose block had a load failure reported by a
+    restore call after the claim's offload (Table 9: a recompute is not a
+    restore, a wrong claim's record does not count); a claim never restored
+    has no outcome."""
+    rng = np.random.default_rng(7000 + seed)
+    w = TINY
+    g = w.geometry
+    pool = host_pool(w).copy()
+    hot = rng.choice(g.num_blocks, size=6, replace=False)
+    op = fresh()
+    ledger = {}  # claim id -> [blocks, tokens, stored copies, call index, restored]
+    reports = []  # (block, call index)
+    calls = 0
+    seen_outcomes = set()
+    for step in range(14):
+        act = rng.choice(["offload", "rewrite", "restore", "check"], p=[0.3, 0.3, 0.2, 0.2])
+        if step == 13:
+            act = "restore"  # the last step restores and then checks every claim
+        if act == "offload" or not ledger:
+            calls += 1
+            rows = []
+            for _ in range(int(rng.integers(1, 4))):
+                cid = 100 + len(ledger) + len(rows)
+                n = int(rng.integers(1, 4))
+                blks = [int(x) for x in rng.choice(hot, size=n)]
+                rows.append((cid, blks, toks(n)))
+            batch = from_claims(rows)
+            assert op.offload(batch, digests(pool, w)) == O.OK
+            for cid, blks, tk in rows:
+                copies = [O.canonical_block(pool, g.planes, g.num_blocks, g.chunk_bytes, b).copy()
+                          for b in blks]
+                ledger[cid] = [blks, tk, copies, calls, False]
+        elif act == "rewrite":
+            b = int(rng.choice(hot))
+            u = rng.random()
+            if u < 0.4:  # a recompute: bytes equal to some claim's stored copy of b
+                copies = [c[2][j] for c in ledger.values() for j, x in enumerate(c[0]) if x == b]
+                if not copies:
+                    continue
+                _write_block(pool, g, b, copies[int(rng.integers(len(copies)))])
+            elif u < 0.7:  # other bytes
+                _write_block(pool, g, b, rng.integers(0, 256, size=g.block_bytes, dtype=np.uint8))
+            else:  # a silent single-bit flip
+                O.apply_flip(pool, g.planes, g.num_blocks, g.chunk_bytes, b,
+                             int(rng.integers(0, 8 * g.block_bytes)))
+        elif act == "restore":
+            calls += 1
+            cids = [c for c in ledger if rng.random() < 0.8 or step == 13]
+            lost = [int(b) for b in hot if rng.random() < 0.15]
+            batch = from_claims([(c, ledger[c][0], ledger[c][1]) for c in cids])
+            assert op.restore(batch, load_failed_blocks=lost) == O.OK
+            reports += [(b, calls) for b in lost]
+            for c in cids:
+                ledger[c][4] = True
+        if act == "check" or step == 13:
+            cids = list(ledger)
+            rng.shuffle(cids)
+            batch = from_claims([(c, ledger[c][0], ledger[c][1]) for c in cids])
+            out = op.check(batch, digests(pool, w))
+            for o, c in zip(out, cids):
+                blks, _, copies, at, restored = ledger[c]
+                if not restored:
+                    assert (int(o["code"]), int(o["first_failing_block"])) == (O.UNKNOWN, NONE32)
+                    assert o["reasons"] & O.R_NO_RESTORE
+                    continue
+                bad = []
+                for j, b in enumerate(blks):
+                    now = O.canonical_block(pool, g.planes, g.num_blocks, g.chunk_bytes, b)
+                    lost = any(rb == b and rc > at for rb, rc in reports)
+                    if lost or not np.array_equal(now, copies[j]):
+                        bad.append(j)
+                if not bad:
+                    assert o["code"] == O.MATERIALIZED and o["reasons"] == 0, (seed, step, c)
+                else:
+                    j = bad[0]
+                    assert (int(o["code"]), int(o["first_failing_block"])) == \
+                        (O.RESTORE_FAILED_FAIL_CLOSED, j), (seed, step, c, bad)
+                    assert int(o["expected_digest"]) == O.block_digest(copies[j], w.seed)
+                seen_outcomes.add(int(o["code"]))
+    assert seen_outcomes  # restored claims were checked
+
+
+def test_event_payloads_against_independent_values(pool, d0):
+    """Each event's aux payload (section 7 event list, paths A and B),
+    against a value computed without the lifecycle code: OFFLOADED carries
+    the number of block-table entries offloaded; RESTORE_REQUIRED the
+    accepted number, whatever the restore batch presents; RESTORATION_FAILED
+    the restored (observed) digest at the failing block, here from the exact
+    single-flip delta D_off + (w' - w) * k_i mod 2^64; OUTCOME_UNKNOWN the
+    reason bits; a malformed row's chain hash is the seed (no tokens are
+    read)."""
+    cid = 0xB0B
+    blocks = [10, 11, 12]
+    tk = toks(3)
+    b = from_claims([(cid, blocks, tk)])
+    bit = 8 * 4096 * 2 + 64 * 37 + 61  # plane 2 of the 4 planes, word 37 there, bit 61
+    f = FaultSpec(np.array([11], np.uint32), np.array([bit], np.uint64), np.zeros(0, np.uint32))
+    op = fresh()
+    assert op.offload(b, d0) == O.OK
+    # the restore presents the claim with a shorter row: aux is the accepted count
+    assert op.restore(from_claims([(cid, blocks[:2], tk[: 2 * BS])])) == O.OK
+    restored = apply_flips(pool, TINY, f)
+    out = op.check(b, digests(restored, TINY))[0]
+    ev = op.events()
+    aux = {int(e["kind"]): int(e["aux"]) for e in ev}
+    assert aux[O.EV_OFFLOADED] == len(blocks)
+    assert aux[O.EV_RESTORE_REQUIRED] == len(blocks)
+    g = TINY.geometry
+    canon = O.canonical_block(pool, g.planes, g.num_blocks, g.chunk_bytes, 11)
+    i = bit // 64
+    w_old = int.from_bytes(bytes(canon[8 * i:8 * i + 8]), "little")
+    w_new = w_old ^ (1 << (bit % 64))
+    want = (int(d0[11]) + (w_new - w_old) * O.kv_key(TINY.seed, i)) % (1 << 64)
+    assert want != int(d0[11])
+    assert (int(out["code"]), int(out["first_failing_block"])) == (O.RESTORE_FAILED_FAIL_CLOSED, 1)
+    assert aux[O.EV_RESTORATION_FAILED] == want  # the observed digest, not the expected one
+    assert int(out["observed_digest"]) == want and int(out["expected_digest"]) == int(d0[11])
+    assert aux[O.EV_ACTIVE_REQUEST_REFUSED] == cid
+
+    # OUTCOME_UNKNOWN carries the reason bits (the header's values)
     op2 = fresh()
-    op2.offload(b, d0)
-    op2.restore(b, load_failed_blocks=[21])
-    b2 = from_claims([(10, [21], toks(1))])
-    op2.offload(b2, d0)
-    op2.restore(b2)
-    assert op2.check(b2, d0)[0]["code"] == O.MATERIALIZED
+    rows = [(1, [4, MISSING, 5], toks(3)), (2, [6, 7], toks(2)), (0xFFFFFFFFFFFFFFFF, [8], toks(1))]
+    op2.offload(from_claims(rows[:2]), d0)
+    op2.events(clear=True)
+    out2 = op2.check(from_claims(rows), d0)
+    ev2 = op2.events()
+    assert [int(e["kind"]) for e in ev2] == [O.EV_OUTCOME_UNKNOWN] * 3
+    assert [int(e["aux"]) for e in ev2] == [0x020 | 0x002 | 0x004, 0x004, 0x200]
+    assert [int(e["block_index"]) for e in ev2] == [1, NONE32, NONE32]
+    assert int(out2[2]["chain_hash"]) == TINY.seed and int(out2[2]["num_blocks"]) == 0
+    empty = op2.check(from_claims([(3, [], toks(0))]), d0)[0]
+    assert int(empty["chain_hash"]) == TINY.seed
 
 
 def test_ordinary_offload_without_claim_is_not_an_outcome(d0):
