@@ -12,14 +12,17 @@
  * closed (Table 2, last rule).  This library supplies those obligations for
  * paged KV blocks on the GPU:
  *
- *   claim_offload  accept a claim batch and record a 64-bit digest of every
- *                  referenced physical block (optionally staging the bytes);
+ *   claim_offload  accept a claim batch; each claim keeps its own offload
+ *                  record, a 64-bit digest of every block it references
+ *                  (optionally staging the bytes);
  *   claim_restore  move accepted, offloaded claims to restore-required,
  *                  optionally scattering staged bytes back, and apply the
  *                  given faults (bit flips = silent corruption, reported load
- *                  failures = the paper's controlled CPU->GPU load failure);
- *   claim_check    re-digest the referenced blocks, compare, chain each
- *                  claim's token prefix hash and reduce every claim to one
+ *                  failures = the paper's controlled CPU->GPU load failure,
+ *                  which fails the claims that recorded the block before it);
+ *   claim_check    re-digest the referenced blocks, compare each claim's
+ *                  blocks with its own offload record, chain each claim's
+ *                  token prefix hash and reduce every claim to one
  *                  outcome (MATERIALIZED, RESTORE_FAILED_FAIL_CLOSED or
  *                  UNKNOWN) with the first failing block, appending the
  *                  ordered events;
@@ -102,12 +105,12 @@ extern "C" {
 #define CLAIM_R_TOKEN_MISMATCH 0x008    /* token count, or a block's chain hash, differs from acceptance */
 #define CLAIM_R_FOOTPRINT_MISMATCH 0x010 /* block list differs from acceptance */
 #define CLAIM_R_MISSING_ENTRY 0x020     /* entry is CLAIM_NONE or >= num_blocks */
-#define CLAIM_R_NO_OFFLOAD_RECORD 0x040 /* block has no offload digest */
+#define CLAIM_R_NO_OFFLOAD_RECORD 0x040 /* the claim recorded no offload of this block at this position */
 #define CLAIM_R_SHAPE_MISMATCH 0x080    /* blocks != ceil(tokens / block_size) */
 #define CLAIM_R_EMPTY 0x100             /* claim has no blocks */
 #define CLAIM_R_MALFORMED 0x200         /* offsets inconsistent, or reserved id */
-#define CLAIM_R_LOAD_FAILED 0x400       /* reported load failure */
-#define CLAIM_R_DIGEST_MISMATCH 0x800   /* restored digest != offload digest */
+#define CLAIM_R_LOAD_FAILED 0x400       /* load failure reported after the claim's offload */
+#define CLAIM_R_DIGEST_MISMATCH 0x800   /* restored digest != the claim's own offload digest */
 #define CLAIM_R_BEYOND_PREDICATE 0x1000 /* a failed block lies past the predicate (not a failure) */
 
 #define CLAIM_NONE 0xFFFFFFFFu                   /* no position; missing block-table entry */
@@ -191,8 +194,13 @@ typedef struct claim_batch {
 /* Faults applied by claim_restore (host memory, read before it returns).
  * flip f XORs canonical bit flip_bits[f] (bit 0 = least significant bit of
  * canonical byte 0) of block flip_blocks[f]; a bit flipped twice is
- * restored.  load_failed_blocks are reported load failures: they fail
- * every claim that references them until a later offload of the block. */
+ * restored.  load_failed_blocks are reported load failures (section 7 path
+ * B, the controlled CPU->GPU load failure F0): each fails, at that block,
+ * every claim whose offload recorded the block before this restore, and
+ * nothing clears it for them.  A later offload of the block (a recompute
+ * stored under another claim) is that claim's own record: it does not
+ * restore the earlier claims (Table 9, fallback-recompute row), and the
+ * earlier failure is not the later claim's failure. */
 typedef struct claim_fault_spec {
   uint32_t num_flips;
   uint32_t num_load_failed;
@@ -210,7 +218,7 @@ typedef struct claim_outcome {
   uint32_t num_blocks;          /* block-table entries presented (0 if malformed) */
   uint32_t reasons;             /* OR of CLAIM_R_* found anywhere in the claim */
   uint32_t intact_blocks;       /* leading positions with no problem at all (<= num_blocks) */
-  uint64_t expected_digest;     /* offload digest at j* (failures only, else 0) */
+  uint64_t expected_digest;     /* the claim's own offload digest at j* (failures only, else 0) */
   uint64_t observed_digest;     /* restored digest at j* (failures only, else 0) */
   uint64_t chain_hash;          /* h_{nt-1} of the presented tokens (S if none) */
   uint64_t chain_hash_at_fail;  /* h_{j*} if j* < nt, else 0 */
@@ -265,9 +273,12 @@ typedef struct claim_timing {
 
 /* Create a pool over caller-owned KV memory (section 7: the connector's
  * accepted-claim state; Table 5: fixed cache identity = seed + geometry).
- * Allocates the pool's device state: offload and restored digests, offload
- * records, reported-failure flags, the claim registry (ids, state, token
- * count, chain hash, footprint, per-position accepted identities), the
+ * Allocates the pool's device state: per block the latest offload digest,
+ * the restored digest and latest reported-failure generation (16 bytes),
+ * whether some claim recorded it, and the identity of its latest
+ * registration; the claim registry (ids, state, token count, chain hash,
+ * footprint, offload generation; per position the accepted identity and the
+ * claim's own offload digest: 20 bytes per footprint entry); the
  * cache-identity table (32 bytes per entry: the entry and where its first
  * registrant keeps its accepted identities; next_pow2(2 * max_footprint)
  * entries), the event log and scratch.  Returns EINVAL for a bad
@@ -275,7 +286,8 @@ typedef struct claim_timing {
 int claim_pool_create(const claim_pool_desc* desc, claim_pool** out);
 
 /* Wait for the pool's stream, then free everything the pool owns (not the
- * KV memory).  NULL is accepted. */
+ * KV memory): the end of the connector state of section 7, after which no
+ * claim of the pool can be restored or checked.  NULL is accepted. */
 int claim_pool_destroy(claim_pool* pool);
 
 /* Accept and offload a batch (section 1: accept, materialized, offloaded;
@@ -283,21 +295,30 @@ int claim_pool_destroy(claim_pool* pool);
  * The whole batch is refused with EDUP if a non-reserved id occurs twice or
  * is already registered (Table 2: duplicate ownership fails closed); nothing
  * changes then.  Otherwise each well-formed claim is registered (event
- * ACCEPTED); every in-range block it references gets an offload digest and
- * its reported-failure flag is cleared; a claim whose footprint is
- * non-empty, fully present and equal in length to ceil(tokens/block_size)
- * becomes OFFLOADED (event OFFLOADED).  Each claim's accepted identity
- * h_j (its chain hash after token block j) is kept for every position with
- * both a block and tokens.  For every OFFLOADED claim, (h_j -> block j) is
- * registered in the cache-identity table (section 5 cache identity; Table 5
- * joinable block hashes): a registration equal to an existing one is stored
- * once; the same identity registered to a different block is duplicate
- * ownership and makes the identity ambiguous (Table 2).  Entries are never
- * removed.  With staging != NULL the canonical
- * bytes of every such block are also written to staging (device memory or
- * host memory from hipHostMalloc, 16-byte aligned, else EINVAL), one block
- * after another in ascending block-id order; staging_bytes must cover them
- * (else ENOSPC).  A staged offload replaces the previous one.  Waits twice
+ * ACCEPTED) with its own offload record: the digest of every in-range
+ * block it references, taken by this call (section 5 storage_restorability:
+ * store and load name the same claim), so no later offload of a shared
+ * block by another claim changes what the claim is checked against.  A
+ * claim whose footprint is non-empty, fully present and equal in length to
+ * ceil(tokens/block_size) becomes OFFLOADED (event OFFLOADED).  Each
+ * claim's accepted identity h_j (its chain hash after token block j) is
+ * kept for every position with both a block and tokens.  For every
+ * OFFLOADED claim, (h_j -> block j) is registered in the cache-identity
+ * table (section 5 cache identity; Table 5 joinable block hashes): a
+ * registration equal to an existing one is stored once; the same identity
+ * registered to a different block is duplicate ownership and makes the
+ * identity ambiguous (Table 2).  A block holds the identity of its latest
+ * registration (in call, then batch, then position order); identities it
+ * held before are stale and no longer hit in claim_lookup.  Entries are
+ * never removed.  With staging != NULL the canonical bytes of every such
+ * block are also written to staging (device memory or host memory from
+ * hipHostMalloc, 16-byte aligned, else EINVAL), one block after another in
+ * ascending block-id order; staging_bytes must cover them (else ENOSPC).
+ * Staging holds one generation: a staged offload replaces the previous
+ * one, so claim_restore can copy back only blocks of the last staged
+ * offload; blocks staged only by an earlier offload are then used as the
+ * pool holds them (a claim whose bytes are gone fails closed on its digest
+ * compare), although lookups may still hit their identities.  Waits twice
  * for the stream to read the acceptance verdict (three times when a block
  * row runs backwards).  ENOSPC if the registry, footprint store or event
  * log could overflow; the footprint store takes num_refs entries, or, when
@@ -317,8 +338,13 @@ int claim_restore(claim_pool* pool, const claim_batch* batch, const void* stagin
                   uint64_t staging_bytes, const claim_fault_spec* faults);
 
 /* Check (section 7 path A step 5, path B steps 5-7, path C): digest every
- * in-range, offloaded block the well-formed claims reference, compare with
- * the offload digest, chain each claim's tokens and decide its outcome.
+ * in-range block with an offload record that the well-formed claims
+ * reference, and judge each claim's blocks against its own offload record:
+ * a load failure reported after its offload, or a restored digest that
+ * differs from its own offload digest, is a restoration failure at that
+ * position; an entry that is not the accepted one holds no record of the
+ * claim (CLAIM_R_NO_OFFLOAD_RECORD, with CLAIM_R_FOOTPRINT_MISMATCH).
+ * Chain each claim's tokens and decide its outcome.
  * The cache identity is compared position by position: a token block whose
  * h_j differs from the accepted one, or the block where the token counts
  * part (min(tokens, accepted tokens) / block_size), is an ambiguity at that
@@ -337,8 +363,11 @@ int claim_check(claim_pool* pool, const claim_batch* batch);
  * in the running example).  For each request row c of the batch (its id,
  * token_offsets and tokens; block rows are not read and may be NULL): the
  * chain h_0 .. h_{nt-1} of its tokens, and hit_blocks = the number of
- * leading token blocks whose identity is registered and unambiguous.  The
- * lookup stops at the first block that is not; if that identity is
+ * leading token blocks whose identity is registered, unambiguous and still
+ * held by its block (a block registered since under another identity no
+ * longer holds this prefix: the stale identity stops the lookup as an
+ * absent one does).  The lookup stops at the first block that is not; if
+ * that identity is
  * registered but ambiguous (duplicate ownership), the status is
  * CLAIM_LOOKUP_UNKNOWN rather than a shorter hit (Table 2: duplicate owners
  * fail closed), as it is for a malformed row (reserved id, token offsets
@@ -355,7 +384,10 @@ int claim_lookup(claim_pool* pool, const claim_batch* requests, claim_lookup_res
  * different blocks).  Either pointer may be NULL. */
 int claim_identity_stats(claim_pool* pool, uint64_t* entries, uint64_t* ambiguous);
 
-/* Wait for the pool's stream and copy to the host the outcomes of the last
+/* The section 7 event stream and claim outcomes, read out (paths A and B:
+ * the ordered events E0 .. E13 and the claim-scoped outcome; section 1
+ * running example, the accepted event sequence).
+ * Wait for the pool's stream and copy to the host the outcomes of the last
  * claim_check (into out, capacity out_cap; *num_out = their count) and the
  * events appended since the previous outcomes_read (into events, capacity
  * ev_cap; *num_events = their count), which are then dropped from the log
@@ -371,15 +403,20 @@ int outcomes_read(claim_pool* pool, claim_outcome* out, uint32_t out_cap, uint32
 int claim_timing_read(claim_pool* pool, claim_timing* out);
 
 /* Wait for the pool's stream and copy the per-block state of blocks
- * [first, first + count) to the host: offload digests D_off, restored
- * digests D_res (as of the last check that digested the block), offload
- * records and reported-failure flags (one byte each, 0 or 1).  Any output
- * pointer may be NULL.  EINVAL if the range exceeds the pool.  This is the
- * block-level evidence behind a claim outcome (section 7 path B step 5). */
+ * [first, first + count) to the host: the digest recorded by the block's
+ * latest offload (each claim is checked against its own record, which the
+ * outcome reports as expected_digest), restored digests D_res (as of the
+ * last check that digested the block), whether some claim recorded the
+ * block, and whether a load failure of it has ever been reported (one byte
+ * each, 0 or 1).  Any output pointer may be NULL.  EINVAL if the range
+ * exceeds the pool.  This is the block-level evidence behind a claim
+ * outcome (section 7 path B step 5: affected-block evidence). */
 int claim_block_state_read(claim_pool* pool, uint32_t first, uint32_t count, uint64_t* d_off,
                            uint64_t* d_res, uint8_t* valid_off, uint8_t* load_failed);
 
-/* Text for a status code (static storage). */
+/* Text for a status code (static storage).  Status codes report API misuse
+ * and resource limits only; claim problems are outcomes, never statuses
+ * (Table 2: ambiguity yields no claim outcome rather than an error). */
 const char* claim_strerror(int status);
 
 #ifdef __cplusplus

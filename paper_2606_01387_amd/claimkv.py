@@ -27,7 +27,9 @@ OK, EINVAL, ENOMEM, EHIP, ENOSPC, EDUP = 0, -1, -2, -3, -4, -5
 UNKNOWN, MATERIALIZED, RESTORE_FAILED_FAIL_CLOSED = 0, 1, 2
 EV_ACCEPTED, EV_OFFLOADED, EV_RESTORE_REQUIRED, EV_RESTORED = 1, 2, 3, 4
 EV_RESTORATION_FAILED, EV_ACTIVE_REQUEST_REFUSED, EV_OUTCOME_UNKNOWN = 5, 6, 7
-R_TOKEN_MISMATCH = 0x008
+R_NOT_ACCEPTED, R_NOT_OFFLOADED, R_NO_RESTORE, R_TOKEN_MISMATCH = 0x001, 0x002, 0x004, 0x008
+R_FOOTPRINT_MISMATCH, R_MISSING_ENTRY, R_NO_OFFLOAD_RECORD, R_SHAPE_MISMATCH = 0x010, 0x020, 0x040, 0x080
+R_EMPTY, R_MALFORMED, R_LOAD_FAILED, R_DIGEST_MISMATCH = 0x100, 0x200, 0x400, 0x800
 R_BEYOND_PREDICATE = 0x1000
 LOOKUP_UNKNOWN, LOOKUP_HIT, LOOKUP_PARTIAL, LOOKUP_MISS = 0, 1, 2, 3
 NONE = 0xFFFFFFFF

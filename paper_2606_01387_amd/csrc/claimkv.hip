@@ -28,18 +28,19 @@
 //    claims alias it.
 //  * Claims.  A group of W lanes (W = 2..64, from the batch's mean claim
 //    length) owns one claim: lanes take block positions j = j0 + lane.  A
-//    window first issues every load that depends only on j (block id,
-//    accepted block and identity, the block's tokens), then the block's
-//    status byte (offload record, reported failure, digest mismatch, all
-//    three decided when the check combines the block's digest), which
-//    stays in flight while the serial chain
-//    h_j = splitmix64(h_{j-1} ^ M_j) walks the window (on the scalar unit
-//    when W = 64); the checks (footprint, identity, missing entry, offload
-//    record, reported failure, digest mismatch, predicate) follow.  The
+//    window first issues every load that depends only on j (block id, the
+//    claim's accepted block, identity and offload digest, the block's
+//    tokens), then the block's 16-byte record (restored digest, generation
+//    of its latest reported load failure), which stays in flight while the
+//    identity step runs; the checks (footprint, identity, missing entry,
+//    the claim's own record: a failure reported after its offload or a
+//    restored digest different from its own, predicate) follow.  The
 //    outcome is the minimum of packed keys (class << 32 | position).
 //  * Cache identity.  Offload registers (h_j -> block) of offloaded claims
-//    in an open-addressing table with order-independent atomics; a lookup
-//    walks a request's chain and probes it block by block.
+//    in an open-addressing table with order-independent atomics, and each
+//    block remembers the identity of its latest registration; a lookup
+//    probes a request's identities block by block and stops at one that is
+//    absent, ambiguous, or no longer held by its block.
 //  * Events.  Per-claim event counts (0..2) are scanned by one workgroup for
 //    batches up to 4096 claims, else in three small kernels (tile sums,
 //    one-workgroup scan of the tile sums, write), so the log stays in batch
@@ -210,7 +211,8 @@ struct RegEntry {  // one 64-byte line per slot: a probe touches one line
   uint64_t fpoff;   // accepted footprint: fp[fpoff .. fpoff + nblk)
   uint32_t pred;    // leading positions the accepted predicate covers
   uint32_t pad0;
-  uint64_t pad[2];
+  uint64_t gen;     // generation of the claim's offload
+  uint64_t pad1;
 };
 
 struct RegDev {
@@ -218,6 +220,15 @@ struct RegDev {
   RegEntry* e;
   const uint32_t* fp;
   uint64_t* idn;  // accepted identities h_j, at the footprint's offsets
+  uint64_t* dig;  // the claim's own offload digest of the block at each position
+};
+
+// Per-block record the check reads at every block position (one 16-byte
+// load): the block's restored digest as of the last check that digested
+// it, and the generation of its latest reported load failure (0: none).
+struct BlockRes {
+  uint64_t d_res;
+  uint64_t fail_gen;
 };
 
 // Cache-identity table: open addressing on the identity h_j, linear
@@ -287,6 +298,7 @@ static_assert(sizeof(claim_outcome) == 64, "claim_outcome layout");
 static_assert(sizeof(claim_event) == 40, "claim_event layout");
 static_assert(sizeof(Pend) == 32, "Pend layout");
 static_assert(sizeof(RegEntry) == 64, "RegEntry layout");
+static_assert(sizeof(BlockRes) == 16, "BlockRes layout");
 
 struct Row {
   uint64_t id;
@@ -536,25 +548,9 @@ __global__ void __launch_bounds__(kThreads) k_mark(BatchDev b, uint32_t nb, int 
     if (blk >= nb) continue;
     if (mode == kMarkOffloaded && !valid_off[blk]) continue;
     if (mode == kMarkStaged && slot_of[blk] == kNone) continue;
-    mark[blk] = 1;
-  }
-}
-
-// Mark every in-range, offloaded block listed among the batch's block-table
-// entries (the check's selection: one thread per entry, no row validation).
-__global__ void __launch_bounds__(kThreads) k_mark_entries(const uint32_t* __restrict__ bi,
-                                                           uint64_t N, uint32_t nb,
-                                                           const uint8_t* __restrict__ valid_off,
-                                                           uint8_t* __restrict__ mark) {
-  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
-  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += stride) {
-    const uint32_t blk = bi[i];
-    if (blk >= nb) continue;
-    // most blocks are listed many times: read before writing, so that the
-    // stores (all of the same value) stay about one per block; both flags
-    // are loaded together
-    const uint32_t seen = mark[blk], rec = valid_off[blk];
-    if (!seen && rec) mark[blk] = 1;
+    // most blocks are referenced many times: read before writing, so that
+    // the stores (all of the same value) stay about one per block
+    if (!mark[blk]) mark[blk] = 1;
   }
 }
 
@@ -778,27 +774,21 @@ __global__ void __launch_bounds__(kThreads) k_digest(const u32x2* __restrict__ p
   }
 }
 
-// Per-block status byte of a check (bstat): the three facts the claim stage
-// needs about a block, so that it loads one byte per block position.
-constexpr uint32_t kBsRecord = 1, kBsLoadFailed = 2, kBsMismatch = 4;
-
 // Add each unique block's piece-group partials.
-//   mode 0 (offload): d_off, valid_off = 1, load_failed = 0, slot_of
-//   mode 1 (check):   d_res, and bstat = record | reported failure |
-//                     (d_res != d_off); every block a check's claims can
-//                     find with an offload record is one of its unique
-//                     blocks, so the claim stage reads bstat only for
-//                     blocks written here (others keep 0 = no record)
+//   mode 0 (offload): d_off (the latest offload's digest), valid_off = 1
+//                     (some claim records the block), slot_of
+//   mode 1 (check):   the restored digest in the block's record; every
+//                     block whose record a check's claims compare is one
+//                     of its unique blocks, so the claim stage reads only
+//                     digests written here
 __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restrict__ uniq,
                                                        const Counters* __restrict__ ctr,
                                                        const uint64_t* __restrict__ partial,
                                                        uint32_t pgs, uint32_t groups, int mode,
-                                                       int staged, uint64_t* __restrict__ d_out,
-                                                       const uint64_t* __restrict__ d_off,
+                                                       int staged, uint64_t* __restrict__ d_off,
                                                        uint8_t* __restrict__ valid_off,
-                                                       uint8_t* __restrict__ load_failed,
                                                        uint32_t* __restrict__ slot_of,
-                                                       uint8_t* __restrict__ bstat) {
+                                                       BlockRes* __restrict__ bres) {
   // One lane per unique block.  Unique index u = n * groups + g was digested
   // by the workgroups of group g, which wrote its partials at
   // partial[(pg * groups + g) * NW + n]; slot t = g * NW + n puts
@@ -824,14 +814,12 @@ __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restric
       for (uint32_t k = 0; k < 32; ++k) sum += v[k];
     }
     const uint32_t b = uniq[u];
-    d_out[b] = sum;
     if (mode == 0) {
+      d_off[b] = sum;
       valid_off[b] = 1;
-      load_failed[b] = 0;
       slot_of[b] = staged ? u : kNone;
     } else {
-      bstat[b] = (uint8_t)(kBsRecord | (load_failed[b] ? kBsLoadFailed : 0u) |
-                           (sum != d_off[b] ? kBsMismatch : 0u));
+      bres[b].d_res = sum;
     }
   }
 }
@@ -897,13 +885,16 @@ __global__ void __launch_bounds__(1024) k_footprint_offsets(BatchDev b, uint64_t
 }
 
 // Acceptance: chain hash of the claim's tokens, presence of its footprint
-// (stored as the accepted footprint), its accepted identities and their
-// registration, and the record of its ACCEPTED (+ OFFLOADED) events.
+// (stored as the accepted footprint, with the claim's own offload digest of
+// each in-range block: the offload digest ran before acceptance), its
+// accepted identities and their registration, and the record of its
+// ACCEPTED (+ OFFLOADED) events.
 template <int W>
 __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdDev ids,
                                                      uint32_t nb, uint32_t bs, uint64_t seed,
                                                      uint64_t fp_base,
                                                      const uint64_t* __restrict__ fpo,
+                                                     const uint64_t* __restrict__ d_off,
                                                      uint32_t* __restrict__ fp_out,
                                                      Counters* __restrict__ ctr,
                                                      uint32_t* __restrict__ cnt,
@@ -923,6 +914,7 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
   for (uint64_t j = gl; j < r.n; j += W) {
     const uint32_t blk = b.bi[(uint64_t)r.bo0 + j];
     fp_out[at0 + j] = blk;  // the accepted footprint
+    reg.dig[at0 + j] = blk < nb ? d_off[blk] : 0ull;  // and the claim's own offload record
     if (blk >= nb) missing = 1;
   }
   missing = group_or<W>(missing);
@@ -972,7 +964,7 @@ __global__ void __launch_bounds__(kThreads) k_accept(BatchDev b, RegDev reg, IdD
 // claim took the slot).  Kept out of the claim-group kernel so that each
 // wave waits on its atomics once, for 64 claims.
 __global__ void __launch_bounds__(kThreads) k_register_claims(BatchDev b, RegDev reg, uint32_t bs,
-                                                              uint64_t fp_base,
+                                                              uint64_t fp_base, uint64_t gen,
                                                               const uint64_t* __restrict__ fpo,
                                                               const Pend* __restrict__ pend,
                                                               Counters* __restrict__ ctr) {
@@ -1002,6 +994,7 @@ __global__ void __launch_bounds__(kThreads) k_register_claims(BatchDev b, RegDev
         e.ntok = r.ntok;
         e.chain = pe.aux0;
         e.fpoff = store_at(fpo, fp_base, c, r.bo0);
+        e.gen = gen;
         // leading_prefix_at_least(k): the blocks holding the first k tokens
         uint32_t pred = r.n;
         if (b.pred) {
@@ -1018,18 +1011,26 @@ __global__ void __launch_bounds__(kThreads) k_register_claims(BatchDev b, RegDev
 
 // ----------------------------------------------------------------- restore
 
-// Registration pass 2: duplicate ownership.  Every position an offloaded
-// claim of the batch registered compares its block with the block stored
-// for its identity; a different one makes the identity ambiguous (counted
-// once, by the call that sets the flag).
+// Registration pass 2: duplicate ownership, and each block's latest
+// registration.  Every position an offloaded claim of the batch registered
+// compares its block with the block stored for its identity; a different
+// one makes the identity ambiguous (counted once, by the call that sets the
+// flag).  It also raises the block's owner_at to its identity-store index
+// + 1: store indices grow with the call, the claim and the position, so the
+// maximum is the block's latest registration (k_holders then reads its
+// identity).  Claims are taken in reverse batch order and owner_at is read
+// before the atomic, so most positions find a later one already there and
+// skip it.
 template <int W>
 __global__ void __launch_bounds__(kThreads) k_register_owners(BatchDev b, RegDev reg, IdDev ids,
                                                               uint32_t nb, uint32_t bs,
                                                               uint64_t fp_base,
                                                               const uint64_t* __restrict__ fpo,
+                                                              uint64_t* __restrict__ owner_at,
                                                               Counters* __restrict__ ctr) {
-  const uint64_t c = group_claim<W>();
-  if (c >= b.C) return;
+  const uint64_t c_fwd = group_claim<W>();
+  if (c_fwd >= b.C) return;
+  const uint64_t c = b.C - 1 - c_fwd;
   const uint32_t gl = (threadIdx.x & 63) & (W - 1);
   const Row r = read_row(b, c);
   const uint64_t nt = (r.ntok + bs - 1) / bs;
@@ -1045,12 +1046,34 @@ __global__ void __launch_bounds__(kThreads) k_register_owners(BatchDev b, RegDev
     uint32_t amb = 0;
     if (j < r.n) {
       const uint64_t key = reg.idn[at0 + j];
+      const uint32_t blk = b.bi[(uint64_t)r.bo0 + j];
+      const unsigned long long mine = at0 + j + 1;
       const IdEntry* e = id_find(ids, key);
-      if (e && e->block != b.bi[(uint64_t)r.bo0 + j] &&
+      if (e && e->block != blk &&
           !(atomicOr((uint32_t*)&e->flags, kIdAmbiguous) & kIdAmbiguous))
         amb = 1;
+      if (*(volatile unsigned long long*)(owner_at + blk) < mine)
+        atomicMax((unsigned long long*)(owner_at + blk), mine);
     }
     wave_count(&ctr->id_ambiguous, amb);
+  }
+}
+
+// Registration pass 3: each block of the offload whose latest registration
+// belongs to this call (owner_at past the call's first store index) now
+// holds that registration's identity.
+__global__ void __launch_bounds__(kThreads) k_holders(const uint32_t* __restrict__ uniq,
+                                                      const Counters* __restrict__ ctr,
+                                                      const uint64_t* __restrict__ owner_at,
+                                                      const uint64_t* __restrict__ idn,
+                                                      uint64_t fp_base,
+                                                      uint64_t* __restrict__ holder) {
+  const uint32_t U = ctr->uniq_count;
+  const uint64_t stride = (uint64_t)gridDim.x * kThreads;
+  for (uint64_t u = (uint64_t)blockIdx.x * kThreads + threadIdx.x; u < U; u += stride) {
+    const uint32_t b = uniq[u];
+    const uint64_t o = owner_at[b];
+    if (o > fp_base) holder[b] = idn[o - 1];
   }
 }
 
@@ -1066,11 +1089,14 @@ __global__ void __launch_bounds__(kThreads) k_flips(uint32_t* __restrict__ pool3
   atomicXor(pool32 + (addr >> 2), 1u << ((addr & 3) * 8 + (bits[f] & 7)));
 }
 
-__global__ void __launch_bounds__(kThreads) k_set_failed(uint8_t* __restrict__ load_failed,
-                                                         uint32_t n,
-                                                         const uint32_t* __restrict__ blocks) {
+// Reported load failures: the block's latest failure takes the restore's
+// generation (every claim that recorded the block at an earlier generation
+// now fails there).
+__global__ void __launch_bounds__(kThreads) k_set_failed(BlockRes* __restrict__ bres, uint32_t n,
+                                                         const uint32_t* __restrict__ blocks,
+                                                         uint64_t gen) {
   const uint32_t f = blockIdx.x * kThreads + threadIdx.x;
-  if (f < n) load_failed[blocks[f]] = 1;
+  if (f < n) bres[blocks[f]].fail_gen = gen;
 }
 
 // Copy staged blocks (those in the unique list) back into the pool.
@@ -1121,9 +1147,7 @@ __global__ void __launch_bounds__(kThreads) k_restore_claims(BatchDev b, RegDev 
 // ------------------------------------------------------------------- check
 
 struct CheckState {
-  const uint64_t* d_off;
-  const uint64_t* d_res;
-  const uint8_t* bstat;
+  const BlockRes* bres;
 };
 
 template <int W>
@@ -1146,7 +1170,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   uint64_t special = kNoKey;  // claim-level and length keys
   int64_t slot = -1;
   uint32_t na = 0, state = 0, pred = r.n;
-  uint64_t acc_ntok = 0, acc_chain = 0, fpo = 0, q3 = kNoKey;
+  uint64_t acc_ntok = 0, acc_chain = 0, fpo = 0, q3 = kNoKey, acc_gen = 0;
   if (r.malformed) {
     reasons |= CLAIM_R_MALFORMED;
     special = kClaimLevelKey;
@@ -1163,6 +1187,7 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       acc_ntok = e.ntok;
       acc_chain = e.chain;
       fpo = e.fpoff;
+      acc_gen = e.gen;
       if (!(state & kStOffloaded)) {
         reasons |= CLAIM_R_NOT_OFFLOADED;
         special = kClaimLevelKey;
@@ -1229,16 +1254,19 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
   const uint64_t L = n > nt ? n : nt;
   // Wide groups (long claims, many windows) load a window's position loads
   // and first token chunk during the previous window, so that a window
-  // waits for one round trip (its status bytes) instead of two.
+  // waits for one round trip (its block records) instead of two.
   constexpr bool kAhead = W >= 16;
   auto count_of = [&](uint64_t p) { return r.ntok - p * bs < bs ? r.ntok - p * bs : (uint64_t)bs; };
   uint32_t nx_blk = kNone, nx_acc_blk = kNone;
-  uint64_t nx_acc_h = 0;
+  uint64_t nx_acc_h = 0, nx_acc_d = 0;
   uint32_t nx_ch[kAhead ? 16 : 1];
   if constexpr (kAhead) {
     const uint64_t j = gl;
     if (j < n) nx_blk = b.bi[(uint64_t)r.bo0 + j];
-    if (found && j < common) nx_acc_blk = reg.fp[fpo + j];
+    if (found && j < common) {
+      nx_acc_blk = reg.fp[fpo + j];
+      nx_acc_d = reg.dig[fpo + j];
+    }
     if (j < id_pos) nx_acc_h = reg.idn[fpo + j];
     if (j < nt) prefetch_chunk(nx_ch, b.tok, r.to0 + j * bs, count_of(j));
   }
@@ -1246,29 +1274,36 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     const uint64_t j = j0 + gl;
     // the window's loads that depend only on j, issued together
     uint32_t blk = kNone, acc_blk = kNone;
-    uint64_t acc_h = 0;
+    uint64_t acc_h = 0, acc_d = 0;
     uint64_t m_sum = 0;
     if constexpr (kAhead) {
       blk = nx_blk;
       acc_blk = nx_acc_blk;
       acc_h = nx_acc_h;
+      acc_d = nx_acc_d;
       if (j < nt) m_sum = multilinear_prefetched<1>(nx_ch, b.tok, r.to0 + j * bs, count_of(j), tkey);
     } else {
       if (j < n) blk = b.bi[(uint64_t)r.bo0 + j];
-      if (found && j < common) acc_blk = reg.fp[fpo + j];
+      if (found && j < common) {
+        acc_blk = reg.fp[fpo + j];
+        acc_d = reg.dig[fpo + j];
+      }
       if (j < id_pos) acc_h = reg.idn[fpo + j];
       // the token loads go out first (they do not wait for blk)
       if (j < nt) m_sum = block_multilinear<1>(b.tok, r.to0 + j * bs, count_of(j), tkey);
     }
-    // per-block state, loaded unconditionally (block 0 stands in for a
-    // lane without a pool block) so that it is in flight while the identity
-    // step runs; the empty asm keeps every use, and so the wait, after it
+    // the block's record (restored digest, latest reported failure), loaded
+    // unconditionally (block 0 stands in for a lane without a pool block)
+    // so that it is in flight while the identity step runs; the empty asm
+    // keeps every use, and so the wait, after it
     const uint32_t sb = (j < n && blk < nb) ? blk : 0u;
-    uint32_t bst = st.bstat[sb];
-    if constexpr (kAhead) {  // the next window's loads, issued after the status byte's
+    u32x4 brec = *(const u32x4*)(st.bres + sb);
+    if constexpr (kAhead) {  // the next window's loads, issued after the record's
       const uint64_t jn = j + W;
       nx_blk = jn < n ? b.bi[(uint64_t)r.bo0 + jn] : kNone;
-      nx_acc_blk = found && jn < common ? reg.fp[fpo + jn] : kNone;
+      const bool has = found && jn < common;
+      nx_acc_blk = has ? reg.fp[fpo + jn] : kNone;
+      nx_acc_d = has ? reg.dig[fpo + jn] : 0;
       nx_acc_h = jn < id_pos ? reg.idn[fpo + jn] : 0;
       if (jn < nt) prefetch_chunk(nx_ch, b.tok, r.to0 + jn * bs, count_of(jn));
     }
@@ -1276,11 +1311,12 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     const uint64_t up = prev_lane64(acc_h);  // group lane gl-1's accepted identity
     const uint64_t hh = splitmix_step((gl == 0 ? carry : up) ^ m_sum);
     carry = group_read64<W>(acc_h, gbase, W - 1);
-    asm volatile("" : "+v"(bst));
+    asm volatile("" : "+v"(brec));
     const bool mism = j < id_pos && hh != acc_h;
 
     uint64_t my_key = kNoKey;
     if (j < n) {
+      const bool own = found && j < common && blk == acc_blk;  // the claim recorded this block here
       if (found && j < common && blk != acc_blk) {
         reasons |= CLAIM_R_FOOTPRINT_MISMATCH;
         my_key = j;
@@ -1288,12 +1324,18 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
       if (blk >= nb) {
         reasons |= CLAIM_R_MISSING_ENTRY;
         my_key = j < my_key ? j : my_key;
-      } else if (!(bst & kBsRecord)) {
+      } else if (!found) {
+        // a claim that was never accepted holds no offload record
+      } else if (!own) {
         reasons |= CLAIM_R_NO_OFFLOAD_RECORD;
         my_key = j < my_key ? j : my_key;
       } else {
-        const bool lf = (bst & kBsLoadFailed) != 0;
-        const bool mm = (bst & kBsMismatch) != 0;
+        // the claim's own record: a failure reported after its offload, or
+        // a restored digest different from its own offload digest
+        const uint64_t d_res = ((uint64_t)brec.y << 32) | brec.x;
+        const uint64_t fail_gen = ((uint64_t)brec.w << 32) | brec.z;
+        const bool lf = fail_gen > acc_gen;
+        const bool mm = d_res != acc_d;
         if ((lf || mm) && j < intact) intact = j;
         if (j >= pred) {
           // past the predicate: the claimed prefix is still intact
@@ -1405,9 +1447,9 @@ __global__ void __launch_bounds__(kThreads) k_check(BatchDev b, RegDev reg, Chec
     o.code = cls == 0 ? CLAIM_UNKNOWN : CLAIM_RESTORE_FAILED_FAIL_CLOSED;
     o.first_failing_block = js;
     o.phys_block = (uint64_t)js < n ? b.bi[(uint64_t)r.bo0 + js] : kNone;
-    if (cls == 1) {
-      o.expected_digest = st.d_off[o.phys_block];
-      o.observed_digest = st.d_res[o.phys_block];
+    if (cls == 1) {  // a class-1 key is always at a position the claim recorded
+      o.expected_digest = reg.dig[fpo + js];
+      o.observed_digest = st.bres[o.phys_block].d_res;
     }
     if (js != kNone && (uint64_t)js < nt) o.chain_hash_at_fail = h_js;
     if (cls == 1) {
@@ -1450,8 +1492,10 @@ __device__ __forceinline__ int64_t id_probe_resolve(const IdDev& t, uint64_t key
 }
 
 // Reuse lookup: one group of W lanes per request; the group stops at the
-// first token block whose identity is not a plain hit (absent, or
-// registered but ambiguous).
+// first token block whose identity is not a plain hit (absent, registered
+// but ambiguous, or stale: its block was registered since under another
+// identity, so it no longer holds this prefix; a stale identity stops the
+// walk as an absent one does).
 //
 // Narrow groups (requests of a few blocks) hash one token block per lane,
 // run the chain through the group and probe every lane's h_j.
@@ -1473,8 +1517,9 @@ __device__ __forceinline__ int64_t id_probe_resolve(const IdDev& t, uint64_t key
 // serial chain's.
 template <int W>
 __global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids,
-                                                     const uint64_t* __restrict__ idn, uint32_t bs,
-                                                     uint64_t seed,
+                                                     const uint64_t* __restrict__ idn,
+                                                     const uint64_t* __restrict__ holder,
+                                                     uint32_t bs, uint64_t seed,
                                                      claim_lookup_result* __restrict__ out) {
   __shared__ uint64_t tkey[kMaxBlockSize];
   load_token_keys(tkey, bs, seed);
@@ -1529,14 +1574,15 @@ __global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids,
       if (pre && jn < nt) prefetch_chunk(ch, b.tok, to0 + jn * bs, count_of(jn));
       if (pre_has) pre_acc = idn[a + W + gl];
       int64_t my_e = -1;
-      bool amb = false;
+      bool amb = false, stale = false;
       if (probe) {
         my_e = id_probe_resolve(ids, my_h, home);
         const uint64_t home_slot = my_h == 0 ? ids.mask + 1 : slot_of_id(my_h, ids.mask);
-        amb = my_e >= 0 &&
-              (((uint64_t)my_e == home_slot ? home.w : ids.e[my_e].flags) & kIdAmbiguous);
+        const bool at_home = (uint64_t)my_e == home_slot;
+        amb = my_e >= 0 && ((at_home ? home.w : ids.e[my_e].flags) & kIdAmbiguous);
+        if (my_e >= 0 && !amb) stale = holder[at_home ? home.z : ids.e[my_e].block] != my_h;
       }
-      const uint64_t miss = group_ballot<W>(probe && my_e < 0);
+      const uint64_t miss = group_ballot<W>(probe && (my_e < 0 || stale));
       const uint64_t stops = miss | group_ballot<W>(amb);
       if (stops) {  // the first position that is not a plain hit
         const uint32_t p = (uint32_t)__builtin_ctzll(stops);
@@ -1576,6 +1622,8 @@ __global__ void __launch_bounds__(kThreads) k_lookup(BatchDev b, IdDev ids,
           my_stop = (j << 1) | 1u;
         else if (e->flags & kIdAmbiguous)
           my_stop = j << 1;
+        else if (holder[e->block] != my_h)
+          my_stop = (j << 1) | 1u;  // stale: stops as an absent identity does
       }
       stop = group_min64<W>(my_stop);
       if (stop == kNoKey) {
@@ -1799,15 +1847,19 @@ struct claim_pool {
   int lpw = 32;
   uint32_t segs = 1, ps_total = 1, pgs = 1, groups = 1;
 
-  uint64_t *d_off = nullptr, *d_res = nullptr, *partial = nullptr;
-  uint8_t *valid_off = nullptr, *load_failed = nullptr, *mark = nullptr;
-  uint8_t* bstat = nullptr;  // per-block status of the last check (kBs* bits)
+  uint64_t *d_off = nullptr, *partial = nullptr;
+  BlockRes* bres = nullptr;  // per block: restored digest, latest reported failure
+  uint8_t *valid_off = nullptr, *mark = nullptr;
   uint32_t *uniq = nullptr, *slot_of = nullptr;
+  uint64_t* owner_at = nullptr;  // per block: identity-store index + 1 of its latest registration
+  uint64_t* holder = nullptr;    // per block: the identity of that registration
+  uint64_t gen = 0;              // generation of the latest offload or restore call
 
   uint64_t reg_mask = 0, max_claims = 0;
   RegEntry* reg = nullptr;
   uint32_t* fp_store = nullptr;
   uint64_t* idn_store = nullptr;  // accepted identities, parallel to fp_store
+  uint64_t* dig_store = nullptr;  // each claim's own offload digests, parallel to fp_store
   uint64_t max_fp = 0, fp_used = 0;
   IdEntry* id_table = nullptr;
   IdSrc* id_src = nullptr;  // parallel to id_table
@@ -1930,6 +1982,7 @@ RegDev reg_dev(claim_pool* P) {
   r.e = P->reg;
   r.fp = P->fp_store;
   r.idn = P->idn_store;
+  r.dig = P->dig_store;
   return r;
 }
 
@@ -2067,9 +2120,8 @@ int launch_digest(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_
 int launch_finalize(claim_pool* P, int mode, int staged) {
   const uint32_t grid = grid_for((uint64_t)P->nb + P->groups);  // slots <= U + groups
   hipLaunchKernelGGL(k_finalize, dim3(grid), dim3(kThreads), 0, P->stream, P->uniq, P->ctr,
-                     P->partial, P->pgs, P->groups, mode, staged,
-                     mode == 0 ? P->d_off : P->d_res, P->d_off, P->valid_off, P->load_failed,
-                     P->slot_of, P->bstat);
+                     P->partial, P->pgs, P->groups, mode, staged, P->d_off, P->valid_off,
+                     P->slot_of, P->bres);
   return hip_status(hipGetLastError());
 }
 
@@ -2164,11 +2216,11 @@ int choose_digest_shape(claim_pool* P) {
 
 void free_pool(claim_pool* P) {
   if (!P) return;
-  void* ptrs[] = {P->d_off,    P->d_res,    P->partial, P->valid_off, P->load_failed, P->bstat,
-                  P->mark,     P->uniq,     P->slot_of, P->reg,       P->fp_store,
-                  P->log,      P->ctr,      P->outcomes, P->cnt,      P->pend,
-                  P->tsum,     P->dup_table, P->f_blocks, P->f_bits,   P->idn_store,
-                  P->id_table, P->id_src,    P->fpo};
+  void* ptrs[] = {P->d_off,    P->bres,      P->partial,  P->valid_off, P->mark,
+                  P->uniq,     P->slot_of,   P->owner_at, P->holder,    P->reg,
+                  P->fp_store, P->idn_store, P->dig_store, P->log,      P->ctr,
+                  P->outcomes, P->cnt,       P->pend,     P->tsum,      P->dup_table,
+                  P->f_blocks, P->f_bits,    P->id_table, P->id_src,    P->fpo};
   for (void* p : ptrs)
     if (p) dfree(p);
   if (P->host_ctr) (void)hipHostFree(P->host_ctr);
@@ -2281,12 +2333,11 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     if ((rc = choose_digest_shape(P))) break;
 
     const uint64_t nb = d->num_blocks;
-    if ((rc = dalloc(&P->d_off, nb)) || (rc = dalloc(&P->d_res, nb)) ||
+    if ((rc = dalloc(&P->d_off, nb)) || (rc = dalloc(&P->bres, nb)) ||
         (rc = dalloc(&P->partial, (uint64_t)P->pgs * (nb + P->groups))) ||
-        (rc = dalloc(&P->valid_off, nb)) ||
-        (rc = dalloc(&P->load_failed, nb)) || (rc = dalloc(&P->bstat, nb)) ||
-        (rc = dalloc(&P->mark, (nb + 15) / 16 * 16)) ||
-        (rc = dalloc(&P->uniq, nb)) || (rc = dalloc(&P->slot_of, nb)))
+        (rc = dalloc(&P->valid_off, nb)) || (rc = dalloc(&P->mark, (nb + 15) / 16 * 16)) ||
+        (rc = dalloc(&P->uniq, nb)) || (rc = dalloc(&P->slot_of, nb)) ||
+        (rc = dalloc(&P->owner_at, nb)) || (rc = dalloc(&P->holder, nb)))
       break;
     P->max_claims = d->max_claims;
     const uint64_t cap = next_pow2(2 * d->max_claims);
@@ -2295,6 +2346,7 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
     P->max_fp = d->max_footprint;
     if ((rc = dalloc(&P->fp_store, d->max_footprint))) break;
     if ((rc = dalloc(&P->idn_store, d->max_footprint))) break;
+    if ((rc = dalloc(&P->dig_store, d->max_footprint))) break;
     // every registered identity is a footprint position: at most half full
     const uint64_t id_cap = next_pow2(2 * d->max_footprint < 64 ? 64 : 2 * d->max_footprint);
     P->id_mask = id_cap - 1;
@@ -2314,9 +2366,10 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
       if (!ok) { rc = CLAIM_EHIP; break; }
       P->tev_made = true;
     }
-    if ((rc = fill<uint64_t>(P, P->d_off, nb, 0)) || (rc = fill<uint64_t>(P, P->d_res, nb, 0)) ||
-        (rc = fill<uint8_t>(P, P->valid_off, nb, 0)) || (rc = fill<uint8_t>(P, P->load_failed, nb, 0)) ||
-        (rc = fill<uint8_t>(P, P->bstat, nb, 0)) ||
+    if ((rc = fill<uint64_t>(P, P->d_off, nb, 0)) ||
+        (rc = fill<uint64_t>(P, (uint64_t*)P->bres, 2 * nb, 0)) ||
+        (rc = fill<uint8_t>(P, P->valid_off, nb, 0)) ||
+        (rc = fill<uint64_t>(P, P->owner_at, nb, 0)) || (rc = fill<uint64_t>(P, P->holder, nb, 0)) ||
         (rc = fill<uint8_t>(P, P->mark, (nb + 15) / 16 * 16, 0)) || (rc = fill<uint32_t>(P, P->slot_of, nb, kNone)) ||
         (rc = fill<uint64_t>(P, (uint64_t*)P->reg, cap * (sizeof(RegEntry) / 8), 0)) ||
         (rc = fill_strided_u64(P, (uint64_t*)P->reg, cap, sizeof(RegEntry) / 8, kEmptyId)))
@@ -2383,21 +2436,26 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
   }
   if (P->fp_used + fp_need > P->max_fp) return CLAIM_ENOSPC;  // nothing changed
 
-  // acceptance
-  if (C) {
-    LAUNCH_GROUPED(k_accept, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->seed, P->fp_used, fpo,
-                   P->fp_store, P->ctr, P->cnt, P->pend);
-    hipLaunchKernelGGL(k_register_claims, dim3(grid_for(C, 0x7FFFFFFFu)), dim3(kThreads), 0,
-                       P->stream, bd, rd, P->bs, P->fp_used, fpo, P->pend, P->ctr);
-    HIP_TRY(hipGetLastError());
-    LAUNCH_GROUPED(k_register_owners, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->fp_used, fpo,
-                   P->ctr);
-    TRY(append_events(P, b));
-  }
-  // offload record; a staged offload replaces every earlier staging slot
+  // the offload digest of every block the batch references (a staged
+  // offload replaces every earlier staging slot); acceptance then copies
+  // each claim's digests into its own offload record
+  P->gen += 1;
   if (staging) TRY(fill<uint32_t>(P, P->slot_of, P->nb, kNone));
   TRY(launch_digest(P, P->partial, staging));
   TRY(launch_finalize(P, 0, staging != nullptr));
+  if (C) {
+    LAUNCH_GROUPED(k_accept, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->seed, P->fp_used, fpo,
+                   P->d_off, P->fp_store, P->ctr, P->cnt, P->pend);
+    hipLaunchKernelGGL(k_register_claims, dim3(grid_for(C, 0x7FFFFFFFu)), dim3(kThreads), 0,
+                       P->stream, bd, rd, P->bs, P->fp_used, P->gen, fpo, P->pend, P->ctr);
+    HIP_TRY(hipGetLastError());
+    LAUNCH_GROUPED(k_register_owners, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->fp_used, fpo,
+                   P->owner_at, P->ctr);
+    hipLaunchKernelGGL(k_holders, dim3(grid_for(U ? U : 1, 4096)), dim3(kThreads), 0, P->stream,
+                       P->uniq, P->ctr, P->owner_at, P->idn_store, P->fp_used, P->holder);
+    HIP_TRY(hipGetLastError());
+    TRY(append_events(P, b));
+  }
   TRY(read_counters(P));
   P->fp_used += fp_need;
   if (staging) P->staged_blocks = U;
@@ -2456,11 +2514,12 @@ int claim_restore(claim_pool* P, const claim_batch* b, const void* staging,
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipStreamSynchronize(P->stream));  // the fault lists may be reused next
   }
+  P->gen += 1;
   if (nfail) {
     HIP_TRY(hipMemcpyAsync(P->f_blocks, f->load_failed_blocks, nfail * sizeof(uint32_t),
                            hipMemcpyHostToDevice, P->stream));
-    hipLaunchKernelGGL(k_set_failed, dim3(grid_for(nfail)), dim3(kThreads), 0, P->stream,
-                       P->load_failed, nfail, P->f_blocks);
+    hipLaunchKernelGGL(k_set_failed, dim3(grid_for(nfail)), dim3(kThreads), 0, P->stream, P->bres,
+                       nfail, P->f_blocks, P->gen);
     HIP_TRY(hipGetLastError());
     HIP_TRY(hipStreamSynchronize(P->stream));
   }
@@ -2488,13 +2547,7 @@ int claim_check(claim_pool* P, const claim_batch* b) {
     slot = P->t_head;
   }
   TRY(record_stage(P, slot, 0));
-  if (b->num_refs) {
-    hipLaunchKernelGGL(k_mark_entries, dim3(grid_for(b->num_refs, 8192)), dim3(kThreads), 0,
-                       P->stream, b->block_ids, b->num_refs, P->nb, P->valid_off, P->mark);
-    HIP_TRY(hipGetLastError());
-  }
-  hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, P->stream, P->mark, P->nb, P->uniq, P->ctr);
-  HIP_TRY(hipGetLastError());
+  TRY(select_blocks(P, b, kMarkOffloaded));  // recorded blocks of the well-formed rows
   TRY(record_stage(P, slot, 1));
   TRY(launch_digest(P, P->partial, nullptr));
   TRY(record_stage(P, slot, 2));
@@ -2502,9 +2555,7 @@ int claim_check(claim_pool* P, const claim_batch* b) {
   TRY(record_stage(P, slot, 3));
   if (C) {
     CheckState st;
-    st.d_off = P->d_off;
-    st.d_res = P->d_res;
-    st.bstat = P->bstat;
+    st.bres = P->bres;
     LAUNCH_GROUPED(k_check, P, b, batch_dev(b), reg_dev(P), st, P->nb, P->bs, P->seed, P->outcomes,
                    P->cnt, P->pend);
   }
@@ -2531,7 +2582,7 @@ int claim_lookup(claim_pool* P, const claim_batch* b, claim_lookup_result* out,
   if (b->num_claims == 0) return CLAIM_OK;
   HIP_TRY(hipSetDevice(P->device));
   LAUNCH_GROUPED_W(k_lookup, P, b, lookup_group_width(b, P->bs), batch_dev(b), id_dev(P),
-                   P->idn_store, P->bs, P->seed, out);
+                   P->idn_store, P->holder, P->bs, P->seed, out);
   return CLAIM_OK;
 }
 
@@ -2577,10 +2628,21 @@ int claim_block_state_read(claim_pool* P, uint32_t first, uint32_t count, uint64
   HIP_TRY(hipStreamSynchronize(P->stream));
   if (count == 0) return CLAIM_OK;
   if (d_off) HIP_TRY(hipMemcpy(d_off, P->d_off + first, count * 8ull, hipMemcpyDeviceToHost));
-  if (d_res) HIP_TRY(hipMemcpy(d_res, P->d_res + first, count * 8ull, hipMemcpyDeviceToHost));
   if (valid_off) HIP_TRY(hipMemcpy(valid_off, P->valid_off + first, count, hipMemcpyDeviceToHost));
-  if (load_failed)
-    HIP_TRY(hipMemcpy(load_failed, P->load_failed + first, count, hipMemcpyDeviceToHost));
+  // the per-block records, 16 bytes apart: restored digests and failure generations
+  if (d_res)
+    HIP_TRY(hipMemcpy2D(d_res, 8, &P->bres[first].d_res, sizeof(BlockRes), 8, count,
+                        hipMemcpyDeviceToHost));
+  if (load_failed) {
+    uint64_t* gen = new (std::nothrow) uint64_t[count];
+    if (!gen) return CLAIM_ENOMEM;
+    const hipError_t e = hipMemcpy2D(gen, 8, &P->bres[first].fail_gen, sizeof(BlockRes), 8, count,
+                                     hipMemcpyDeviceToHost);
+    if (e == hipSuccess)
+      for (uint32_t i = 0; i < count; ++i) load_failed[i] = gen[i] != 0;
+    delete[] gen;
+    HIP_TRY(e);
+  }
   return CLAIM_OK;
 }
 

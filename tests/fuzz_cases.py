@@ -4,8 +4,11 @@ irregularity the batch format allows (empty and long rows, missing and
 out-of-range entries, rows whose offsets run backwards or past the arrays,
 rows that share entries, reserved and repeated ids, token rows that do not
 match the block rows, predicates), faults, and check and lookup batches
-that present the claims again with changes.  Inputs only: nothing here
-computes the method's arithmetic."""
+that present the claims again with changes.  Between the two offloads a
+restore of the first batch reports load failures and changes bytes, and the
+second batch re-offloads some of those blocks under other claims (a
+recompute stored by another claim, or other bytes).  Inputs only: nothing
+here computes the method's arithmetic."""
 
 from __future__ import annotations
 
@@ -32,6 +35,8 @@ class Case:
     size: str
     staged: bool  # the second offload stages its blocks, the restore copies them back
     offload: list  # batches offloaded in turn
+    mid: Batch  # restored (with mid_faults) after the first offload, before the second
+    mid_faults: FaultSpec
     restore: Batch
     faults: FaultSpec
     check: Batch
@@ -129,6 +134,23 @@ def make_case(seed: int) -> Case:
         if blks.size and rng.random() < 0.5:
             blks[0] = int(rng.integers(0, g.num_blocks))
         second.append((int(ids[10100]), blks, src[2].copy()))
+    # between the offloads: a restore of some first-batch claims that reports
+    # load failures and flips bytes of blocks they hold; the second batch then
+    # re-offloads some of those blocks under a new claim
+    held = [int(x) for _, blks, _ in first for x in blks if x < g.num_blocks]
+    mid_rows = [r for r in first if rng.random() < 0.7]
+    touched = (rng.choice(held, size=min(len(held), int(rng.integers(1, 4))), replace=False)
+               if held and rng.random() < 0.8 else np.zeros(0, np.int64))
+    lost = touched[: int(rng.integers(0, touched.size + 1))]
+    flipped = np.setdiff1d(touched, lost) if rng.random() < 0.5 else touched
+    mid_faults = FaultSpec(np.asarray(flipped, np.uint32),
+                           rng.integers(0, 8 * g.block_bytes, size=flipped.size).astype(np.uint64),
+                           np.asarray(lost, np.uint32))
+    if touched.size:
+        n_re = int(rng.integers(1, 4))
+        blks = np.concatenate([touched, rng.integers(0, g.num_blocks, size=n_re)]).astype(np.uint32)
+        rng.shuffle(blks)
+        second.append((int(ids[10150]), blks, _tokens(rng, blks.size * g.block_size)))
     b1 = _bend(rng, from_claims(first))
     b1.predicate_tokens = (rng.integers(0, 80, size=b1.num_claims).astype(np.uint64)
                            if rng.random() < 0.4 else None)
@@ -144,7 +166,8 @@ def make_case(seed: int) -> Case:
     reqs = [(int(i), [], p[2][: int(rng.integers(0, p[2].size + 1))] if rng.random() < 0.3 else p[2])
             for i, p in zip(ids[12000:], accepted)]
     lookup = _bend(rng, from_claims(reqs + [(int(ids[10300]), [], _tokens(rng, 3 * g.block_size))]))
-    return Case(w, size, seed % 3 == 0, [b1, b2], restore, flips, check, lookup)
+    return Case(w, size, seed % 3 == 0, [b1, b2], from_claims(mid_rows), mid_faults, restore, flips,
+                check, lookup)
 
 
 

@@ -21,6 +21,7 @@ import pytest
 from oracle import oracle as O
 from paper_2606_01387_amd.synth import FaultSpec, Geometry, Workload, content, make_batch, make_faults
 from tests.helpers import apply_flips, digests
+from tests.test_gpu_parity import free_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -204,3 +205,116 @@ def test_mutation_controls(torch, ck, seed):
     assert (out["reasons"][token] & ck.R_TOKEN_MISMATCH).all()
     assert len(ev) == batch.num_claims  # one terminal event each, none refused
     del kv
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_attribution_after_reoffload(torch, ck, seed):
+    """The controls when blocks are offloaded again (section 5
+    storage_restorability row; Table 9 fallback-recompute and wrong-claim
+    rows).  Batch A is offloaded, restored with faults and checked; then
+    some corrupted blocks are rewritten to their original bytes (a
+    recompute), other blocks get new flips, and batch B (new claims)
+    re-offloads blocks of A, among them blocks whose load failed; then A
+    and B are restored (a few more reported failures) and checked together.
+    GPU equals oracle, and every claim's outcome follows a ledger of its own
+    offload-time bytes: it fails closed at the first position whose bytes
+    now differ from its own offload's, or whose block had a load failure
+    reported after its offload; otherwise it is materialized."""
+    w, batch_a, faults = seeded(100 + seed)
+    g = w.geometry
+    rng = np.random.default_rng(seed)
+    host0 = content.pool_host(g, w.content_seed)
+    after1 = apply_flips(host0, w, faults)
+    # the rewrite: cancel half of the first flips (recompute of the original
+    # bytes), add new flips on referenced blocks
+    half = faults.flip_blocks.size // 2
+    ref_a = batch_a.unique_blocks(g.num_blocks)
+    new_blocks = rng.choice(ref_a, size=6, replace=False).astype(np.uint32)
+    rewrite = FaultSpec(np.concatenate([faults.flip_blocks[:half], new_blocks]).astype(np.uint32),
+                        np.concatenate([faults.flip_bits[:half],
+                                        rng.integers(0, 8 * g.block_bytes, size=6)]).astype(np.uint64),
+                        np.zeros(0, np.uint32))
+    after2 = apply_flips(after1, w, rewrite)
+    # batch B: new claims over blocks of A (failed, rewritten, others)
+    hot = np.unique(np.concatenate([faults.load_failed, faults.flip_blocks, new_blocks])).astype(np.int64)
+    rows = []
+    for k in range(40):
+        n = int(rng.integers(1, 5))
+        pick = np.where(rng.random(n) < 0.5, rng.choice(hot, size=n), rng.choice(ref_a, size=n))
+        rows.append((int(5_000_000 + k), pick.astype(np.uint32),
+                     rng.integers(0, 32000, size=n * g.block_size, dtype=np.uint32)))
+    from paper_2606_01387_amd.synth import from_claims
+    batch_b = from_claims(rows)
+    both = from_claims([batch_a.claim(c) for c in range(batch_a.num_claims)] + rows)
+    late_lost = rng.choice(hot, size=2, replace=False).astype(np.uint32)
+    final = FaultSpec(np.zeros(0, np.uint32), np.zeros(0, np.uint64), late_lost)
+    print(f"re-offload seed {seed}: A {batch_a.num_claims} claims, B {batch_b.num_claims}, "
+          f"{half} flips cancelled, 6 new flips, late failures {late_lost.tolist()}", flush=True)
+
+    kv = torch.empty(g.pool_bytes, dtype=torch.uint8, device="cuda")
+    content.fill_pool_gpu(kv.data_ptr(), kv.numel(), g, w.content_seed,
+                          torch.cuda.current_stream().cuda_stream)
+    with ck.Pool(g, w.seed, kv, max_claims=512, max_footprint=8192, event_capacity=8192) as pool:
+        pool.offload(ck.DeviceBatch(batch_a))
+        pool.restore(ck.DeviceBatch(batch_a), faults=faults)
+        pool.check(ck.DeviceBatch(batch_a))
+        out1, _ = pool.read()
+        pool.restore(ck.DeviceBatch(from_claims([])), faults=rewrite)
+        pool.offload(ck.DeviceBatch(batch_b))
+        pool.restore(ck.DeviceBatch(both), faults=final)
+        pool.read()  # drop the events before the check
+        pool.check(ck.DeviceBatch(both))
+        out2, ev2 = pool.read()
+        pool.stream.synchronize()
+        assert np.array_equal(kv.cpu().numpy(), after2)
+
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    op.offload(batch_a, digests(host0, w))
+    op.restore(batch_a, faults.load_failed)
+    want1 = op.check(batch_a, digests(after1, w))
+    op.restore(from_claims([]), rewrite.load_failed)
+    op.offload(batch_b, digests(after2, w))
+    op.restore(both, final.load_failed)
+    op.events(clear=True)
+    want2 = op.check(both, digests(after2, w))
+    for f in want2.dtype.names:
+        if f != "pad":
+            assert np.array_equal(out1[f], want1[f]), f
+            assert np.array_equal(out2[f], want2[f]), f
+    want_ev = op.events()
+    for f in ("claim_id", "aux", "kind", "block_index", "phys_block"):
+        assert np.array_equal(ev2[f], want_ev[f]), f
+
+    # the ledger: call 1 offload A, 2 restore (first failures), 3 rewrite,
+    # 4 offload B, 5 restore (late failures)
+    reported = [(int(b), 2) for b in faults.load_failed] + [(int(b), 5) for b in late_lost]
+    canon = {}
+
+    def block_bytes(pool_bytes, b):
+        key = (id(pool_bytes), b)
+        if key not in canon:
+            canon[key] = O.canonical_block(pool_bytes, g.planes, g.num_blocks, g.chunk_bytes, b)
+        return canon[key]
+
+    kinds = {"materialized": 0, "failed_a": 0, "failed_b": 0, "a_kept_failed_after_b": 0}
+    b_blocks = set(int(x) for x in batch_b.block_ids)
+    for c in range(both.num_claims):
+        _, blks, _ = both.claim(c)
+        in_a = c < batch_a.num_claims
+        snap, at = (host0, 1) if in_a else (after2, 4)
+        bad = [j for j, b in enumerate(blks)
+               if any(rb == int(b) and rc > at for rb, rc in reported)
+               or not np.array_equal(block_bytes(after2, int(b)), block_bytes(snap, int(b)))]
+        if bad:
+            assert out2[c]["code"] == ck.RESTORE_FAILED_FAIL_CLOSED, (seed, c, bad)
+            assert out2[c]["first_failing_block"] == bad[0]
+            kinds["failed_a" if in_a else "failed_b"] += 1
+            if in_a and int(blks[bad[0]]) in b_blocks:
+                kinds["a_kept_failed_after_b"] += 1
+        else:
+            assert out2[c]["code"] == ck.MATERIALIZED, (seed, c)
+            kinds["materialized"] += 1
+    print(f"  {kinds}", flush=True)
+    assert kinds["a_kept_failed_after_b"] > 0  # B re-offloaded a block A failed on
+    del kv
+    free_gpu(torch)

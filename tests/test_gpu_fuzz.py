@@ -5,9 +5,12 @@ and entry-sharing rows, reserved ids and predicates, shared and
 duplicate-owned identities, faults, a partial restore (in a third of the
 cases from device staging written by the second offload, after the staged
 blocks' device copies are zeroed), a check batch that presents the claims
-again reordered, repeated and changed, and lookups.  The pool's bytes after
-the restore must equal the host model, and every status, outcome field,
-event, per-block digest, lookup field and identity count the oracle's."""
+again reordered, repeated and changed, and lookups; between the two
+offloads a restore of first-batch claims reports load failures and flips
+bytes of their blocks, which the second batch re-offloads under another
+claim.  The pool's bytes after the restore must equal the host model, and
+every status, outcome field, event, per-block digest, lookup field and
+identity count the oracle's."""
 
 import numpy as np
 import pytest
@@ -49,8 +52,15 @@ def test_fuzz_lifecycle(torch, ck, seed):
     op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
     kv = gpu_pool_tensor(torch, w)
     staging, restored = None, host.copy()
+    print(f"  mid restore {case.mid.num_claims} claims, {case.mid_faults.flip_blocks.size} flips, "
+          f"{case.mid_faults.load_failed.size} load failures", flush=True)
     with ck.Pool(g, w.seed, kv, **capacities(case)) as pool:
         for i, b in enumerate(case.offload):
+            if i == 1:  # the restore between the offloads: failures, changed bytes
+                pool.restore(ck.DeviceBatch(case.mid), faults=case.mid_faults)
+                assert op.restore(case.mid, case.mid_faults.load_failed) == O.OK
+                host = apply_flips(host, w, case.mid_faults)
+                restored = host.copy()
             want = op.offload(b, digests(host, w))
             if case.staged and i == len(case.offload) - 1:
                 staged = well_formed_blocks(b, g.num_blocks)

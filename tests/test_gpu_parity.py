@@ -251,6 +251,29 @@ class Mirror:
         self.host = apply_flips(self.host, self.w, f)
         assert self.op.restore(batch, f.load_failed) == O.OK
 
+    def rewrite(self, block, canon):
+        """Replace block's bytes (canonical order) on the GPU pool and the host copy."""
+        g = self.w.geometry
+        self.pool.stream.synchronize()
+        src = self.torch.from_numpy(np.ascontiguousarray(canon).reshape(g.planes, g.chunk_bytes)).cuda()
+        self.kv.view(g.planes, g.num_blocks, g.chunk_bytes)[:, block, :] = src
+        self.torch.cuda.synchronize()
+        self.host.reshape(g.planes, g.num_blocks, g.chunk_bytes)[:, block, :] = \
+            np.ascontiguousarray(canon).reshape(g.planes, g.chunk_bytes)
+
+    def canonical(self, block):
+        g = self.w.geometry
+        return O.canonical_block(self.host, g.planes, g.num_blocks, g.chunk_bytes, block)
+
+    def lookup(self, batch):
+        got = self.pool.lookup(self.ck.DeviceBatch(batch))
+        want = self.op.lookup(batch)
+        for f in want.dtype.names:
+            if f != "pad":
+                assert np.array_equal(got[f], want[f]), f
+        assert self.pool.identity_stats() == self.op.identity_stats()
+        return got
+
     def check(self, batch):
         self.pool.check(self.ck.DeviceBatch(batch))
         want = self.op.check(batch, digests(self.host, self.w))
@@ -332,11 +355,18 @@ def test_controls_mirrored(torch, ck):
     assert out["code"].tolist() == [ck_.MATERIALIZED, ck_.RESTORE_FAILED_FAIL_CLOSED]
     assert out["intact_blocks"].tolist() == [28, 28]
     assert out[0]["reasons"] == ck_.R_BEYOND_PREDICATE
-    # a later offload of a block clears its reported failure (fresh record)
+    # a later offload of the failed block by another claim records that
+    # claim's own offload: it is materialized, the first claim stays failed
     q = from_claims([(0x449, [55], toks(1))])
     m.offload(q)
     m.restore(q)
-    assert m.check(q)[0]["code"] == ck_.MATERIALIZED
+    m.restore(p)
+    out = m.check(from_claims([p.claim(0), q.claim(0)]))
+    assert out["code"].tolist() == [ck_.RESTORE_FAILED_FAIL_CLOSED, ck_.MATERIALIZED]
+    # block 48 (position 20 of the 448 claim) was flipped after its offload,
+    # by the restore of the longer claims: that now decides first
+    assert out[0]["first_failing_block"] == 20
+    assert out[0]["reasons"] == ck_.R_LOAD_FAILED | ck_.R_DIGEST_MISMATCH
     # malformed offsets in a device batch never fault and give UNKNOWN
     bad = from_claims([(0x30, [1, 2], toks(2)), (0x31, [3], toks(1))])
     bad.block_offsets[1] = 3
@@ -349,6 +379,80 @@ def test_controls_mirrored(torch, ck):
     m.offload(empty)
     m.restore(empty)
     m.check(empty)
+    m.finish()
+    del m
+    free_gpu(torch)
+
+
+def test_claim_scoped_records_mirrored(torch, ck):
+    """Section 5 storage_restorability row and Table 9 (fallback-recompute
+    and wrong-claim rows), on the GPU against the oracle with real bytes:
+    (1) claim C's restore reports block 6 lost; the block is recomputed with
+    the same bytes and stored by another claim X's offload: C still fails
+    closed at position 1, X is materialized; (2) claim D is restored intact,
+    then its block 12 receives other bytes that claim Y offloads: D fails
+    closed at position 1 against its own offload digest, Y is materialized."""
+    note("claim-scoped offload records mirrored")
+    m = Mirror(torch, ck)
+    c = from_claims([(0xC0, [5, 6, 7], toks(3))])
+    m.offload(c)
+    m.restore(c, load_failed=[6])
+    out = m.check(c)
+    assert (int(out[0]["code"]), int(out[0]["first_failing_block"])) == (ck.RESTORE_FAILED_FAIL_CLOSED, 1)
+    x = from_claims([(0xA0, [6], toks(1))])
+    m.rewrite(6, m.canonical(6).copy())  # the recompute: the same bytes written again
+    m.offload(x)
+    m.restore(x)
+    m.restore(c)
+    out = m.check(from_claims([c.claim(0), x.claim(0)]))
+    assert out["code"].tolist() == [ck.RESTORE_FAILED_FAIL_CLOSED, ck.MATERIALIZED]
+    assert int(out[0]["reasons"]) == ck.R_LOAD_FAILED
+
+    d = from_claims([(0xD0, [11, 12, 13], toks(3))])
+    m.offload(d)
+    m.restore(d)
+    assert m.check(d)[0]["code"] == ck.MATERIALIZED
+    before = m.canonical(12).copy()
+    m.rewrite(12, np.random.default_rng(3).integers(0, 256, size=before.size, dtype=np.uint8))
+    y = from_claims([(0xB0, [12], toks(1))])
+    m.offload(y)
+    m.restore(y)
+    out = m.check(from_claims([d.claim(0), y.claim(0)]))
+    assert out["code"].tolist() == [ck.RESTORE_FAILED_FAIL_CLOSED, ck.MATERIALIZED]
+    assert int(out[0]["first_failing_block"]) == 1 and int(out[0]["reasons"]) == ck.R_DIGEST_MISMATCH
+    assert int(out[0]["expected_digest"]) == O.block_digest(before, m.w.seed)
+    # C and D presented in one batch with a shared block of another claim
+    z = from_claims([(0xE0, [6, 12, 20], toks(3))])
+    m.offload(z)
+    m.restore(z)
+    out = m.check(from_claims([c.claim(0), d.claim(0), z.claim(0)]))
+    assert out["code"].tolist() == [ck.RESTORE_FAILED_FAIL_CLOSED, ck.RESTORE_FAILED_FAIL_CLOSED,
+                                    ck.MATERIALIZED]
+    m.finish()
+    del m
+    free_gpu(torch)
+
+
+def test_reassigned_block_identity_mirrored(torch, ck):
+    """A block registered under a second identity no longer answers lookups
+    of the first (section 7 E1; Table 2), across offload calls and within
+    one batch, on the GPU against the oracle; a later registration of the
+    first identity in the block makes it hit again."""
+    note("block reassignment and stale identities mirrored")
+    m = Mirror(torch, ck)
+    p_tok, q_tok, long_tok = toks(1), toks(1), toks(3)
+    m.offload(from_claims([(1, [5], p_tok), (10, [30, 31, 32], long_tok)]))
+    reqs = from_claims([(100, [], p_tok), (101, [], q_tok), (102, [], long_tok)])
+    got = m.lookup(reqs)
+    assert got["status"].tolist() == [ck.LOOKUP_HIT, ck.LOOKUP_MISS, ck.LOOKUP_HIT]
+    m.offload(from_claims([(2, [5], q_tok), (11, [31], toks(1))]))
+    got = m.lookup(reqs)
+    assert got["status"].tolist() == [ck.LOOKUP_MISS, ck.LOOKUP_HIT, ck.LOOKUP_PARTIAL]
+    assert int(got[2]["hit_blocks"]) == 1
+    m.offload(from_claims([(3, [5], p_tok.copy()), (4, [7], q_tok.copy()), (5, [7], p_tok.copy())]))
+    got = m.lookup(reqs)
+    # p: registered to 5 and 7 (ambiguous); q: registered to 5 and 7 as well
+    assert got["status"].tolist() == [ck.LOOKUP_UNKNOWN, ck.LOOKUP_UNKNOWN, ck.LOOKUP_PARTIAL]
     m.finish()
     del m
     free_gpu(torch)
@@ -425,7 +529,11 @@ def test_rows_sharing_entries(torch, ck):
     got = m.pool.lookup(ck.DeviceBatch(reqs))
     for f in [n for n in O.LOOKUP_DTYPE.names if n != "pad"]:
         assert np.array_equal(got[f], want[f]), (f, got[f].tolist(), want[f].tolist())
-    assert got["status"][:3].tolist() == [ck.LOOKUP_HIT] * 3
+    # the rows register blocks 9, 27 and 30 under A's, then C's, then E's
+    # prefixes: each block holds its latest registration, so A and C hit
+    # only their first block and E all three
+    assert got["status"][:3].tolist() == [ck.LOOKUP_PARTIAL, ck.LOOKUP_PARTIAL, ck.LOOKUP_HIT]
+    assert got["hit_blocks"][:3].tolist() == [1, 1, 3]
     assert m.pool.identity_stats() == m.op.identity_stats()
     m.finish()
     free_gpu(torch)

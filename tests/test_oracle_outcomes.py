@@ -784,7 +784,10 @@ def test_fuzz_cases_run_on_the_oracle():
         w, g = case.w, case.w.geometry
         host = content.pool_host(g, w.content_seed)
         op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
-        for b in case.offload:
+        for i, b in enumerate(case.offload):
+            if i == 1:
+                assert op.restore(case.mid, case.mid_faults.load_failed) == O.OK
+                host = apply_flips(host, w, case.mid_faults)
             assert op.offload(b, digests(host, w)) == O.OK
         assert op.restore(case.restore, case.faults.load_failed) == O.OK
         op.events(clear=True)
