@@ -61,7 +61,7 @@ def cpu_baseline(w, batch, faults, sample_gb: float):
 
     from oracle import oracle as O
     from paper_2606_01387_amd.synth import content
-    from tests.helpers import canon_digest, modeled_digests
+    from oracle.pool_digests import canon_digest, modeled_digests
 
     g = w.geometry
     uniq = batch.unique_blocks(g.num_blocks)

@@ -9,6 +9,7 @@ from __future__ import annotations
 import numpy as np
 
 from oracle import oracle as O
+from oracle.pool_digests import canon_digest, modeled_digests, real_digests
 from paper_2606_01387_amd.synth import MISSING, Batch, FaultSpec, Workload, content, make_batch, make_faults
 
 NONE32 = 0xFFFFFFFF
@@ -29,16 +30,6 @@ def apply_flips(pool: np.ndarray, w: Workload, faults: FaultSpec) -> np.ndarray:
     for b, bit in zip(faults.flip_blocks, faults.flip_bits):
         O.apply_flip(out, planes, nb, chunk, int(b), int(bit))
     return out
-
-
-def canon_digest(canon: np.ndarray, w: Workload) -> int:
-    """The oracle's digest of one block's canonical bytes: the block digest,
-    or for a head-shard pool the shard's part of the full block's digest."""
-    g = w.geometry
-    if not g.sharded:
-        return O.block_digest(canon, w.seed)
-    return O.shard_digest(canon, w.seed, g.planes, g.block_size, g.num_kv_heads, g.row_bytes,
-                          g.total_kv_heads, g.first_kv_head)
 
 
 def digests(pool: np.ndarray, w: Workload, blocks=None) -> np.ndarray:
@@ -68,30 +59,6 @@ def oracle_lifecycle(w: Workload, batch: Batch, faults: FaultSpec, pool: np.ndar
     d1 = digests(restored, w)
     out = op.check(batch, d1)
     return op, out, op.events(), d0, d1
-
-
-def modeled_digests(w: Workload, faults: FaultSpec, blocks_needed) -> tuple[np.ndarray, np.ndarray]:
-    """Offload-time and check-time digests for pools too large to digest on
-    the host.  Blocks whose bytes the faults change, reported-failure blocks
-    and ``blocks_needed`` get real oracle digests of their generated bytes
-    (before and after the flips); every other block keeps its bytes, so its
-    two digests are equal whatever their value, and a placeholder stands in
-    for it."""
-    g = w.geometry
-    d_before = np.arange(g.num_blocks, dtype=np.uint64) * np.uint64(0x9E3779B97F4A7C15) + np.uint64(1)
-    d_after = d_before.copy()
-    changed = set(int(b) for b in faults.changed_blocks())
-    real = sorted(changed | set(int(b) for b in faults.load_failed) | set(int(b) for b in blocks_needed))
-    flips_by_block: dict[int, list[int]] = {}
-    for b, bit in zip(faults.flip_blocks, faults.flip_bits):
-        flips_by_block.setdefault(int(b), []).append(int(bit))
-    for b in real:
-        canon = content.block_canonical(g, w.content_seed, b)
-        d_before[b] = canon_digest(canon, w)
-        for bit in flips_by_block.get(b, []):
-            canon[bit // 8] ^= np.uint8(1 << (bit % 8))
-        d_after[b] = canon_digest(canon, w)
-    return d_before, d_after
 
 
 def expected_by_scan(batch: Batch, num_blocks: int, block_size: int, failing: set[int]):
@@ -185,5 +152,6 @@ def validate_lifecycle(batch: Batch, events_pre: np.ndarray, events_check: np.nd
 
 __all__ = [
     "MISSING", "NONE32", "host_pool", "apply_flips", "canon_digest", "digests", "oracle_lifecycle",
-    "modeled_digests", "expected_by_scan", "make_batch", "make_faults", "validate_lifecycle",
+    "modeled_digests", "real_digests", "expected_by_scan", "make_batch", "make_faults",
+    "validate_lifecycle",
 ]
