@@ -81,6 +81,7 @@ extern "C" {
 #define CLAIM_EHIP (-3)   /* HIP runtime error */
 #define CLAIM_ENOSPC (-4) /* registry, footprint store, event log, staging or output too small */
 #define CLAIM_EDUP (-5)   /* duplicate claim id: acceptance refused */
+#define CLAIM_ELIMIT (-6) /* batch larger than claim_check_static's fixed scratch */
 
 /* ----------------------------------------------------------- outcomes */
 #define CLAIM_UNKNOWN 0 /* no claim outcome (ambiguity fails closed); zero-initialised = fail closed */
@@ -357,6 +358,28 @@ int claim_restore(claim_pool* pool, const claim_batch* batch, const void* stagin
  * claim is its own blocking id), or OUTCOME_UNKNOWN.  The registry is not
  * changed.  ENOSPC if the event log could overflow. */
 int claim_check(claim_pool* pool, const claim_batch* batch);
+
+/* claim_check for callers that cannot allocate memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  It does
+ * the same work with the same kernels and the same results, but allocates
+ * nothing: its per-claim scratch (event counts, pending events, event-scan
+ * tile sums; 36 bytes per claim) lives in one fixed device array per GPU of
+ * about 9.4 MB, which the library holds until the process ends, and the
+ * outcomes go to `out` (device memory, capacity out_cap records), not to
+ * the pool.  Events are appended to the pool's log as by claim_check and
+ * read with outcomes_read, which then reports no outcomes (they are in
+ * `out`, complete once the pool's stream reaches this call; the call does
+ * not wait).  Batches of more than CLAIM_STATIC_MAX_CLAIMS claims return
+ * CLAIM_ELIMIT; out_cap < num_claims or a log that could overflow return
+ * CLAIM_ENOSPC; a NULL out with claims returns CLAIM_EINVAL; nothing is
+ * queued then.  Every call on one GPU, from any pool, shares that GPU's
+ * array, and each call overwrites what the previous one left there: calls
+ * that overlap on one GPU (pools on different streams, or host threads)
+ * race and must be serialized by the caller.  Nothing in the array needs to
+ * start at zero: each call writes every entry it reads. */
+#define CLAIM_STATIC_MAX_CLAIMS 262144u
+int claim_check_static(claim_pool* pool, const claim_batch* batch, claim_outcome* out,
+                       uint32_t out_cap);
 
 /* Reuse lookup (section 7 paths A and B, order 3: the lookup reports how
  * many of the request's tokens hit the offloaded claim footprint, hit=448

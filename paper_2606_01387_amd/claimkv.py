@@ -23,7 +23,8 @@ HIP_FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-shared", "-std=c++17",
              "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 # ------------------------------------------------------------ vocabulary
-OK, EINVAL, ENOMEM, EHIP, ENOSPC, EDUP = 0, -1, -2, -3, -4, -5
+OK, EINVAL, ENOMEM, EHIP, ENOSPC, EDUP, ELIMIT = 0, -1, -2, -3, -4, -5, -6
+STATIC_MAX_CLAIMS = 262144
 UNKNOWN, MATERIALIZED, RESTORE_FAILED_FAIL_CLOSED = 0, 1, 2
 EV_ACCEPTED, EV_OFFLOADED, EV_RESTORE_REQUIRED, EV_RESTORED = 1, 2, 3, 4
 EV_RESTORATION_FAILED, EV_ACTIVE_REQUEST_REFUSED, EV_OUTCOME_UNKNOWN = 5, 6, 7
@@ -50,7 +51,7 @@ LOOKUP_DTYPE = np.dtype(
      ("hit_blocks", "<u4"), ("last_block", "<u4"), ("reserved", "<u4")])
 
 EXPORTS = ("claim_pool_create", "claim_pool_destroy", "claim_offload", "claim_restore",
-           "claim_check", "claim_lookup", "claim_identity_stats", "outcomes_read",
+           "claim_check", "claim_check_static", "claim_lookup", "claim_identity_stats", "outcomes_read",
            "claim_timing_read", "claim_block_state_read", "claim_strerror")
 
 
@@ -123,6 +124,7 @@ def lib() -> ctypes.CDLL:
             "claim_offload": ([vp, ctypes.POINTER(CBatch), vp, u64], i32),
             "claim_restore": ([vp, ctypes.POINTER(CBatch), vp, u64, ctypes.POINTER(CFaults)], i32),
             "claim_check": ([vp, ctypes.POINTER(CBatch)], i32),
+            "claim_check_static": ([vp, ctypes.POINTER(CBatch), vp, u32], i32),
             "claim_lookup": ([vp, ctypes.POINTER(CBatch), vp, u32], i32),
             "claim_identity_stats": ([vp, ctypes.POINTER(u64), ctypes.POINTER(u64)], i32),
             "outcomes_read": ([vp, vp, u32, ctypes.POINTER(u32), vp, u64, ctypes.POINTER(u64)], i32),
@@ -285,6 +287,21 @@ class Pool:
     def check(self, batch: DeviceBatch) -> None:
         _check(lib().claim_check(self._h, ctypes.byref(batch.struct)), "claim_check")
         self._inflight.append(batch)
+
+    def check_static(self, batch: DeviceBatch, out=None):
+        """claim_check_static: the check with no allocation by the library;
+        outcomes go to ``out`` (a device uint8 tensor of 64 bytes per claim,
+        made here if None), which is returned."""
+        torch = _torch()
+        n = batch.num_claims
+        if out is None:
+            out = torch.empty(max(1, n) * OUTCOME_DTYPE.itemsize, dtype=torch.uint8,
+                              device=self.kv.device)
+        cap = out.numel() // OUTCOME_DTYPE.itemsize
+        _check(lib().claim_check_static(self._h, ctypes.byref(batch.struct), out.data_ptr(), cap),
+               "claim_check_static")
+        self._inflight += [batch, out]
+        return out
 
     def lookup_async(self, batch: DeviceBatch, out=None):
         """Queue a reuse lookup of the batch's token rows on the pool stream;

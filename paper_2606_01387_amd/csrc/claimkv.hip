@@ -51,6 +51,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 
 #include "claimkv.h"
@@ -1831,6 +1832,50 @@ __global__ void __launch_bounds__(kThreads) k_write_events(const uint32_t* __res
 const int kTimingSlots = 64;
 const int kStages = 6;  // start, selected, digested, finalized, claims, events
 
+// Fixed scratch of claim_check_static: per-claim event counts (4 B),
+// pending events (32 B) and event-scan tile sums (4 B per 1024 claims) for
+// batches of up to CLAIM_STATIC_MAX_CLAIMS claims, each part 256-byte
+// aligned.
+constexpr uint64_t kStaticCntOff = 0;
+constexpr uint64_t kStaticPendOff =
+    (kStaticCntOff + CLAIM_STATIC_MAX_CLAIMS * sizeof(uint32_t) + 255) / 256 * 256;
+constexpr uint64_t kStaticTsumOff =
+    (kStaticPendOff + CLAIM_STATIC_MAX_CLAIMS * sizeof(Pend) + 255) / 256 * 256;
+constexpr uint64_t kStaticBytes =
+    (kStaticTsumOff + (CLAIM_STATIC_MAX_CLAIMS + kTile - 1) / kTile * sizeof(uint32_t) + 255) / 256 * 256;
+
+}  // namespace
+
+// The scratch array itself: one copy on every GPU the library runs on, held
+// until the process ends.  Host code never passes its name to a kernel (on
+// the host it is only a stand-in for the symbol): claim_pool_create looks up
+// its device address on each device once, with hipGetSymbolAddress, and
+// claim_check_static hands that address to the kernels.
+static __device__ __align__(256) uint8_t scratch[kStaticBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch` on each device
+
+// The address of this device's scratch array (looked up on the first call
+// for the device, which must be current).
+int static_scratch(int device, void** out) {
+  if (device < 0 || device >= kMaxDevices) return CLAIM_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return CLAIM_EHIP;
+    }
+    g_scratch_ptr[device] = p;
+  }
+  *out = g_scratch_ptr[device];
+  return CLAIM_OK;
+}
+
 }  // namespace
 
 struct claim_pool {
@@ -1869,6 +1914,8 @@ struct claim_pool {
 
   claim_event* log = nullptr;
   uint64_t ev_cap = 0, log_ub = 0;
+
+  uint8_t* static_scratch = nullptr;  // this device's fixed scratch (claim_check_static)
 
   Counters* ctr = nullptr;
   Counters* host_ctr = nullptr;  // pinned
@@ -2125,23 +2172,32 @@ int launch_finalize(claim_pool* P, int mode, int staged) {
   return hip_status(hipGetLastError());
 }
 
+// Per-claim scratch of one call: event counts, pending events, tile sums.
+struct ClaimScratch {
+  uint32_t* cnt;
+  Pend* pend;
+  uint32_t* tsum;
+};
+
+ClaimScratch pool_scratch(claim_pool* P) { return ClaimScratch{P->cnt, P->pend, P->tsum}; }
+
 // Scan the per-claim event counts and append the events.
-int append_events(claim_pool* P, const claim_batch* b) {
+int append_events(claim_pool* P, const claim_batch* b, ClaimScratch sc) {
   const uint64_t C = b->num_claims;
   if (C == 0) return CLAIM_OK;
   if (C <= kSmallEvents) {
-    hipLaunchKernelGGL(k_events_small, dim3(1), dim3(1024), 0, P->stream, P->cnt, P->pend,
+    hipLaunchKernelGGL(k_events_small, dim3(1), dim3(1024), 0, P->stream, sc.cnt, sc.pend,
                        b->claim_ids, C, P->ctr, P->log);
     return hip_status(hipGetLastError());
   }
   const uint64_t ntiles = (C + kTile - 1) / kTile;
-  hipLaunchKernelGGL(k_tile_sums, dim3((uint32_t)ntiles), dim3(kThreads), 0, P->stream, P->cnt, C,
-                     P->tsum);
+  hipLaunchKernelGGL(k_tile_sums, dim3((uint32_t)ntiles), dim3(kThreads), 0, P->stream, sc.cnt, C,
+                     sc.tsum);
   HIP_TRY(hipGetLastError());
-  hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, P->stream, P->tsum, ntiles, P->ctr);
+  hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, P->stream, sc.tsum, ntiles, P->ctr);
   HIP_TRY(hipGetLastError());
-  hipLaunchKernelGGL(k_write_events, dim3((uint32_t)ntiles), dim3(kThreads), 0, P->stream, P->cnt,
-                     P->pend, b->claim_ids, C, P->tsum, P->ctr, P->log);
+  hipLaunchKernelGGL(k_write_events, dim3((uint32_t)ntiles), dim3(kThreads), 0, P->stream, sc.cnt,
+                     sc.pend, b->claim_ids, C, sc.tsum, P->ctr, P->log);
   return hip_status(hipGetLastError());
 }
 
@@ -2275,6 +2331,7 @@ const char* claim_strerror(int status) {
     case CLAIM_EHIP: return "HIP runtime error";
     case CLAIM_ENOSPC: return "capacity exceeded (registry, footprint, event log, staging or output)";
     case CLAIM_EDUP: return "duplicate claim id: acceptance refused";
+    case CLAIM_ELIMIT: return "batch has more claims than claim_check_static's fixed scratch holds";
     default: return "unknown status";
   }
 }
@@ -2314,6 +2371,9 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
       break;
     }
     P->cus = cus > 0 ? (uint32_t)cus : 256;
+    void* sp = nullptr;
+    if ((rc = static_scratch(P->device, &sp))) break;
+    P->static_scratch = (uint8_t*)sp;
     P->stream = (hipStream_t)d->stream;
     P->flags = d->flags;
     if (P->flags & CLAIM_POOL_STAGE_TIMING) P->flags |= CLAIM_POOL_TIMING;
@@ -2454,7 +2514,7 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
     hipLaunchKernelGGL(k_holders, dim3(grid_for(U ? U : 1, 4096)), dim3(kThreads), 0, P->stream,
                        P->uniq, P->ctr, P->owner_at, P->idn_store, P->fp_used, P->holder);
     HIP_TRY(hipGetLastError());
-    TRY(append_events(P, b));
+    TRY(append_events(P, b, pool_scratch(P)));
   }
   TRY(read_counters(P));
   P->fp_used += fp_need;
@@ -2527,20 +2587,19 @@ int claim_restore(claim_pool* P, const claim_batch* b, const void* staging,
     hipLaunchKernelGGL(k_restore_claims, dim3(grid_for(C, 0x7FFFFFFFu)), dim3(kThreads), 0,
                        P->stream, batch_dev(b), reg_dev(P), P->cnt, P->pend);
     HIP_TRY(hipGetLastError());
-    TRY(append_events(P, b));
+    TRY(append_events(P, b, pool_scratch(P)));
   }
   P->log_ub += C;
   return CLAIM_OK;
 }
 
-int claim_check(claim_pool* P, const claim_batch* b) {
-  if (!P) return CLAIM_EINVAL;
-  TRY(check_batch(P, b));
-  HIP_TRY(hipSetDevice(P->device));
-  const uint64_t C = b->num_claims;
-  if (P->log_ub + 2 * C > P->ev_cap) return CLAIM_ENOSPC;
-  TRY(ensure_claim_scratch(P, C, true));
+}  // extern "C"
 
+namespace {
+
+// The check itself: outcomes to `out`, per-claim scratch in `sc`.
+int check_body(claim_pool* P, const claim_batch* b, claim_outcome* out, ClaimScratch sc) {
+  const uint64_t C = b->num_claims;
   int slot = 0;
   if (P->flags & CLAIM_POOL_TIMING) {
     if (P->t_count == kTimingSlots) TRY(fold_timing_slot(P));
@@ -2556,19 +2615,51 @@ int claim_check(claim_pool* P, const claim_batch* b) {
   if (C) {
     CheckState st;
     st.bres = P->bres;
-    LAUNCH_GROUPED(k_check, P, b, batch_dev(b), reg_dev(P), st, P->nb, P->bs, P->seed, P->outcomes,
-                   P->cnt, P->pend);
+    LAUNCH_GROUPED(k_check, P, b, batch_dev(b), reg_dev(P), st, P->nb, P->bs, P->seed, out,
+                   sc.cnt, sc.pend);
   }
   TRY(record_stage(P, slot, 4));
-  TRY(append_events(P, b));
+  TRY(append_events(P, b, sc));
   TRY(record_stage(P, slot, 5));
   if (P->flags & CLAIM_POOL_TIMING) {
     P->t_head = (P->t_head + 1) % kTimingSlots;
     P->t_count += 1;
   }
+  P->log_ub += 2 * C;
+  return CLAIM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int claim_check(claim_pool* P, const claim_batch* b) {
+  if (!P) return CLAIM_EINVAL;
+  TRY(check_batch(P, b));
+  HIP_TRY(hipSetDevice(P->device));
+  const uint64_t C = b->num_claims;
+  if (P->log_ub + 2 * C > P->ev_cap) return CLAIM_ENOSPC;
+  TRY(ensure_claim_scratch(P, C, true));
+  TRY(check_body(P, b, P->outcomes, pool_scratch(P)));
   P->last_check_claims = C;
   P->have_outcomes = true;
-  P->log_ub += 2 * C;
+  return CLAIM_OK;
+}
+
+int claim_check_static(claim_pool* P, const claim_batch* b, claim_outcome* out,
+                       uint32_t out_cap) {
+  if (!P) return CLAIM_EINVAL;
+  TRY(check_batch(P, b));
+  const uint64_t C = b->num_claims;
+  if (C > CLAIM_STATIC_MAX_CLAIMS) return CLAIM_ELIMIT;
+  if (C > 0 && !out) return CLAIM_EINVAL;
+  if (out_cap < C || P->log_ub + 2 * C > P->ev_cap) return CLAIM_ENOSPC;
+  HIP_TRY(hipSetDevice(P->device));
+  uint8_t* sp = P->static_scratch;  // the device address, never the symbol's host name
+  const ClaimScratch sc{(uint32_t*)(sp + kStaticCntOff), (Pend*)(sp + kStaticPendOff),
+                        (uint32_t*)(sp + kStaticTsumOff)};
+  TRY(check_body(P, b, out, sc));
+  P->have_outcomes = false;  // this check's outcomes are in `out`
   return CLAIM_OK;
 }
 

@@ -74,8 +74,8 @@ def test_record_layouts_match_header(tmp_path):
 
 
 def test_strerror(L):
-    for code in (ck.OK, ck.EINVAL, ck.ENOMEM, ck.EHIP, ck.ENOSPC, ck.EDUP):
-        assert ck.strerror(code)
+    for code in (ck.OK, ck.EINVAL, ck.ENOMEM, ck.EHIP, ck.ENOSPC, ck.EDUP, ck.ELIMIT):
+        assert ck.strerror(code) != "unknown status"
     assert ck.strerror(-99) == "unknown status"
     assert "duplicate" in ck.strerror(ck.EDUP)
 
@@ -131,6 +131,7 @@ def test_null_arguments_are_rejected(L):
     assert L.claim_offload(None, ctypes.byref(b), None, 0) == ck.EINVAL
     assert L.claim_restore(None, ctypes.byref(b), None, 0, None) == ck.EINVAL
     assert L.claim_check(None, ctypes.byref(b)) == ck.EINVAL
+    assert L.claim_check_static(None, ctypes.byref(b), None, 0) == ck.EINVAL
     assert L.outcomes_read(None, None, 0, None, None, 0, None) == ck.EINVAL
     assert L.claim_timing_read(None, None) == ck.EINVAL
     assert L.claim_block_state_read(None, 0, 0, None, None, None, None) == ck.EINVAL
