@@ -741,6 +741,83 @@ def test_staged_round_trip(torch, ck, w, where):
     free_gpu(torch)
 
 
+@pytest.mark.parametrize("where", ["device", "pinned-host"])
+def test_two_staged_offloads(torch, ck, where):
+    """Staging holds one generation (the header's capability limit): after
+    two staged offloads only the second's blocks can be copied back.  Batch A
+    (claims over blocks 0..23) is offloaded with staging, then batch B
+    (claims over blocks 16..39) with a second staging buffer; every staged
+    block's device copy is then lost (zeroed).  A restore of A and B from
+    B's staging copies back blocks 16..39 only: B's claims and A's claims
+    inside 16..23 are materialized, A's claims touching 0..15 fail closed on
+    the digest compare (their bytes are gone), never a false success.  GPU
+    against the oracle, with the pool bytes after the restore against the
+    host model."""
+    note(f"two staged offloads via {where}")
+    w = TINY
+    g = w.geometry
+    rng = np.random.default_rng(41)
+
+    def rows(first_id, lo, hi, n):
+        out = []
+        for k in range(n):
+            m = int(rng.integers(1, 4))
+            out.append((first_id + k, [int(x) for x in rng.integers(lo, hi, size=m)],
+                        rng.integers(0, 32000, size=m * g.block_size, dtype=np.uint32)))
+        return out
+
+    a_rows = rows(0xA000, 0, 24, 12) + [(0xAF00, [16, 17, 23], rng.integers(0, 32000, size=48,
+                                                                           dtype=np.uint32))]
+    b_rows = rows(0xB000, 16, 40, 12)
+    a, b, both = from_claims(a_rows), from_claims(b_rows), from_claims(a_rows + b_rows)
+    ua, ub = a.unique_blocks(g.num_blocks), b.unique_blocks(g.num_blocks)
+    kv = gpu_pool_tensor(torch, w)
+
+    def staging_for(n):
+        if where == "device":
+            return torch.empty(n * g.block_bytes, dtype=torch.uint8, device="cuda")
+        return torch.empty(n * g.block_bytes, dtype=torch.uint8, pin_memory=True)
+
+    st_a, st_b = staging_for(ua.size), staging_for(ub.size)
+    host = content.pool_host(g, w.content_seed)
+    with ck.Pool(g, w.seed, kv, max_claims=128, max_footprint=1024, event_capacity=1024) as pool:
+        pool.offload(ck.DeviceBatch(a), staging=st_a)
+        pool.offload(ck.DeviceBatch(b), staging=st_b)
+        pool.stream.synchronize()
+        lost = np.union1d(ua, ub)
+        idx = torch.as_tensor(lost.astype(np.int64), device="cuda")
+        kv.view(g.planes, g.num_blocks, g.chunk_bytes)[:, idx, :] = 0
+        torch.cuda.synchronize()
+        db = ck.DeviceBatch(both)
+        pool.restore(db, staging=st_b)
+        pool.read()
+        pool.check(db)
+        out, ev = pool.read()
+    model = host.copy()
+    gone = np.setdiff1d(ua, ub)  # staged only by the first offload
+    model.reshape(g.planes, g.num_blocks, g.chunk_bytes)[:, gone, :] = 0
+    assert np.array_equal(kv.cpu().numpy(), model)
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    op.offload(a, digests(host, w))
+    op.offload(b, digests(host, w))
+    op.restore(both)
+    op.events(clear=True)
+    same_outcomes(out, op.check(both, digests(model, w)))
+    same_events(ev, op.events())
+    gone_set = set(int(x) for x in gone)
+    for c, (cid, blks, _) in enumerate(a_rows + b_rows):
+        hit = [j for j, x in enumerate(blks) if x in gone_set]
+        if hit:
+            assert (int(out[c]["code"]), int(out[c]["first_failing_block"])) == \
+                (ck.RESTORE_FAILED_FAIL_CLOSED, hit[0]), cid
+            assert out[c]["reasons"] & ck.R_DIGEST_MISMATCH
+        else:
+            assert out[c]["code"] == ck.MATERIALIZED, cid
+    assert (out["code"] == ck.MATERIALIZED).any() and (out["code"] == ck.RESTORE_FAILED_FAIL_CLOSED).any()
+    del kv, st_a, st_b
+    free_gpu(torch)
+
+
 # ----------------------------------------------------------- full-size workloads
 
 
