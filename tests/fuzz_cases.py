@@ -194,3 +194,110 @@ def capacities(case: Case) -> dict:
 
 # CLAIMKV_FUZZ_SEEDS widens a one-off run; the suite replays the first 160
 SEEDS = range(int(os.environ.get("CLAIMKV_FUZZ_SEEDS", "160")))
+
+
+# ------------------------------------------------- multi-step lifecycles
+
+
+@dataclass
+class Step:
+    kind: str  # "offload", "restore", "check" or "lookup"
+    batch: Batch
+    faults: FaultSpec | None = None
+
+
+@dataclass
+class Sequence:
+    w: Workload
+    steps: list
+    claims: int  # claims offloaded over the whole sequence
+    refs: int
+
+
+def make_sequence(seed: int, num_steps: int = 12) -> Sequence:
+    """A random lifecycle of several offloads over a few hot blocks, so that
+    claims share blocks, re-offload blocks whose loads failed or whose bytes
+    changed, and register other prefixes in them; restores of random subsets
+    of the claims with reported failures and bit flips (some flips undo
+    earlier ones: a recompute of the original bytes); checks of random
+    subsets, some presented changed or never accepted; lookups of their
+    tokens.  Inputs only."""
+    rng = np.random.default_rng(90_000 + seed)
+    g = GEOMETRIES[seed % len(GEOMETRIES)]
+    w = Workload(name=f"seq-{seed}", geometry=g, seed=int(rng.integers(0, 2**63)),
+                 num_claims=0, length=TINY.length, sharing=TINY.sharing, corrupt_rate=0.0,
+                 gen_seed=seed, content_seed=int(rng.integers(0, 2**31)))
+    bs = g.block_size
+    hot = rng.choice(g.num_blocks, size=min(g.num_blocks, int(rng.integers(6, 16))), replace=False)
+    accepted = []  # (id, blocks, tokens)
+    flips_done = []  # (block, bit) applied so far
+    steps = []
+    next_id = 1
+    refs = 0
+    for k in range(num_steps):
+        kind = "offload" if k == 0 else str(rng.choice(["offload", "restore", "check", "lookup"],
+                                                        p=[0.3, 0.3, 0.3, 0.1]))
+        if kind == "offload":
+            rows = []
+            for _ in range(int(rng.integers(1, 7))):
+                n = int(rng.integers(0, 6))
+                blks = rng.choice(hot, size=n).astype(np.int64)
+                if n and rng.random() < 0.05:
+                    blks[int(rng.integers(n))] = MISSING
+                if accepted and rng.random() < 0.35:  # an earlier claim's tokens (shared identities)
+                    src = accepted[int(rng.integers(len(accepted)))]
+                    tk = src[2][: int(rng.integers(0, src[2].size + 1))].copy()
+                    n = -(-tk.size // bs)
+                    blks = np.concatenate([src[1][:n], rng.choice(hot, size=max(0, n - src[1].size))])
+                    if n and rng.random() < 0.5:
+                        blks[int(rng.integers(n))] = int(rng.choice(hot))
+                else:
+                    tk = _tokens(rng, n * bs - (int(rng.integers(0, bs)) if n and rng.random() < 0.3 else 0))
+                rows.append((next_id, blks.astype(np.uint32), tk))
+                next_id += 1
+            b = from_claims(rows)
+            if rng.random() < 0.3:
+                b.predicate_tokens = rng.integers(0, 6 * bs, size=b.num_claims).astype(np.uint64)
+            accepted += rows
+            refs += b.num_refs
+            steps.append(Step("offload", b))
+        elif kind == "restore":
+            sub = [r for r in accepted if rng.random() < 0.7]
+            fb, fbits = [], []
+            for _ in range(int(rng.integers(0, 4))):
+                if flips_done and rng.random() < 0.4:  # undo an earlier flip: a recompute
+                    b0, bit0 = flips_done.pop(int(rng.integers(len(flips_done))))
+                else:
+                    b0, bit0 = int(rng.choice(hot)), int(rng.integers(0, 8 * g.block_bytes))
+                    flips_done.append((b0, bit0))
+                fb.append(b0)
+                fbits.append(bit0)
+            lost = rng.choice(hot, size=int(rng.integers(0, 3)), replace=False)
+            steps.append(Step("restore", from_claims(sub),
+                              FaultSpec(np.array(fb, np.uint32), np.array(fbits, np.uint64),
+                                        np.asarray(lost, np.uint32))))
+        elif kind == "check":
+            pres = []
+            for r in accepted:
+                if rng.random() < 0.8:
+                    cid, blks, tk = r[0], r[1].copy(), r[2].copy()
+                    if rng.random() < 0.08 and blks.size:
+                        blks[int(rng.integers(blks.size))] = int(rng.choice(hot))
+                    elif rng.random() < 0.08 and tk.size:
+                        tk[int(rng.integers(tk.size))] ^= 3
+                    pres.append((cid, blks, tk))
+            rng.shuffle(pres)
+            pres.append((int(50_000 + k), rng.choice(hot, size=2).astype(np.uint32), _tokens(rng, 2 * bs)))
+            steps.append(Step("check", from_claims(pres)))
+        else:
+            reqs = [(int(60_000 + 100 * k + i), [], r[2][: int(rng.integers(0, r[2].size + 1))])
+                    for i, r in enumerate(accepted)]
+            reqs.append((int(70_000 + k), [], _tokens(rng, 3 * bs)))
+            steps.append(Step("lookup", from_claims(reqs)))
+    steps.append(Step("restore", from_claims(accepted), FaultSpec(np.zeros(0, np.uint32), np.zeros(0, np.uint64),
+                                                                   np.zeros(0, np.uint32))))
+    steps.append(Step("check", from_claims(accepted)))
+    return Sequence(w, steps, len(accepted), refs)
+
+
+SEQUENCE_SEEDS = range(int(os.environ.get("CLAIMKV_SEQUENCE_SEEDS", "80")))

@@ -797,3 +797,68 @@ def test_fuzz_cases_run_on_the_oracle():
         assert op.events().size == out.size + failed
         codes += np.bincount(out["code"], minlength=3)
     assert (codes > 20).all(), codes
+
+
+@pytest.mark.parametrize("seed", range(80))
+def test_sequences_follow_the_claim_ledger(seed):
+    """The oracle over the multi-step lifecycles the GPU differential test
+    replays (tests/fuzz_cases.make_sequence): at every check, each claim that
+    was offloaded whole, restored since, and is presented as accepted has
+    the outcome a byte ledger gives, with no digest: it fails closed at the
+    first position inside its predicate whose bytes differ from its own
+    offload-time copy, or whose block had a load failure reported by a later
+    restore; otherwise it is materialized (section 5 storage_restorability;
+    Table 9; section 1 predicate)."""
+    from tests.fuzz_cases import make_sequence
+
+    seq = make_sequence(seed)
+    w, g = seq.w, seq.w.geometry
+    bs = g.block_size
+    host = host_pool(w).copy()
+    op = O.OraclePool(g.num_blocks, bs, w.seed)
+    ledger = {}  # id -> (blocks, tokens, copies, call, pred_blocks, offloaded)
+    restored = set()
+    reports = []
+    judged = 0
+    for call, st in enumerate(seq.steps):
+        b = st.batch
+        if st.kind == "offload":
+            assert op.offload(b, digests(host, w)) == O.OK
+            for c in range(b.num_claims):
+                cid, blks, tk = b.claim(c)
+                n = len(blks)
+                whole = n > 0 and (blks < g.num_blocks).all() and n == -(-len(tk) // bs)
+                k = None if b.predicate_tokens is None else int(b.predicate_tokens[c])
+                pred = n if k is None else min(n, -(-k // bs))
+                copies = [O.canonical_block(host, g.planes, g.num_blocks, g.chunk_bytes, int(x)).copy()
+                          if x < g.num_blocks else None for x in blks]
+                ledger[int(cid)] = (blks.copy(), tk.copy(), copies, call, pred, whole)
+        elif st.kind == "restore":
+            assert op.restore(b, st.faults.load_failed) == O.OK
+            host = apply_flips(host, w, st.faults)
+            reports += [(int(x), call) for x in st.faults.load_failed]
+            restored |= {int(x) for x in b.claim_ids if int(x) in ledger and ledger[int(x)][5]}
+        elif st.kind == "check":
+            out = op.check(b, digests(host, w))
+            for c in range(b.num_claims):
+                cid, blks, tk = b.claim(c)
+                cid = int(cid)
+                if cid not in ledger or cid not in restored:
+                    continue
+                a_blks, a_tk, copies, at, pred, _ = ledger[cid]
+                if not (np.array_equal(blks, a_blks) and np.array_equal(tk, a_tk)):
+                    continue
+                bad = [j for j in range(pred)
+                       if any(rb == int(a_blks[j]) and rc > at for rb, rc in reports)
+                       or not np.array_equal(O.canonical_block(host, g.planes, g.num_blocks,
+                                                               g.chunk_bytes, int(a_blks[j])), copies[j])]
+                o = out[c]
+                if bad:
+                    assert (int(o["code"]), int(o["first_failing_block"])) == \
+                        (O.RESTORE_FAILED_FAIL_CLOSED, bad[0]), (seed, call, cid, bad)
+                else:
+                    assert o["code"] == O.MATERIALIZED, (seed, call, cid)
+                judged += 1
+        else:
+            op.lookup(b)
+    assert judged > 0
