@@ -127,12 +127,16 @@ int synth_copy_probe(void* dst, const void* src, uint64_t nbytes, void* stream) 
 }
 
 // Stream-read the first nbytes of src (rounded down to a multiple of 32 KiB)
-// with grid = cus * 16 workgroups; sink is a 4-byte device scratch word.
+// with grid = cus * 2 workgroups (64 KiB of loads in flight per CU); sink is
+// a 4-byte device scratch word.  Of grids of 1 to 16 workgroups per CU with
+// 16 or 32 loads per lane, measured in one process over the 8B, stress and
+// MLA pools, 2 per CU with 16 loads read fastest (8B 7.27 TB/s against
+// 7.08 with 16 per CU).
 int synth_read_probe(const void* src, uint64_t nbytes, uint32_t cus, void* sink, void* stream) {
   if (!src || !sink || ((uintptr_t)src & 15) || cus == 0) return -1;
   const uint64_t n = (nbytes / 8) / 4096 * 4096;
   if (n == 0) return -1;
-  hipLaunchKernelGGL(read_kernel, dim3(cus * 16), dim3(256), 0, (hipStream_t)stream,
+  hipLaunchKernelGGL(read_kernel, dim3(cus * 2), dim3(256), 0, (hipStream_t)stream,
                      (const u32x2*)src, n, (uint32_t*)sink);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
