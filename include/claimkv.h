@@ -376,7 +376,11 @@ int claim_check(claim_pool* pool, const claim_batch* batch);
  * array, and each call overwrites what the previous one left there: calls
  * that overlap on one GPU (pools on different streams, or host threads)
  * race and must be serialized by the caller.  Nothing in the array needs to
- * start at zero: each call writes every entry it reads. */
+ * start at zero: each call writes every entry it reads.  On a pool created
+ * without timing flags the call only queues kernels, so it can be captured
+ * into a HIP graph; each replay checks the batch again and appends its
+ * events (all or none: see outcomes_read), and the caller reads or resets
+ * the log between replays as between calls. */
 #define CLAIM_STATIC_MAX_CLAIMS 262144u
 int claim_check_static(claim_pool* pool, const claim_batch* batch, claim_outcome* out,
                        uint32_t out_cap);
@@ -416,7 +420,13 @@ int claim_identity_stats(claim_pool* pool, uint64_t* entries, uint64_t* ambiguou
  * ev_cap; *num_events = their count), which are then dropped from the log
  * (sequence numbers keep counting).  A NULL out or events skips that part
  * (events are then kept).  ENOSPC, with nothing copied or dropped, if a
- * capacity is too small. */
+ * capacity is too small.  Every call checks on the host that its events
+ * fit the log before it queues work; the device also appends each call's
+ * events all or none, so work the host did not bound (a captured
+ * claim_check_static replayed from a graph) can never write past the log:
+ * a call whose events did not fit appends none and marks the log, and the
+ * next outcomes_read copies what the log holds, clears the mark when it
+ * reads the events, and returns ENOSPC. */
 int outcomes_read(claim_pool* pool, claim_outcome* out, uint32_t out_cap, uint32_t* num_out,
                   claim_event* events, uint64_t ev_cap, uint64_t* num_events);
 

@@ -267,19 +267,27 @@ struct Pend {  // events a claim will append (0..2), written before the scan
   uint32_t pad;
 };
 
-struct Counters {  // device-resident counters of one pool (64 bytes)
+struct Counters {  // device-resident counters of one pool (72 bytes)
   uint32_t uniq_count;
   uint32_t dup_flag;      // kFlagDupId | kFlagBackwardRow
   uint64_t log_count;     // events held in the log
   uint64_t seq_next;      // next global sequence number
-  uint64_t call_pos;      // log position of the current call's first event
+  uint64_t call_pos;      // log position of the current call's first event (kDropped: none)
   uint64_t call_seq;      // its sequence number
   uint64_t reg_count;     // claims registered
   uint64_t id_entries;    // identities registered
   uint64_t id_ambiguous;  // identities registered to two or more blocks
+  uint32_t log_dropped;   // a call's events did not fit the log and were dropped
+  uint32_t pad;
 };
 
-static_assert(sizeof(Counters) == 64, "Counters layout");
+static_assert(sizeof(Counters) == 72, "Counters layout");
+
+// call_pos of a call whose events do not fit the log: they are dropped, all
+// of them, and log_dropped is set.  The host bounds every call it queues
+// itself; the device bound keeps the log in bounds for work the host cannot
+// see (a captured graph replayed).
+constexpr uint64_t kDropped = ~0ull;
 
 // dup_flag bits set by k_dupcheck: a claim id occurs twice or is already
 // registered (the batch is refused); some block row runs backwards, so the
@@ -1678,11 +1686,23 @@ constexpr uint64_t kSmallEvents = 4096;
 __global__ void __launch_bounds__(1024) k_events_small(const uint32_t* __restrict__ cnt,
                                                        const Pend* __restrict__ pend,
                                                        const uint64_t* __restrict__ ids, uint64_t C,
-                                                       Counters* __restrict__ ctr,
+                                                       uint64_t ev_cap, Counters* __restrict__ ctr,
                                                        claim_event* __restrict__ log) {
   __shared__ uint32_t lds[17];
   __shared__ claim_event s_ev[2 * 1024];
   const uint64_t base_pos = ctr->log_count, base_seq = ctr->seq_next;
+  // the call's events, counted first: all of them are appended, or none
+  uint64_t all = 0;
+  for (uint64_t c0 = 0; c0 < C; c0 += 1024) {
+    const uint64_t c = c0 + threadIdx.x;
+    uint32_t total;
+    (void)block_exclusive_scan_1024(c < C ? cnt[c] : 0u, &total, lds);
+    all += total;
+  }
+  if (base_pos + all > ev_cap) {
+    if (threadIdx.x == 0) ctr->log_dropped = 1;
+    return;  // uniform: every thread computed the same total
+  }
   uint64_t run = 0;
   for (uint64_t c0 = 0; c0 < C; c0 += 1024) {
     const uint64_t c = c0 + threadIdx.x;
@@ -1737,7 +1757,7 @@ __global__ void __launch_bounds__(kThreads) k_tile_sums(const uint32_t* __restri
 // One workgroup: exclusive scan of the tile sums; reserves the call's range
 // of the log.
 __global__ void __launch_bounds__(1024) k_scan_tiles(uint32_t* __restrict__ tsum, uint64_t ntiles,
-                                                     Counters* __restrict__ ctr) {
+                                                     uint64_t ev_cap, Counters* __restrict__ ctr) {
   __shared__ uint32_t lds[17];
   __shared__ uint64_t run;
   if (threadIdx.x == 0) run = 0;
@@ -1754,10 +1774,15 @@ __global__ void __launch_bounds__(1024) k_scan_tiles(uint32_t* __restrict__ tsum
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    ctr->call_pos = ctr->log_count;
-    ctr->call_seq = ctr->seq_next;
-    ctr->log_count += run;
-    ctr->seq_next += run;
+    if (ctr->log_count + run > ev_cap) {  // does not fit: the call's events are dropped
+      ctr->call_pos = kDropped;
+      ctr->log_dropped = 1;
+    } else {
+      ctr->call_pos = ctr->log_count;
+      ctr->call_seq = ctr->seq_next;
+      ctr->log_count += run;
+      ctr->seq_next += run;
+    }
   }
 }
 
@@ -1779,6 +1804,7 @@ __global__ void __launch_bounds__(kThreads) k_write_events(const uint32_t* __res
   __shared__ claim_event s_ev[2 * kThreads];
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint64_t base_pos = ctr->call_pos, base_seq = ctr->call_seq;
+  if (base_pos == kDropped) return;  // uniform: the call's events did not fit
   uint64_t run = tprefix[blockIdx.x];  // events of the tile before this round
   for (uint32_t r = 0; r < kTile / kThreads; ++r) {
     const uint64_t c = (uint64_t)blockIdx.x * kTile + r * kThreads + threadIdx.x;
@@ -2187,14 +2213,15 @@ int append_events(claim_pool* P, const claim_batch* b, ClaimScratch sc) {
   if (C == 0) return CLAIM_OK;
   if (C <= kSmallEvents) {
     hipLaunchKernelGGL(k_events_small, dim3(1), dim3(1024), 0, P->stream, sc.cnt, sc.pend,
-                       b->claim_ids, C, P->ctr, P->log);
+                       b->claim_ids, C, P->ev_cap, P->ctr, P->log);
     return hip_status(hipGetLastError());
   }
   const uint64_t ntiles = (C + kTile - 1) / kTile;
   hipLaunchKernelGGL(k_tile_sums, dim3((uint32_t)ntiles), dim3(kThreads), 0, P->stream, sc.cnt, C,
                      sc.tsum);
   HIP_TRY(hipGetLastError());
-  hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, P->stream, sc.tsum, ntiles, P->ctr);
+  hipLaunchKernelGGL(k_scan_tiles, dim3(1), dim3(1024), 0, P->stream, sc.tsum, ntiles, P->ev_cap,
+                     P->ctr);
   HIP_TRY(hipGetLastError());
   hipLaunchKernelGGL(k_write_events, dim3((uint32_t)ntiles), dim3(kThreads), 0, P->stream, sc.cnt,
                      sc.pend, b->claim_ids, C, sc.tsum, P->ctr, P->log);
@@ -2705,6 +2732,7 @@ int outcomes_read(claim_pool* P, claim_outcome* out, uint32_t out_cap, uint32_t*
   TRY(read_counters(P));
   const uint64_t nev = P->host_ctr->log_count;
   const uint64_t nout = P->have_outcomes ? P->last_check_claims : 0;
+  const bool dropped = P->host_ctr->log_dropped != 0;
   if ((out && nout > out_cap) || (events && nev > ev_cap)) return CLAIM_ENOSPC;
   if (out) {
     if (nout) HIP_TRY(hipMemcpy(out, P->outcomes, nout * sizeof(claim_outcome), hipMemcpyDeviceToHost));
@@ -2716,12 +2744,17 @@ int outcomes_read(claim_pool* P, claim_outcome* out, uint32_t out_cap, uint32_t*
     P->host_ctr->log_count = 0;
     HIP_TRY(hipMemcpyAsync(&P->ctr->log_count, &P->host_ctr->log_count, sizeof(uint64_t),
                            hipMemcpyHostToDevice, P->stream));
+    if (dropped) {
+      P->host_ctr->log_dropped = 0;
+      HIP_TRY(hipMemcpyAsync(&P->ctr->log_dropped, &P->host_ctr->log_dropped, sizeof(uint32_t),
+                             hipMemcpyHostToDevice, P->stream));
+    }
     HIP_TRY(hipStreamSynchronize(P->stream));
     P->log_ub = 0;
   } else {
     P->log_ub = nev;
   }
-  return CLAIM_OK;
+  return dropped ? CLAIM_ENOSPC : CLAIM_OK;
 }
 
 int claim_block_state_read(claim_pool* P, uint32_t first, uint32_t count, uint64_t* d_off,
