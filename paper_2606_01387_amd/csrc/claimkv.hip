@@ -51,6 +51,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <new>
 
@@ -638,7 +639,11 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 // A piece is one 64-lane x LPW-word segment of a plane's chunk (piece index
 // ps = plane * segs + segment).  Workgroup (piece group pg, group g) runs 4
 // waves on the 4 consecutive pieces 4pg .. 4pg+3 of the same blocks
-// u = g, g + groups, g + 2 groups, ...: lane l, slot k of a wave covers the
+// u = g, g + groups, g + 2 groups, ...  Only pga piece groups are read at a
+// time (pga divides the piece-group count): workgroup blockIdx takes piece
+// groups pgl, pgl + pga, pgl + 2 pga, ... in turn (pgl = blockIdx % pga,
+// g = blockIdx / pga), each one a phase over its blocks, so every workgroup
+// runs the same number of phases.  Lane l, slot k of a wave covers the
 // 64-bit word q = s*64*LPW + 64k + l of the plane's chunk, canonical word
 // i = p*CW + q, whose key it keeps in VGPRs.  Each load instruction moves
 // 512 contiguous bytes (8 per lane); 8-byte loads measured about 2 % faster
@@ -704,7 +709,7 @@ struct KeyMap {
 template <int LPW, bool RAGGED, bool STAGE>
 __global__ void __launch_bounds__(kThreads) k_digest(const u32x2* __restrict__ pool, uint32_t nb,
                                                      uint32_t chunk_words, uint32_t planes,
-                                                     uint32_t segs, uint32_t groups,
+                                                     uint32_t segs, uint32_t pga, uint32_t groups,
                                                      const uint32_t* __restrict__ uniq,
                                                      const Counters* __restrict__ ctr,
                                                      uint64_t seed, KeyMap km,
@@ -715,70 +720,71 @@ __global__ void __launch_bounds__(kThreads) k_digest(const u32x2* __restrict__ p
   const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t ps_total = planes * segs;
   const uint32_t pgs = (ps_total + 3) / 4;
-  const uint32_t pg = blockIdx.x % pgs;
-  const uint32_t g = blockIdx.x / pgs;
+  const uint32_t g = blockIdx.x / pga;
   if (g >= groups) return;
-  const uint32_t ps = pg * 4 + w;
-  const bool active = ps < ps_total;  // wave-uniform: the last piece group may be short
-  const uint32_t p = active ? ps / segs : 0, s = active ? ps % segs : 0;
-  const uint32_t q0 = s * 64u * LPW + lane;  // this lane's word in slot 0
-
-  uint32_t klo[LPW], khi[LPW];
-#pragma unroll
-  for (int k = 0; k < LPW; ++k) {
-    const uint32_t q = q0 + 64u * k;
-    const uint64_t key = stream_output(seed, km.at(p, q)) | 1ull;
-    const bool ok = !RAGGED || q < chunk_words;
-    klo[k] = ok ? (uint32_t)key : 0u;  // a masked slot contributes 0
-    khi[k] = ok ? (uint32_t)(key >> 32) : 0u;
-  }
-
   const uint32_t U = ctr->uniq_count;
   const uint32_t NW = (U + groups - 1) / groups;
-  const u32x2* plane = pool + (uint64_t)p * nb * chunk_words;
-  uint32_t n = 0;
-  for (uint32_t u = g; u < U; u += groups, ++n) {
-    uint64_t sum = 0;
-    if (active) {
-      const u32x2* chunk = plane + (uint64_t)uniq[u] * chunk_words;
-      const u32x2* lanep = chunk + q0;  // slot k at lanep + 64k: immediate offsets
-      u32x2 x[LPW];
+  for (uint32_t pg = blockIdx.x % pga; pg < pgs; pg += pga) {  // one phase per piece group
+    const uint32_t ps = pg * 4 + w;
+    const bool active = ps < ps_total;  // wave-uniform: the last piece group may be short
+    const uint32_t p = active ? ps / segs : 0, s = active ? ps % segs : 0;
+    const uint32_t q0 = s * 64u * LPW + lane;  // this lane's word in slot 0
+
+    uint32_t klo[LPW], khi[LPW];
 #pragma unroll
-      for (int k = 0; k < LPW; ++k) {
-        // a masked slot reads the chunk's first word (its key is 0): no
-        // address outside the chunk is ever formed
-        if (!RAGGED || q0 + 64u * k < chunk_words)
-          x[k] = __builtin_nontemporal_load(lanep + 64 * k);
-        else
-          x[k] = __builtin_nontemporal_load(chunk);
-      }
-      __builtin_amdgcn_sched_barrier(0);  // every load in flight before any use
-      uint64_t acc = 0;
-      uint32_t cross = 0;
-#pragma unroll
-      for (int k = 0; k < LPW; ++k) {
-        // word = (x.y:x.x); only the low 32 bits of the cross terms reach
-        // the product mod 2^64
-        acc += (uint64_t)x[k].x * klo[k];
-        cross += x[k].x * khi[k] + x[k].y * klo[k];
-      }
-      sum = dpp_wave_sum64(acc + ((uint64_t)cross << 32));
-      if constexpr (STAGE) {
-        u32x2* dst = staging + ((uint64_t)u * planes + p) * chunk_words + q0;
-#pragma unroll
-        for (int k = 0; k < LPW; ++k)
-          if (!RAGGED || q0 + 64u * k < chunk_words) dst[64 * k] = x[k];
-      }
+    for (int k = 0; k < LPW; ++k) {
+      const uint32_t q = q0 + 64u * k;
+      const uint64_t key = stream_output(seed, km.at(p, q)) | 1ull;
+      const bool ok = !RAGGED || q < chunk_words;
+      klo[k] = ok ? (uint32_t)key : 0u;  // a masked slot contributes 0
+      khi[k] = ok ? (uint32_t)(key >> 32) : 0u;
     }
-    const uint32_t slot = n % kRing;
-    if (lane == 0) ring[w][slot] = sum;
-    if (slot == kRing - 1 || u + groups >= U) {  // the same for all 4 waves
-      __syncthreads();
-      const uint32_t n0 = n - slot;
-      for (uint32_t i = threadIdx.x; i <= slot; i += kThreads)
-        partial[((uint64_t)pg * groups + g) * NW + n0 + i] =
-            ring[0][i] + ring[1][i] + ring[2][i] + ring[3][i];
-      __syncthreads();
+
+    const u32x2* plane = pool + (uint64_t)p * nb * chunk_words;
+    uint32_t n = 0;
+    for (uint32_t u = g; u < U; u += groups, ++n) {
+      uint64_t sum = 0;
+      if (active) {
+        const u32x2* chunk = plane + (uint64_t)uniq[u] * chunk_words;
+        const u32x2* lanep = chunk + q0;  // slot k at lanep + 64k: immediate offsets
+        u32x2 x[LPW];
+#pragma unroll
+        for (int k = 0; k < LPW; ++k) {
+          // a masked slot reads the chunk's first word (its key is 0): no
+          // address outside the chunk is ever formed
+          if (!RAGGED || q0 + 64u * k < chunk_words)
+            x[k] = __builtin_nontemporal_load(lanep + 64 * k);
+          else
+            x[k] = __builtin_nontemporal_load(chunk);
+        }
+        __builtin_amdgcn_sched_barrier(0);  // every load in flight before any use
+        uint64_t acc = 0;
+        uint32_t cross = 0;
+#pragma unroll
+        for (int k = 0; k < LPW; ++k) {
+          // word = (x.y:x.x); only the low 32 bits of the cross terms reach
+          // the product mod 2^64
+          acc += (uint64_t)x[k].x * klo[k];
+          cross += x[k].x * khi[k] + x[k].y * klo[k];
+        }
+        sum = dpp_wave_sum64(acc + ((uint64_t)cross << 32));
+        if constexpr (STAGE) {
+          u32x2* dst = staging + ((uint64_t)u * planes + p) * chunk_words + q0;
+#pragma unroll
+          for (int k = 0; k < LPW; ++k)
+            if (!RAGGED || q0 + 64u * k < chunk_words) dst[64 * k] = x[k];
+        }
+      }
+      const uint32_t slot = n % kRing;
+      if (lane == 0) ring[w][slot] = sum;
+      if (slot == kRing - 1 || u + groups >= U) {  // the same for all 4 waves
+        __syncthreads();
+        const uint32_t n0 = n - slot;
+        for (uint32_t i = threadIdx.x; i <= slot; i += kThreads)
+          partial[((uint64_t)pg * groups + g) * NW + n0 + i] =
+              ring[0][i] + ring[1][i] + ring[2][i] + ring[3][i];
+        __syncthreads();
+      }
     }
   }
 }
@@ -1916,7 +1922,8 @@ struct claim_pool {
   void* kv = nullptr;
 
   int lpw = 32;
-  uint32_t segs = 1, ps_total = 1, pgs = 1, groups = 1;
+  uint32_t segs = 1, ps_total = 1, pgs = 1;
+  uint32_t slots = 1;  // digest workgroups resident at once (per CU x CUs)
 
   uint64_t *d_off = nullptr, *partial = nullptr;
   BlockRes* bres = nullptr;  // per block: restored digest, latest reported failure
@@ -2150,8 +2157,15 @@ int select_blocks(claim_pool* P, const claim_batch* b, int mode) {
   return hip_status(hipGetLastError());
 }
 
+// The digest grid of one launch: pga piece groups read at a time, groups
+// workgroups on each (grid = pga x groups).
+struct DigestGrid {
+  uint32_t pga, groups;
+};
+
 template <int LPW>
-int launch_digest_lpw(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_cu) {
+int launch_digest_lpw(claim_pool* P, DigestGrid gr, uint64_t* partial, void* staging,
+                      int* wgs_per_cu) {
   const uint32_t cw = (uint32_t)(2 * P->chunk_vecs);
   const bool ragged = (uint64_t)P->segs * 64 * LPW != cw;
   const void* fn;
@@ -2163,10 +2177,10 @@ int launch_digest_lpw(claim_pool* P, uint64_t* partial, void* staging, int* wgs_
     return hip_status(hipOccupancyMaxActiveBlocksPerMultiprocessor(wgs_per_cu, fn, kThreads, 0));
   const u32x2* pool = (const u32x2*)P->kv;
   u32x2* st = (u32x2*)staging;
-  const dim3 grid(P->pgs * P->groups), block(kThreads);
+  const dim3 grid(gr.pga * gr.groups), block(kThreads);
 #define GO(R, S)                                                                                \
   hipLaunchKernelGGL((k_digest<LPW, R, S>), grid, block, 0, P->stream, pool, P->nb, cw, P->planes, \
-                     P->segs, P->groups, P->uniq, P->ctr, P->seed, P->kmap, partial, st)
+                     P->segs, gr.pga, gr.groups, P->uniq, P->ctr, P->seed, P->kmap, partial, st)
   if (ragged) {
     if (staging) GO(true, true); else GO(true, false);
   } else {
@@ -2176,12 +2190,13 @@ int launch_digest_lpw(claim_pool* P, uint64_t* partial, void* staging, int* wgs_
   return hip_status(hipGetLastError());
 }
 
-// Launch the digest (or, with wgs_per_cu, query its occupancy).
-int launch_digest(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_cu = nullptr) {
+// Launch the digest on grid gr (or, with wgs_per_cu, query its occupancy).
+int launch_digest(claim_pool* P, DigestGrid gr, uint64_t* partial, void* staging,
+                  int* wgs_per_cu = nullptr) {
   switch (P->lpw) {
 #define DIGEST_CASE(l) \
   case l:              \
-    return launch_digest_lpw<l>(P, partial, staging, wgs_per_cu);
+    return launch_digest_lpw<l>(P, gr, partial, staging, wgs_per_cu);
     DIGEST_CASE(1) DIGEST_CASE(2) DIGEST_CASE(4) DIGEST_CASE(8) DIGEST_CASE(12) DIGEST_CASE(16)
     DIGEST_CASE(24) DIGEST_CASE(32)
 #undef DIGEST_CASE
@@ -2190,10 +2205,10 @@ int launch_digest(claim_pool* P, uint64_t* partial, void* staging, int* wgs_per_
   }
 }
 
-int launch_finalize(claim_pool* P, int mode, int staged) {
-  const uint32_t grid = grid_for((uint64_t)P->nb + P->groups);  // slots <= U + groups
+int launch_finalize(claim_pool* P, DigestGrid gr, int mode, int staged) {
+  const uint32_t grid = grid_for((uint64_t)P->nb + gr.groups);  // slots <= U + groups
   hipLaunchKernelGGL(k_finalize, dim3(grid), dim3(kThreads), 0, P->stream, P->uniq, P->ctr,
-                     P->partial, P->pgs, P->groups, mode, staged, P->d_off, P->valid_off,
+                     P->partial, P->pgs, gr.groups, mode, staged, P->d_off, P->valid_off,
                      P->slot_of, P->bres);
   return hip_status(hipGetLastError());
 }
@@ -2264,8 +2279,9 @@ int append_events(claim_pool* P, const claim_batch* b, ClaimScratch sc) {
 // streams up to 16 KiB per block; chunks that are not a whole number of
 // 512-byte rows, or whose only exact widths are tiny, use the smallest width
 // covering the chunk (at most 32) with a ragged last segment.  The grid is
-// persistent and fully resident (no tail of late waves): groups = workgroups
-// per CU x CUs / piece groups.  Workgroups per CU: enough for about
+// persistent and fully resident (no tail of late waves): slots = workgroups
+// per CU x CUs, shared by the piece groups read at a time (digest_grid).
+// Workgroups per CU: enough for about
 // kInflightPerCu bytes of loads in flight per CU (each wave keeps
 // LPW x 512 bytes in flight), at most what can be resident.  Measured on
 // MI355X in one process over one pool allocation, 32 KiB per CU read the
@@ -2297,16 +2313,58 @@ int choose_digest_shape(claim_pool* P) {
   P->ps_total = P->planes * P->segs;
   P->pgs = (P->ps_total + 3) / 4;
   int per_cu = 0;
-  TRY(launch_digest(P, nullptr, nullptr, &per_cu));  // the check kernel's occupancy
-  const int wg_bytes = 4 * best * 64 * 8;             // loads in flight per workgroup
+  TRY(launch_digest(P, DigestGrid{1, 1}, nullptr, nullptr, &per_cu));  // the kernel's occupancy
+  const int wg_bytes = 4 * best * 64 * 8;  // loads in flight per workgroup
   const int want = kInflightPerCu / wg_bytes > 1 ? kInflightPerCu / wg_bytes : 1;
   if (per_cu > want) per_cu = want;
   if (per_cu < 1) per_cu = 1;
-  uint64_t g = (uint64_t)per_cu * P->cus / P->pgs;
-  if (g < 1) g = 1;
-  if (g > P->nb) g = P->nb;
-  P->groups = (uint32_t)g;
+  P->slots = (uint32_t)per_cu * P->cus;
   return CLAIM_OK;
+}
+
+// How many piece groups a digest launch reads at a time (pga, a divisor of
+// the piece-group count, so that every workgroup runs the same number of
+// phases) and how many workgroups share each (groups = slots / pga).
+//
+// Reading every piece group at once suits pools up to a few tens of GB, but
+// not the largest.  Measured on MI355X in one process over one allocation,
+// every block referenced once: with all piece groups at once, pools of 13 to
+// 30 GB read at 6.96-7.20 TB/s, while pools of 84 and 105 GB read at only
+// 6.77-6.84 TB/s.  The same 84 and 105 GB pools read in phases of 2.6-5.2 GB
+// reached 7.07-7.10 TB/s.  The loss is not address translation: the phased
+// launches take more translation misses (about 46 000 and 113 000 per launch
+// against 2 000 on the 105 GB pool).  What separates them is the number of
+// requests outstanding at the memory interface: about 6 000-6 240 on
+// average with phases against 5 500-5 660 without.  A phase costs a key
+// computation and a ring flush, which a pool with few blocks per workgroup
+// feels (a 21 GB pool of 4000 blocks read in 80 phases: -6 %), so phases
+// start only past kOnePhaseBytes of referenced blocks, each phase then
+// covering at most kPhaseBytes.  Independently, a launch whose
+// one-phase grid would leave more than 15 % of the slots idle (many piece
+// groups, few slots each) reads in phases that fill it (320 planes: 6.05 ->
+// 7.2 TB/s).  refs bounds the launch's unique blocks.
+constexpr uint64_t kOnePhaseBytes = 32ull << 30;
+constexpr uint64_t kPhaseBytes = 4ull << 30;
+constexpr uint32_t kMinFillPct = 85;
+
+DigestGrid digest_grid(const claim_pool* P, uint64_t refs) {
+  const uint64_t ub = std::max<uint64_t>(1, std::min<uint64_t>(refs, P->nb));
+  const long double bytes = (long double)ub * P->block_bytes;
+  DigestGrid best{1, 1};
+  uint64_t best_fill = 0;
+  for (uint32_t d = P->pgs; d >= 1; --d) {
+    if (P->pgs % d) continue;
+    const bool one = bytes <= (long double)kOnePhaseBytes;
+    if (d > 1 && !one && bytes * d > (long double)kPhaseBytes * P->pgs) continue;
+    const uint64_t groups = std::min<uint64_t>(std::max<uint32_t>(1u, P->slots / d), ub);
+    const uint64_t fill = (uint64_t)d * groups;
+    if (fill * 100 >= (uint64_t)kMinFillPct * P->slots) return {d, (uint32_t)groups};
+    if (fill > best_fill) {
+      best_fill = fill;
+      best = {d, (uint32_t)groups};
+    }
+  }
+  return best;
 }
 
 void free_pool(claim_pool* P) {
@@ -2433,7 +2491,7 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
 
     const uint64_t nb = d->num_blocks;
     if ((rc = dalloc(&P->d_off, nb)) || (rc = dalloc(&P->bres, nb)) ||
-        (rc = dalloc(&P->partial, (uint64_t)P->pgs * (nb + P->groups))) ||
+        (rc = dalloc(&P->partial, (uint64_t)P->pgs * (nb + P->slots))) ||
         (rc = dalloc(&P->valid_off, nb)) || (rc = dalloc(&P->mark, (nb + 15) / 16 * 16)) ||
         (rc = dalloc(&P->uniq, nb)) || (rc = dalloc(&P->slot_of, nb)) ||
         (rc = dalloc(&P->owner_at, nb)) || (rc = dalloc(&P->holder, nb)))
@@ -2540,8 +2598,9 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
   // each claim's digests into its own offload record
   P->gen += 1;
   if (staging) TRY(fill<uint32_t>(P, P->slot_of, P->nb, kNone));
-  TRY(launch_digest(P, P->partial, staging));
-  TRY(launch_finalize(P, 0, staging != nullptr));
+  const DigestGrid gr = digest_grid(P, b->num_refs);
+  TRY(launch_digest(P, gr, P->partial, staging));
+  TRY(launch_finalize(P, gr, 0, staging != nullptr));
   if (C) {
     LAUNCH_GROUPED(k_accept, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->seed, P->fp_used, fpo,
                    P->d_off, P->fp_store, P->ctr, P->cnt, P->pend);
@@ -2647,9 +2706,10 @@ int check_body(claim_pool* P, const claim_batch* b, claim_outcome* out, ClaimScr
   TRY(record_stage(P, slot, 0));
   TRY(select_blocks(P, b, kMarkOffloaded));  // recorded blocks of the well-formed rows
   TRY(record_stage(P, slot, 1));
-  TRY(launch_digest(P, P->partial, nullptr));
+  const DigestGrid gr = digest_grid(P, b->num_refs);
+  TRY(launch_digest(P, gr, P->partial, nullptr));
   TRY(record_stage(P, slot, 2));
-  TRY(launch_finalize(P, 1, 0));
+  TRY(launch_finalize(P, gr, 1, 0));
   TRY(record_stage(P, slot, 3));
   if (C) {
     CheckState st;

@@ -136,6 +136,20 @@ MIN_BS = Workload(
     length=("blocks", 1, 90, True), sharing=("zipf", 1.2, 5), corrupt_rate=0.1, num_load_failed=2,
     gen_seed=38, content_seed=39)
 
+# Many planes with few digest workgroups each: the digest reads its piece
+# groups in phases so that the grid stays full.  320 planes of 32 KiB chunks
+# (160 piece groups, two phases of 80) and 122 planes of 36 KiB chunks in
+# three 12 KiB pieces each (92 piece groups, the last with two pieces; two
+# phases of 46).
+MANY_PLANES = Workload(
+    name="320-planes-phased", geometry=Geometry(160, 2, 16, 8, 128, 2, 24), seed=41, num_claims=30,
+    length=("blocks", 1, 6, True), sharing=("fraction", 0.3), corrupt_rate=0.15, num_load_failed=1,
+    gen_seed=42, content_seed=43)
+MANY_PLANES_RAGGED = Workload(
+    name="122-planes-phased-short-last-group", geometry=Geometry(122, 1, 64, 1, 576, 1, 10),
+    seed=44, num_claims=12, length=("blocks", 1, 4, True), sharing=("fraction", 0.3),
+    corrupt_rate=0.2, num_load_failed=1, gen_seed=45, content_seed=46)
+
 SCALED = [
     replace(TINY, num_load_failed=1),
     scaled(FULL["llama3-8b"], 48, 60, corrupt_rate=0.1, num_load_failed=2),
@@ -160,6 +174,8 @@ SCALED = [
     # one GPU's head shard of the 70B pool under 8-way tensor parallelism
     scaled(SHARDS["llama3-70b-tp8-shard"], 24, 40, corrupt_rate=0.1, missing_claim_rate=0.1,
            num_load_failed=1),
+    MANY_PLANES,
+    MANY_PLANES_RAGGED,
 ]
 
 
@@ -699,6 +715,7 @@ STAGED = [
     scaled(FULL["mla-fp8"], 30, 40, corrupt_rate=0.1, num_load_failed=1),  # 3 pieces per chunk
     scaled(FULL["small-claim-stress"], 96, 300, corrupt_rate=0.1, num_load_failed=1),  # 1 piece
     TINY_CHUNK,  # 48-byte chunks: one ragged piece
+    MANY_PLANES_RAGGED,  # staging written in two phases
 ]
 
 
