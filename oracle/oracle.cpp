@@ -385,6 +385,22 @@ int orc_canonical_block(const uint8_t* pool, uint32_t planes, uint32_t num_block
   return ORC_OK;
 }
 
+/* The block digest of every block of a host pool laid out
+ * [plane][block][chunk]: block b's canonical bytes (as orc_canonical_block
+ * forms them) digested with block_digest, one block after another.  Only a
+ * loop over the single-block definition, for pools with millions of
+ * blocks. */
+int orc_pool_digests(const uint8_t* pool, uint32_t planes, uint32_t num_blocks,
+                     uint64_t chunk_bytes, uint64_t seed, uint64_t* out) {
+  if ((planes * chunk_bytes) % 8) return ORC_EINVAL;
+  std::vector<uint8_t> canon(planes * chunk_bytes);
+  for (uint32_t b = 0; b < num_blocks; ++b) {
+    orc_canonical_block(pool, planes, num_blocks, chunk_bytes, b, canon.data());
+    out[b] = block_digest(canon.data(), canon.size(), seed);
+  }
+  return ORC_OK;
+}
+
 /* Flip canonical bit `bit` of block b in place (bit 0 = least significant
  * bit of canonical byte 0). */
 int orc_apply_flip(uint8_t* pool, uint32_t planes, uint32_t num_blocks, uint64_t chunk_bytes,

@@ -113,6 +113,7 @@ def lib() -> ctypes.CDLL:
             ("orc_kv_key", [u64, u64], u64),
             ("orc_token_key", [u64, u64], u64),
             ("orc_block_digest", [vp, u64, u64], u64),
+            ("orc_pool_digests", [vp, u32, u32, u64, u64, vp], ctypes.c_int),
             ("orc_shard_digest", [vp, u32, u32, u32, u32, u32, u32, u64], u64),
             ("orc_token_multilinear", [vp, u64, u64], u64),
             ("orc_chain", [vp, u64, u32, u64, vp], u64),
@@ -231,7 +232,14 @@ def pool_digests(pool: np.ndarray, planes: int, num_blocks: int, chunk_bytes: in
                  blocks=None) -> np.ndarray:
     """Digest of every (or of each listed) block of a host pool array."""
     out = np.zeros(num_blocks, dtype=np.uint64)
-    for b in range(num_blocks) if blocks is None else blocks:
+    if blocks is None:  # every block, in one loop of the oracle library
+        p = _arr(pool, np.uint8).reshape(-1)
+        assert p.size >= planes * num_blocks * chunk_bytes
+        rc = lib().orc_pool_digests(_ptr(p), planes, num_blocks, chunk_bytes, seed, _ptr(out))
+        if rc != OK:
+            raise ValueError("block bytes not a whole number of 64-bit words")
+        return out
+    for b in blocks:
         out[b] = block_digest(canonical_block(pool, planes, num_blocks, chunk_bytes, int(b)), seed)
     return out
 
@@ -250,6 +258,7 @@ class OraclePool:
         self.num_blocks = num_blocks
         self.block_size = block_size
         self.seed = seed
+        self._free = lib().orc_pool_free  # kept: module globals may be gone at exit
         self._h = lib().orc_pool_new(num_blocks, block_size, seed)
         if not self._h:
             raise ValueError("bad pool geometry")
@@ -257,7 +266,7 @@ class OraclePool:
     def __del__(self):
         h = getattr(self, "_h", None)
         if h:
-            lib().orc_pool_free(h)
+            self._free(h)
             self._h = None
 
     @staticmethod

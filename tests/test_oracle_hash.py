@@ -216,6 +216,22 @@ def test_canonical_block_is_plane_major_concatenation():
             assert not O.canonical_block(pool, planes, nb, chunk, other).any()
 
 
+def test_whole_pool_digests_are_the_single_block_digests():
+    rng = np.random.default_rng(12)
+    for planes, nb, chunk in ((1, 7, 16), (3, 5, 32), (4, 9, 8)):
+        pool = rng.integers(0, 256, size=planes * nb * chunk, dtype=np.uint8)
+        whole = O.pool_digests(pool, planes, nb, chunk, 23)
+        one = [O.block_digest(O.canonical_block(pool, planes, nb, chunk, b), 23) for b in range(nb)]
+        assert whole.tolist() == one
+    # one set byte reaches only its own block, weighted by its word's key
+    planes, nb, chunk = 3, 5, 32
+    pool = np.zeros(planes * nb * chunk, np.uint8)
+    pool[(2 * nb + 3) * chunk + 11] = 0x5C
+    idx = 2 * chunk + 11
+    want = (0x5C << (8 * (idx % 8))) * O.kv_key(17, idx // 8) & M64
+    assert O.pool_digests(pool, planes, nb, chunk, 17).tolist() == [0, 0, 0, want, 0]
+
+
 def test_apply_flip_addresses_canonical_bits():
     planes, nb, chunk = 4, 3, 16
     rng = np.random.default_rng(6)
