@@ -150,6 +150,15 @@ MANY_PLANES_RAGGED = Workload(
     seed=44, num_claims=12, length=("blocks", 1, 4, True), sharing=("fraction", 0.3),
     corrupt_rate=0.2, num_load_failed=1, gen_seed=45, content_seed=46)
 
+# 2^22 blocks (two 16-byte chunks each, a 128 MiB pool) under 100 000
+# claims of 1-80 blocks: 3.8 M unique blocks, so the mark array is
+# compacted in many passes, each digest workgroup flushes its partials
+# many times, and the event scan runs over many tiles.
+MANY_BLOCKS = Workload(
+    name="4m-blocks", geometry=Geometry(1, 2, 1, 1, 8, 2, 1 << 22), seed=51, num_claims=100_000,
+    length=("blocks", 1, 80, True), sharing=("fraction", 0.2), corrupt_rate=0.0005,
+    num_load_failed=3, gen_seed=52, content_seed=53)
+
 SCALED = [
     replace(TINY, num_load_failed=1),
     scaled(FULL["llama3-8b"], 48, 60, corrupt_rate=0.1, num_load_failed=2),
@@ -176,6 +185,7 @@ SCALED = [
            num_load_failed=1),
     MANY_PLANES,
     MANY_PLANES_RAGGED,
+    MANY_BLOCKS,
 ]
 
 
