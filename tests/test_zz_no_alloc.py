@@ -89,3 +89,35 @@ def test_check_static_matches_check(torch, ck):
         same_outcomes(got, op.check(b, d1))
     del kv
     free_gpu(torch)
+
+
+def test_check_static_at_its_limit(torch, ck):
+    # exactly CLAIM_STATIC_MAX_CLAIMS claims: every byte of the fixed scratch
+    w = scaled(FULL["small-claim-stress"], 256, ck.STATIC_MAX_CLAIMS, corrupt_rate=0.05,
+               num_load_failed=3)
+    g = w.geometry
+    batch = make_batch(w)
+    faults = make_faults(w, batch)
+    assert batch.num_claims == ck.STATIC_MAX_CLAIMS
+    note(f"check_static at its limit: {batch.num_claims} claims over {g.num_blocks} blocks")
+    kv = gpu_pool_tensor(torch, w)
+    with ck.Pool(g, w.seed, kv, max_claims=2 * batch.num_claims, max_footprint=2 * batch.num_refs,
+                 event_capacity=6 * batch.num_claims) as pool:
+        db = ck.DeviceBatch(batch)
+        pool.offload(db)
+        pool.restore(db, faults=faults)
+        pool.read()
+        pool.check(db)
+        want, want_ev = pool.read()
+        out = pool.check_static(db)
+        _, got_ev = pool.read()
+        got = out.cpu().numpy().view(ck.OUTCOME_DTYPE)[: batch.num_claims].copy()
+        same_outcomes(got, want)
+        assert got_ev.size == want_ev.size
+        for f in EV_FIELDS:
+            assert np.array_equal(got_ev[f], want_ev[f]), f
+        codes = np.bincount(got["code"], minlength=3)
+        note(f"  outcomes unknown/materialized/failed = {codes.tolist()}, {got_ev.size} events")
+        assert codes[1] and codes[2]
+    del kv
+    free_gpu(torch)
