@@ -299,6 +299,26 @@ def main() -> int:
     out, ev = pool.read()
     state = pool.block_state()
 
+    # outcomes_read of one check (its outcomes and events, D2H), timed apart:
+    # into page-locked host buffers, then into new pageable arrays
+    out_pin = torch.empty(max(1, C) * ck.OUTCOME_DTYPE.itemsize, dtype=torch.uint8, pin_memory=True)
+    ev_pin = torch.empty((2 * C + 16) * ck.EVENT_DTYPE.itemsize, dtype=torch.uint8, pin_memory=True)
+    read = {}
+    for kind in ("pinned", "pageable"):
+        pool.check(db)
+        torch.cuda.synchronize()
+        r0 = time.perf_counter()
+        if kind == "pinned":
+            o1, e1 = pool.read(out=out_pin.numpy().view(ck.OUTCOME_DTYPE),
+                               events=ev_pin.numpy().view(ck.EVENT_DTYPE))
+        else:
+            o1, e1 = pool.read(max_outcomes=max(1, C), max_events=2 * C + 16)
+        r1 = time.perf_counter()
+        assert np.array_equal(o1, out), "a repeated check read back other outcomes"
+        nbytes = o1.size * ck.OUTCOME_DTYPE.itemsize + e1.size * ck.EVENT_DTYPE.itemsize
+        read[kind] = (r1 - r0, nbytes, int(e1.size))
+    del out_pin, ev_pin
+
     # spread of single checks, in a separate pass after the timed region:
     # hipEvents on the pool stream around each check
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
@@ -392,6 +412,18 @@ def main() -> int:
         "hit_tokens": int(lk["hit_tokens"].sum()),
         "status_unknown_hit_partial_miss": np.bincount(lk["status"], minlength=4).tolist(),
         "identities_registered_ambiguous": list(identities),
+    }
+    line["outcomes_read"] = {
+        "bytes": read["pinned"][1],
+        "outcomes": int(out.size),
+        "events": read["pinned"][2],
+        "pinned_ms": round(read["pinned"][0] * 1e3, 3),
+        "pinned_GBps": round(read["pinned"][1] / read["pinned"][0] / 1e9, 2),
+        "pageable_ms": round(read["pageable"][0] * 1e3, 3),
+        "pageable_GBps": round(read["pageable"][1] / read["pageable"][0] / 1e9, 2),
+        "note": "one outcomes_read call after one more check: that check's outcomes and events, "
+                "D2H into page-locked host buffers, then into new pageable arrays (synchronous "
+                "copies, host wall time)",
     }
     if round_trip is not None:
         line["round_trip"] = round_trip

@@ -332,18 +332,34 @@ class Pool:
         self._inflight = []  # waited for the stream
         return int(e.value), int(a.value)
 
-    def read(self, max_outcomes: int = 1 << 22, max_events: int | None = None):
-        """(outcomes of the last check, events since the last read)."""
-        if max_events is None:
-            max_events = self.event_capacity
-        out = np.zeros(max_outcomes, dtype=OUTCOME_DTYPE)
-        ev = np.zeros(max_events, dtype=EVENT_DTYPE)
+    def read(self, max_outcomes: int = 1 << 22, max_events: int | None = None, out=None,
+             events=None):
+        """(outcomes of the last check, events since the last read).
+
+        With ``out`` / ``events`` (host arrays of OUTCOME_DTYPE / EVENT_DTYPE,
+        for instance views of page-locked memory) the records are written
+        there and views of them are returned; otherwise into new arrays."""
+        if out is None:
+            out = np.zeros(max_outcomes, dtype=OUTCOME_DTYPE)
+            fresh_out = True
+        else:
+            assert out.dtype == OUTCOME_DTYPE and out.flags["C_CONTIGUOUS"]
+            fresh_out = False
+        if events is None:
+            events = np.zeros(self.event_capacity if max_events is None else max_events,
+                              dtype=EVENT_DTYPE)
+            fresh_ev = True
+        else:
+            assert events.dtype == EVENT_DTYPE and events.flags["C_CONTIGUOUS"]
+            fresh_ev = False
         n_out = ctypes.c_uint32()
         n_ev = ctypes.c_uint64()
         _check(lib().outcomes_read(self._h, out.ctypes.data, out.size, ctypes.byref(n_out),
-                                   ev.ctypes.data, ev.size, ctypes.byref(n_ev)), "outcomes_read")
+                                   events.ctypes.data, events.size, ctypes.byref(n_ev)),
+               "outcomes_read")
         self._inflight = []  # waited for the stream
-        return out[: n_out.value].copy(), ev[: n_ev.value].copy()
+        o, e = out[: n_out.value], events[: n_ev.value]
+        return (o.copy() if fresh_out else o), (e.copy() if fresh_ev else e)
 
     def block_state(self, first: int = 0, count: int | None = None) -> dict:
         """Per-block digests and flags of blocks [first, first + count)."""
