@@ -2,7 +2,9 @@
 oracle: block sizes, head counts, head widths and element sizes that give
 chunks from 16 bytes to 72 KiB (every words-per-lane width the kernel
 instantiates, whole and ragged chunks, one or several segments per chunk),
-planes from 1 to 12, and head shards at random offsets.  Every block's
+planes from 1 to 12, and head shards at random offsets; and pools of 100 to
+860 planes over 8 to 16 blocks, whose digest mostly reads its piece groups
+in phases (one phase would leave much of the grid idle).  Every block's
 offload digest, and its restore digest after seeded flips, must equal the
 oracle's."""
 
@@ -54,11 +56,42 @@ def random_geometry(rng) -> Geometry:
         return Geometry(layers, ppl, bs, heads, dim, eb, nb)
 
 
+# Chunks of 12 to 72 words per lane (6 to 36 KiB) and the segments they
+# split into: pieces of 12, 16, 24 or 32 words per lane, one digest
+# workgroup per CU.
+_PLANE_CHUNKS = [(6144, 1), (8192, 1), (12288, 1), (16384, 1), (24576, 2), (32768, 2), (36864, 3)]
+
+
+def many_plane_geometry(rng) -> Geometry:
+    """Planes enough for 87-108 or 130-216 piece groups of 4 pieces (the
+    last group often short): one phase would fill at most 85 % of a grid of
+    one workgroup per CU on 256 CUs."""
+    while True:
+        chunk, segs = _PLANE_CHUNKS[int(rng.integers(len(_PLANE_CHUNKS)))]
+        pgs = int(rng.integers(87, 109)) if rng.random() < 0.3 else int(rng.integers(130, 217))
+        planes = max(1, (4 * pgs - int(rng.integers(0, 4))) // segs)
+        ppl = 2 if planes % 2 == 0 and rng.random() < 0.5 else 1
+        bs = int(rng.choice([1, 2, 4, 8, 16]))
+        nb = int(rng.integers(8, 17))  # enough blocks for several workgroups per phase
+        if planes * chunk * nb > 160 << 20:
+            continue
+        return Geometry(planes // ppl, ppl, bs, 1, chunk // bs, 1, nb)
+
+
 # CLAIMKV_SHAPE_SEEDS widens a one-off run; the suite runs the first 60
 @pytest.mark.parametrize("seed", range(int(os.environ.get("CLAIMKV_SHAPE_SEEDS", "60"))))
 def test_digest_shapes(torch, ck, seed):
     rng = np.random.default_rng(70_000 + seed)
-    g = random_geometry(rng)
+    run_shape(torch, ck, random_geometry(rng), rng, seed)
+
+
+@pytest.mark.parametrize("seed", range(int(os.environ.get("CLAIMKV_PLANE_SEEDS", "16"))))
+def test_digest_shapes_many_planes(torch, ck, seed):
+    rng = np.random.default_rng(80_000 + seed)
+    run_shape(torch, ck, many_plane_geometry(rng), rng, seed)
+
+
+def run_shape(torch, ck, g, rng, seed):
     w = Workload(name=f"shape-{seed}", geometry=g, seed=int(rng.integers(0, 2**63)), num_claims=0,
                  length=TINY.length, sharing=TINY.sharing, corrupt_rate=0.0, gen_seed=seed,
                  content_seed=int(rng.integers(0, 2**31)))
