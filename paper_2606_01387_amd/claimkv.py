@@ -161,7 +161,8 @@ class DeviceBatch:
     ``batch`` is any object with numpy arrays ``claim_ids`` (u64),
     ``block_offsets`` (u32), ``block_ids`` (u32), ``token_offsets`` (u64)
     and ``tokens`` (u32), and optionally ``predicate_tokens`` (u64 per claim
-    or None)."""
+    or None).  The upload is complete when the constructor returns, so a
+    pool on any stream may use the batch."""
 
     def __init__(self, batch, device="cuda"):
         torch = _torch()
@@ -179,6 +180,9 @@ class DeviceBatch:
         self.tok = up(batch.tokens, np.uint32, torch.int32)
         pred = getattr(batch, "predicate_tokens", None)
         self.pred = None if pred is None else up(pred, np.uint64, torch.int64)
+        # copies from pageable memory may still be in flight on the current
+        # stream; the pool's kernels can run on another one
+        torch.cuda.current_stream(self.ids.device).synchronize()
         n_claims = int(self.ids.numel())
         # the kernels read offsets[c + 1] and predicate[c] for every claim c
         if n_claims and (self.bo.numel() != n_claims + 1 or self.to.numel() != n_claims + 1):
