@@ -404,6 +404,7 @@ def test_controls_mirrored(torch, ck):
     m.offload(empty)
     m.restore(empty)
     m.check(empty)
+    assert m.lookup(empty).size == 0
     m.finish()
     del m
     free_gpu(torch)

@@ -121,3 +121,18 @@ def test_check_static_at_its_limit(torch, ck):
         assert codes[1] and codes[2]
     del kv
     free_gpu(torch)
+
+
+def test_check_static_empty_batch(torch, ck):
+    # no claims: nothing to write, no events, and the log stays as it was
+    w = scaled(FULL["small-claim-stress"], 64, 8)
+    kv = gpu_pool_tensor(torch, w)
+    with ck.Pool(w.geometry, w.seed, kv, max_claims=64, max_footprint=256,
+                 event_capacity=256) as pool:
+        empty = ck.DeviceBatch(from_claims([]))
+        out = pool.check_static(empty)
+        got, ev = pool.read()
+        assert got.size == 0 and ev.size == 0
+        assert out.numel() >= ck.OUTCOME_DTYPE.itemsize
+    del kv
+    free_gpu(torch)
