@@ -314,12 +314,19 @@ int claim_pool_destroy(claim_pool* pool);
  * never removed.  With staging != NULL the canonical bytes of every such
  * block are also written to staging (device memory or host memory from
  * hipHostMalloc, 16-byte aligned, else EINVAL), one block after another in
- * ascending block-id order; staging_bytes must cover them (else ENOSPC).
- * Staging holds one generation: a staged offload replaces the previous
- * one, so claim_restore can copy back only blocks of the last staged
- * offload; blocks staged only by an earlier offload are then used as the
- * pool holds them (a claim whose bytes are gone fails closed on its digest
- * compare), although lookups may still hit their identities.  Waits twice
+ * ascending block-id order, as the offload tier of section 7 paths A and B.
+ * Staged offloads into the same staging buffer accumulate: each appends its
+ * blocks after those the buffer already holds, and a block's staged copy is
+ * its latest staged offload's.  staging_bytes must cover the blocks already
+ * there and this offload's (else ENOSPC).  A staged offload into another
+ * buffer starts a new generation, as does claim_staging_reset: the blocks
+ * staged before are no longer restored from staging.  An offload without
+ * staging drops the staged copies of its blocks (they are no longer the
+ * bytes of the block's latest offload).  A block with no staged copy is used
+ * as the pool holds it (a claim whose bytes are gone fails closed on its
+ * digest compare), although lookups may still hit its identity.  Stores
+ * are not deduplicated across calls: a block staged again takes a new slot.
+ * Waits twice
  * for the stream to read the acceptance verdict (three times when a block
  * row runs backwards).  ENOSPC if the registry, footprint store or event
  * log could overflow; the footprint store takes num_refs entries, or, when
@@ -328,15 +335,22 @@ int claim_offload(claim_pool* pool, const claim_batch* batch, void* staging,
                   uint64_t staging_bytes);
 
 /* Restore (section 7 path A steps 4-5, path B steps 3-5).  If staging is
- * not NULL it must hold the bytes of the pool's last staged offload
- * (staging_bytes covering every block it staged, else EINVAL): every staged
- * block referenced by a well-formed claim of the batch is copied back into
- * the pool.  Then the faults are applied (faults may be NULL).  Then each
+ * not NULL it must be the buffer of the pool's current staging generation
+ * (staging_bytes covering every slot staged to it, else EINVAL): every
+ * block with a staged copy that a well-formed claim of the batch references
+ * is copied back into the pool from that copy.  Then the faults are applied (faults may be NULL).  Then each
  * well-formed, registered and OFFLOADED claim of the batch moves to
  * RESTORE_REQUIRED (event RESTORE_REQUIRED).  EINVAL for an out-of-range
  * fault or a staging pointer that is not 16-byte aligned. */
 int claim_restore(claim_pool* pool, const claim_batch* batch, const void* staging,
                   uint64_t staging_bytes, const claim_fault_spec* faults);
+
+/* Start a new staging generation (section 7 paths A and B: the offload
+ * tier): no block keeps a staged copy, and the next staged offload writes
+ * from the start of its buffer, whichever buffer it is.  For a caller that
+ * reuses one staging buffer for unrelated offloads.  Queued on the pool's
+ * stream; EINVAL for a NULL pool. */
+int claim_staging_reset(claim_pool* pool);
 
 /* Check (section 7 path A step 5, path B steps 5-7, path C): digest every
  * in-range block with an offload record that the well-formed claims

@@ -51,8 +51,9 @@ LOOKUP_DTYPE = np.dtype(
      ("hit_blocks", "<u4"), ("last_block", "<u4"), ("reserved", "<u4")])
 
 EXPORTS = ("claim_pool_create", "claim_pool_destroy", "claim_offload", "claim_restore",
-           "claim_check", "claim_check_static", "claim_lookup", "claim_identity_stats", "outcomes_read",
-           "claim_timing_read", "claim_block_state_read", "claim_strerror")
+           "claim_staging_reset", "claim_check", "claim_check_static", "claim_lookup",
+           "claim_identity_stats", "outcomes_read", "claim_timing_read", "claim_block_state_read",
+           "claim_strerror")
 
 
 class PoolDesc(ctypes.Structure):
@@ -123,6 +124,7 @@ def lib() -> ctypes.CDLL:
             "claim_pool_destroy": ([vp], i32),
             "claim_offload": ([vp, ctypes.POINTER(CBatch), vp, u64], i32),
             "claim_restore": ([vp, ctypes.POINTER(CBatch), vp, u64, ctypes.POINTER(CFaults)], i32),
+            "claim_staging_reset": ([vp], i32),
             "claim_check": ([vp, ctypes.POINTER(CBatch)], i32),
             "claim_check_static": ([vp, ctypes.POINTER(CBatch), vp, u32], i32),
             "claim_lookup": ([vp, ctypes.POINTER(CBatch), vp, u32], i32),
@@ -287,6 +289,11 @@ class Pool:
                                    ctypes.byref(fs) if fs is not None else None), "claim_restore")
         del keep  # host fault lists: read before claim_restore returns
         self._inflight += [batch, staging]
+
+    def staging_reset(self) -> None:
+        """claim_staging_reset: the next staged offload starts a new
+        staging generation."""
+        _check(lib().claim_staging_reset(self._h), "claim_staging_reset")
 
     def check(self, batch: DeviceBatch) -> None:
         _check(lib().claim_check(self._h, ctypes.byref(batch.struct)), "claim_check")

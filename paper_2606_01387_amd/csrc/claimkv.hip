@@ -801,7 +801,8 @@ __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restric
                                                        const Counters* __restrict__ ctr,
                                                        const uint64_t* __restrict__ partial,
                                                        uint32_t pgs, uint32_t groups, int mode,
-                                                       int staged, uint64_t* __restrict__ d_off,
+                                                       int staged, uint32_t slot0,
+                                                       uint64_t* __restrict__ d_off,
                                                        uint8_t* __restrict__ valid_off,
                                                        uint32_t* __restrict__ slot_of,
                                                        BlockRes* __restrict__ bres) {
@@ -833,7 +834,7 @@ __global__ void __launch_bounds__(kThreads) k_finalize(const uint32_t* __restric
     if (mode == 0) {
       d_off[b] = sum;
       valid_off[b] = 1;
-      slot_of[b] = staged ? u : kNone;
+      slot_of[b] = staged ? slot0 + u : kNone;
     } else {
       bres[b].d_res = sum;
     }
@@ -1943,7 +1944,10 @@ struct claim_pool {
   IdEntry* id_table = nullptr;
   IdSrc* id_src = nullptr;  // parallel to id_table
   uint64_t id_mask = 0;
-  uint64_t staged_blocks = 0;  // blocks written by the last staged offload
+  // staging of the current generation: the buffer staged offloads append
+  // to, and the slots written to it so far
+  const void* stage_base = nullptr;
+  uint64_t stage_used = 0;
   uint64_t reg_used_ub = 0;  // upper bound on registered claims
 
   claim_event* log = nullptr;
@@ -2206,10 +2210,10 @@ int launch_digest(claim_pool* P, DigestGrid gr, uint64_t* partial, void* staging
   }
 }
 
-int launch_finalize(claim_pool* P, DigestGrid gr, int mode, int staged) {
+int launch_finalize(claim_pool* P, DigestGrid gr, int mode, int staged, uint32_t slot0 = 0) {
   const uint32_t grid = grid_for((uint64_t)P->nb + gr.groups);  // slots <= U + groups
   hipLaunchKernelGGL(k_finalize, dim3(grid), dim3(kThreads), 0, P->stream, P->uniq, P->ctr,
-                     P->partial, P->pgs, gr.groups, mode, staged, P->d_off, P->valid_off,
+                     P->partial, P->pgs, gr.groups, mode, staged, slot0, P->d_off, P->valid_off,
                      P->slot_of, P->bres);
   return hip_status(hipGetLastError());
 }
@@ -2578,7 +2582,12 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
   TRY(read_counters(P));
   if (P->host_ctr->dup_flag & kFlagDupId) return CLAIM_EDUP;
   const uint64_t U = P->host_ctr->uniq_count;
-  if (staging && staging_bytes < U * P->block_bytes) return CLAIM_ENOSPC;  // nothing changed
+  // staging into the current generation's buffer appends after its slots;
+  // any other buffer starts a new generation
+  const bool append = staging && staging == P->stage_base;
+  const uint64_t slot0 = append ? P->stage_used : 0;
+  if (staging && (staging_bytes / P->block_bytes < slot0 + U || slot0 + U >= kNone))
+    return CLAIM_ENOSPC;  // nothing changed
   // footprint and identity storage: the rows' own offsets when they are
   // disjoint (no row runs backwards), else a run per claim
   const uint64_t* fpo = nullptr;
@@ -2598,10 +2607,11 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
   // offload replaces every earlier staging slot); acceptance then copies
   // each claim's digests into its own offload record
   P->gen += 1;
-  if (staging) TRY(fill<uint32_t>(P, P->slot_of, P->nb, kNone));
+  if (staging && !append) TRY(fill<uint32_t>(P, P->slot_of, P->nb, kNone));
   const DigestGrid gr = digest_grid(P, b->num_refs);
-  TRY(launch_digest(P, gr, P->partial, staging));
-  TRY(launch_finalize(P, gr, 0, staging != nullptr));
+  uint8_t* stage_at = staging ? (uint8_t*)staging + slot0 * P->block_bytes : nullptr;
+  TRY(launch_digest(P, gr, P->partial, stage_at));
+  TRY(launch_finalize(P, gr, 0, staging != nullptr, (uint32_t)slot0));
   if (C) {
     LAUNCH_GROUPED(k_accept, P, b, bd, rd, id_dev(P), P->nb, P->bs, P->seed, P->fp_used, fpo,
                    P->d_off, P->fp_store, P->ctr, P->cnt, P->pend);
@@ -2617,7 +2627,10 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
   }
   TRY(read_counters(P));
   P->fp_used += fp_need;
-  if (staging) P->staged_blocks = U;
+  if (staging) {
+    P->stage_base = staging;
+    P->stage_used = slot0 + U;
+  }
   P->reg_used_ub = P->host_ctr->reg_count;
   P->log_ub = P->host_ctr->log_count;
   return CLAIM_OK;
@@ -2626,7 +2639,7 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
 int claim_restore(claim_pool* P, const claim_batch* b, const void* staging,
                   uint64_t staging_bytes, const claim_fault_spec* f) {
   if (!P || ((uintptr_t)staging & 15)) return CLAIM_EINVAL;
-  if (staging && staging_bytes < P->staged_blocks * P->block_bytes) return CLAIM_EINVAL;
+  if (staging && staging_bytes / P->block_bytes < P->stage_used) return CLAIM_EINVAL;
   TRY(check_batch(P, b));
   HIP_TRY(hipSetDevice(P->device));
   const uint64_t C = b->num_claims;
@@ -2842,6 +2855,15 @@ int claim_block_state_read(claim_pool* P, uint32_t first, uint32_t count, uint64
     delete[] rec;
     HIP_TRY(e);
   }
+  return CLAIM_OK;
+}
+
+int claim_staging_reset(claim_pool* P) {
+  if (!P) return CLAIM_EINVAL;
+  HIP_TRY(hipSetDevice(P->device));
+  TRY(fill<uint32_t>(P, P->slot_of, P->nb, kNone));  // queued: ordered with earlier restores
+  P->stage_base = nullptr;
+  P->stage_used = 0;
   return CLAIM_OK;
 }
 

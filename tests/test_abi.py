@@ -130,6 +130,7 @@ def test_null_arguments_are_rejected(L):
     b = ck.CBatch()
     assert L.claim_offload(None, ctypes.byref(b), None, 0) == ck.EINVAL
     assert L.claim_restore(None, ctypes.byref(b), None, 0, None) == ck.EINVAL
+    assert L.claim_staging_reset(None) == ck.EINVAL
     assert L.claim_check(None, ctypes.byref(b)) == ck.EINVAL
     assert L.claim_check_static(None, ctypes.byref(b), None, 0) == ck.EINVAL
     assert L.outcomes_read(None, None, 0, None, None, 0, None) == ck.EINVAL

@@ -771,10 +771,11 @@ def test_staged_round_trip(torch, ck, w, where):
 
 @pytest.mark.parametrize("where", ["device", "pinned-host"])
 def test_two_staged_offloads(torch, ck, where):
-    """Staging holds one generation (the header's capability limit): after
-    two staged offloads only the second's blocks can be copied back.  Batch A
-    (claims over blocks 0..23) is offloaded with staging, then batch B
-    (claims over blocks 16..39) with a second staging buffer; every staged
+    """A staged offload into another staging buffer starts a new generation:
+    after two staged offloads into two buffers only the second's blocks can
+    be copied back.  Batch A (claims over blocks 0..23) is offloaded with
+    staging, then batch B (claims over blocks 16..39) with a second staging
+    buffer; every staged
     block's device copy is then lost (zeroed).  A restore of A and B from
     B's staging copies back blocks 16..39 only: B's claims and A's claims
     inside 16..23 are materialized, A's claims touching 0..15 fail closed on
@@ -847,6 +848,110 @@ def test_two_staged_offloads(torch, ck, where):
 
 
 # ----------------------------------------------------------- full-size workloads
+
+
+@pytest.mark.parametrize("case", ["append", "too-small", "reset", "unstaged-between"])
+@pytest.mark.parametrize("where", ["device", "pinned-host"])
+def test_staging_buffer_accumulates(torch, ck, where, case):
+    """Staged offloads into one staging buffer accumulate (section 7 paths A
+    and B: the offload tier holds the blocks of every staged offload).
+    Batch A (claims over blocks 0..23) is staged, then batch B (blocks
+    16..39) into the same buffer; every staged block's device copy is then
+    lost (zeroed), and A and B are restored from the buffer.
+      append:           every block comes back; every claim is materialized.
+      too-small:        the buffer lacks one block for B: B's offload is
+                        refused with ENOSPC and changes nothing; A still
+                        comes back whole.
+      reset:            claim_staging_reset between the offloads: B starts a
+                        new generation at the start of the buffer, so the
+                        blocks only A staged are lost and A's claims on them
+                        fail closed.
+      unstaged-between: an offload of blocks 0..7 without staging between A
+                        and B drops their staged copies, so they are lost.
+    GPU against the oracle, with the pool bytes after the restore against
+    the host model."""
+    note(f"staging buffer accumulates: {case} via {where}")
+    w = TINY
+    g = w.geometry
+    rng = np.random.default_rng(43)
+
+    def rows(first_id, lo, hi, n):
+        out = []
+        for k in range(n):
+            m = int(rng.integers(1, 4))
+            out.append((first_id + k, [int(x) for x in rng.integers(lo, hi, size=m)],
+                        rng.integers(0, 32000, size=m * g.block_size, dtype=np.uint32)))
+        return out
+
+    a_rows = rows(0xA000, 0, 24, 12) + [(0xAF00, [0, 8, 23], rng.integers(0, 32000, size=48,
+                                                                          dtype=np.uint32))]
+    b_rows = rows(0xB000, 16, 40, 12)
+    c_rows = [(0xC000, list(range(0, 8)), rng.integers(0, 32000, size=8 * g.block_size,
+                                                        dtype=np.uint32))]
+    a, b, c = from_claims(a_rows), from_claims(b_rows), from_claims(c_rows)
+    ua, ub = a.unique_blocks(g.num_blocks), b.unique_blocks(g.num_blocks)
+    slots = ua.size + ub.size - (1 if case == "too-small" else 0)
+    if where == "device":
+        arena = torch.empty(slots * g.block_bytes, dtype=torch.uint8, device="cuda")
+    else:
+        arena = torch.empty(slots * g.block_bytes, dtype=torch.uint8, pin_memory=True)
+    host = content.pool_host(g, w.content_seed)
+    kv = gpu_pool_tensor(torch, w)
+    op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
+    staged_a = ck.DeviceBatch(a)
+    with ck.Pool(g, w.seed, kv, max_claims=128, max_footprint=1024, event_capacity=1024) as pool:
+        pool.offload(staged_a, staging=arena)
+        assert op.offload(a, digests(host, w)) == O.OK
+        if case == "reset":
+            pool.staging_reset()
+        if case == "unstaged-between":
+            pool.offload(ck.DeviceBatch(c))
+            assert op.offload(c, digests(host, w)) == O.OK
+        offloaded = [a] + ([c] if case == "unstaged-between" else [])
+        if case == "too-small":
+            with pytest.raises(ck.ClaimError) as e:
+                pool.offload(ck.DeviceBatch(b), staging=arena)
+            assert e.value.status == ck.ENOSPC
+        else:
+            pool.offload(ck.DeviceBatch(b), staging=arena)
+            assert op.offload(b, digests(host, w)) == O.OK
+            offloaded.append(b)
+        pool.stream.synchronize()
+        lost = np.union1d(ua, ub)
+        idx = torch.as_tensor(lost.astype(np.int64), device="cuda")
+        kv.view(g.planes, g.num_blocks, g.chunk_bytes)[:, idx, :] = 0
+        torch.cuda.synchronize()
+        every = from_claims(a_rows + (c_rows if case == "unstaged-between" else [])
+                            + (b_rows if case != "too-small" else []))
+        db = ck.DeviceBatch(every)
+        pool.restore(db, staging=arena)
+        pool.read()
+        pool.check(db)
+        out, ev = pool.read()
+    # blocks without a staged copy stay zero
+    if case == "append":
+        gone = np.zeros(0, np.int64)
+    elif case == "too-small":
+        gone = np.setdiff1d(ub, ua)  # B was refused: only A's blocks were staged
+    elif case == "reset":
+        gone = np.setdiff1d(ua, ub)
+    else:  # A's blocks among C's, whose staged copies C dropped (B stages none of them)
+        gone = np.setdiff1d(np.intersect1d(ua, np.arange(8)), ub)
+    model = host.copy()
+    model.reshape(g.planes, g.num_blocks, g.chunk_bytes)[:, gone, :] = 0
+    assert np.array_equal(kv.cpu().numpy(), model)
+    assert op.restore(every) == O.OK
+    op.events(clear=True)
+    same_outcomes(out, op.check(every, digests(model, w)))
+    same_events(ev, op.events())
+    codes = out["code"]
+    if case in ("append", "too-small"):
+        assert (codes[: len(a_rows)] == ck.MATERIALIZED).all()
+    else:
+        assert (codes == ck.RESTORE_FAILED_FAIL_CLOSED).any()
+        assert (codes == ck.MATERIALIZED).any()
+    del kv, arena
+    free_gpu(torch)
 
 
 @pytest.mark.parametrize("name", ["llama3-8b", "llama3-70b", "small-claim-stress", "mla-fp8",
