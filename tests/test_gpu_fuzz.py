@@ -1,14 +1,16 @@
-"""Differential test of the library against the oracle over seeded
-irregular lifecycles (tests/fuzz_cases.py): five pool geometries (one a head
-shard, one whose digest runs in two phases), offload batches with empty, long, missing, out-of-range, malformed
-and entry-sharing rows, reserved ids and predicates, shared and
-duplicate-owned identities, faults, a partial restore (in a third of the
-cases from device staging written by the second offload, after the staged
-blocks' device copies are zeroed), a check batch that presents the claims
-again reordered, repeated and changed, and lookups; between the two
+"""Differential test of the library against the oracle over seeded irregular
+lifecycles (tests/fuzz_cases.py): five pool geometries (one a head shard, one
+whose digest runs in two phases), offload batches with empty, long, missing,
+out-of-range, malformed and entry-sharing rows, reserved ids and predicates,
+shared and duplicate-owned identities, faults, a partial restore (in a third
+of the cases from device staging, after the staged blocks' device copies are
+zeroed: staging written by the second offload into a new buffer, or by both
+offloads into one buffer, which accumulates and so keeps the first offload's
+bytes of blocks the second does not restage), a check batch that presents the
+claims again reordered, repeated and changed, and lookups; between the two
 offloads a restore of first-batch claims reports load failures and flips
 bytes of their blocks, which the second batch re-offloads under another
-claim.  The pool's bytes after the restore must equal the host model, and
+claim. The pool's bytes after the restore must equal the host model, and
 every status, outcome field, event, per-block digest, lookup field and
 identity count the oracle's."""
 
@@ -51,36 +53,61 @@ def test_fuzz_lifecycle(torch, ck, seed):
     host = content.pool_host(g, w.content_seed)
     op = O.OraclePool(g.num_blocks, g.block_size, w.seed)
     kv = gpu_pool_tensor(torch, w)
-    staging, restored = None, host.copy()
+    # staged cases alternate: the second offload stages into a new buffer,
+    # or both offloads stage into one buffer, which accumulates
+    accumulate = case.staged and (seed // 3) % 2 == 1
+    staging = None
+    if accumulate:
+        slots = sum(well_formed_blocks(b, g.num_blocks).size for b in case.offload)
+        staging = torch.empty(max(1, slots) * g.block_bytes, dtype=torch.uint8, device="cuda")
+    snap = {}  # block -> its bytes at its latest staged offload (its staged copy)
     print(f"  mid restore {case.mid.num_claims} claims, {case.mid_faults.flip_blocks.size} flips, "
-          f"{case.mid_faults.load_failed.size} load failures", flush=True)
+          f"{case.mid_faults.load_failed.size} load failures{', one staging buffer' if accumulate else ''}",
+          flush=True)
     with ck.Pool(g, w.seed, kv, **capacities(case)) as pool:
         for i, b in enumerate(case.offload):
             if i == 1:  # the restore between the offloads: failures, changed bytes
                 pool.restore(ck.DeviceBatch(case.mid), faults=case.mid_faults)
                 assert op.restore(case.mid, case.mid_faults.load_failed) == O.OK
                 host = apply_flips(host, w, case.mid_faults)
-                restored = host.copy()
             want = op.offload(b, digests(host, w))
-            if case.staged and i == len(case.offload) - 1:
-                staged = well_formed_blocks(b, g.num_blocks)
-                staging = torch.empty(max(1, staged.size) * g.block_bytes, dtype=torch.uint8,
+            blocks = well_formed_blocks(b, g.num_blocks)
+            use = None
+            if accumulate:
+                use = staging
+            elif case.staged and i == len(case.offload) - 1:
+                staging = torch.empty(max(1, blocks.size) * g.block_bytes, dtype=torch.uint8,
                                       device="cuda")
+                use = staging
             try:
-                pool.offload(ck.DeviceBatch(b), staging=staging)
+                pool.offload(ck.DeviceBatch(b), staging=use)
                 got = ck.OK
             except ck.ClaimError as e:
                 got = e.status
             assert got == want
+            if got == ck.OK:
+                if use is not None and not accumulate:
+                    snap = {}  # a new buffer: a new staging generation
+                host3 = host.reshape(g.planes, g.num_blocks, g.chunk_bytes)
+                for blk in blocks.tolist():
+                    if use is not None:
+                        snap[blk] = host3[:, blk, :].copy()
+                    else:
+                        snap.pop(blk, None)  # an unstaged offload drops the staged copy
+        restored = host.copy()
         if case.staged:
             # the staged blocks' device copies are gone; the restore copies
-            # back those its well-formed rows reference
+            # back, from their staged copies, those its well-formed rows
+            # reference
+            staged = np.array(sorted(snap), dtype=np.int64)
             pool.stream.synchronize()
-            idx = torch.as_tensor(staged.astype(np.int64), device="cuda")
+            idx = torch.as_tensor(staged, device="cuda")
             kv.view(g.planes, g.num_blocks, g.chunk_bytes)[:, idx, :] = 0
             torch.cuda.synchronize()
-            lost = np.setdiff1d(staged, well_formed_blocks(case.restore, g.num_blocks))
-            restored.reshape(g.planes, g.num_blocks, g.chunk_bytes)[:, lost, :] = 0
+            r3 = restored.reshape(g.planes, g.num_blocks, g.chunk_bytes)
+            r3[:, staged, :] = 0
+            for blk in np.intersect1d(staged, well_formed_blocks(case.restore, g.num_blocks)).tolist():
+                r3[:, blk, :] = snap[blk]
         pool.restore(ck.DeviceBatch(case.restore), staging=staging, faults=case.faults)
         assert op.restore(case.restore, case.faults.load_failed) == O.OK
         restored = apply_flips(restored, w, case.faults)
