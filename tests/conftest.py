@@ -34,3 +34,22 @@ def _host_libs():
 
         subprocess.run(["gcc", "-O2", "-std=c99", "-shared", "-fPIC", content.HOST_SRC,
                         "-o", content.HOST_LIB], check=True)
+
+
+@pytest.fixture(scope="session")
+def torch():
+    """torch, on a machine with a GPU (the GPU tests' fixture)."""
+    import torch as t
+
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    return t
+
+
+@pytest.fixture(scope="session")
+def ck():
+    """The library's binding, with the library loaded (it fails loudly when
+    the library has not been built: there is no fallback)."""
+    from paper_2606_01387_amd import claimkv
+
+    claimkv.lib()
+    return claimkv

@@ -26,22 +26,6 @@ from tests.test_gpu_parity import free_gpu
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(scope="module")
-def torch():
-    import torch as t
-
-    assert t.cuda.is_available()
-    return t
-
-
-@pytest.fixture(scope="module")
-def ck():
-    from paper_2606_01387_amd import claimkv
-
-    claimkv.lib()
-    return claimkv
-
-
 def seeded(seed):
     w = Workload(
         name=f"attribution-{seed}", geometry=Geometry(2, 2, 16, 2, 32, 2, 400), seed=9000 + seed,

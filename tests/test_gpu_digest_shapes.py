@@ -21,22 +21,6 @@ from tests.test_gpu_parity import free_gpu, gpu_pool_tensor
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(scope="module")
-def torch():
-    import torch as t
-
-    assert t.cuda.is_available(), "GPU tests need a GPU"
-    return t
-
-
-@pytest.fixture(scope="module")
-def ck():
-    from paper_2606_01387_amd import claimkv
-
-    claimkv.lib()
-    return claimkv
-
-
 def random_geometry(rng) -> Geometry:
     while True:
         layers, ppl = int(rng.integers(1, 7)), int(rng.choice([1, 2]))

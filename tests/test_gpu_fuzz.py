@@ -26,22 +26,6 @@ from tests.test_gpu_parity import free_gpu, gpu_pool_tensor, same_events, same_o
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(scope="module")
-def torch():
-    import torch as t
-
-    assert t.cuda.is_available(), "GPU tests need a GPU"
-    return t
-
-
-@pytest.fixture(scope="module")
-def ck():
-    from paper_2606_01387_amd import claimkv
-
-    claimkv.lib()
-    return claimkv
-
-
 @pytest.mark.parametrize("seed", SEEDS)
 def test_fuzz_lifecycle(torch, ck, seed):
     case = make_case(seed)

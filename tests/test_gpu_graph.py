@@ -22,22 +22,6 @@ CAPTURE_RELAXED = 2  # hipStreamCaptureModeRelaxed
 
 
 @pytest.fixture(scope="module")
-def torch():
-    import torch as t
-
-    assert t.cuda.is_available(), "GPU tests need a GPU"
-    return t
-
-
-@pytest.fixture(scope="module")
-def ck():
-    from paper_2606_01387_amd import claimkv
-
-    claimkv.lib()
-    return claimkv
-
-
-@pytest.fixture(scope="module")
 def hip():
     h = ctypes.CDLL("libamdhip64.so")
     vp = ctypes.c_void_p

@@ -23,22 +23,6 @@ pytestmark = pytest.mark.gpu
 LK_FIELDS = [n for n in O.LOOKUP_DTYPE.names if n != "pad"]
 
 
-@pytest.fixture(scope="module")
-def torch():
-    import torch as t
-
-    assert t.cuda.is_available(), "GPU tests need a GPU"
-    return t
-
-
-@pytest.fixture(scope="module")
-def ck():
-    from paper_2606_01387_amd import claimkv
-
-    claimkv.lib()
-    return claimkv
-
-
 def same_lookups(got, want):
     assert len(got) == len(want)
     for f in LK_FIELDS:

@@ -34,22 +34,6 @@ OUT_FIELDS = [n for n in O.OUTCOME_DTYPE.names if n != "pad"]
 EV_FIELDS = [n for n in O.EVENT_DTYPE.names if n != "pad"]
 
 
-@pytest.fixture(scope="module")
-def torch():
-    import torch as t
-
-    assert t.cuda.is_available(), "GPU tests need a GPU"
-    return t
-
-
-@pytest.fixture(scope="module")
-def ck():
-    from paper_2606_01387_amd import claimkv
-
-    claimkv.lib()
-    return claimkv
-
-
 def note(msg):
     print(msg, flush=True)
     sys.stdout.flush()

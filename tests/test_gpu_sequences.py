@@ -25,22 +25,6 @@ from tests.test_gpu_parity import free_gpu, gpu_pool_tensor, same_events, same_o
 pytestmark = pytest.mark.gpu
 
 
-@pytest.fixture(scope="module")
-def torch():
-    import torch as t
-
-    assert t.cuda.is_available(), "GPU tests need a GPU"
-    return t
-
-
-@pytest.fixture(scope="module")
-def ck():
-    from paper_2606_01387_amd import claimkv
-
-    claimkv.lib()
-    return claimkv
-
-
 @pytest.mark.parametrize("seed", SEQUENCE_SEEDS)
 def test_lifecycle_sequence(torch, ck, seed):
     seq = make_sequence(seed)

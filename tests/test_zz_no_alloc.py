@@ -18,22 +18,6 @@ pytestmark = pytest.mark.gpu
 EV_FIELDS = ("claim_id", "aux", "kind", "block_index", "phys_block")
 
 
-@pytest.fixture(scope="module")
-def torch():
-    import torch as t
-
-    assert t.cuda.is_available(), "GPU tests need a GPU"
-    return t
-
-
-@pytest.fixture(scope="module")
-def ck():
-    from paper_2606_01387_amd import claimkv
-
-    claimkv.lib()
-    return claimkv
-
-
 def test_check_static_matches_check(torch, ck):
     # 20000 claims (the tiled event scan), then 3000 of them (one workgroup)
     w = scaled(FULL["small-claim-stress"], 256, 20000, corrupt_rate=0.05, num_load_failed=3)
