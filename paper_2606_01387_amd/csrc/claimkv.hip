@@ -792,7 +792,9 @@ __global__ void __launch_bounds__(kThreads) k_digest(const u32x2* __restrict__ p
 
 // Add each unique block's piece-group partials.
 //   mode 0 (offload): d_off (the latest offload's digest), valid_off = 1
-//                     (some claim records the block), slot_of
+//                     (some claim records the block), slot_of: the
+//                     block's staging slot slot0 + u when staged, else none
+//                     (an unstaged offload drops the block's staged copy)
 //   mode 1 (check):   the restored digest in the block's record; every
 //                     block whose record a check's claims compare is one
 //                     of its unique blocks, so the claim stage reads only
@@ -2603,9 +2605,10 @@ int claim_offload(claim_pool* P, const claim_batch* b, void* staging, uint64_t s
   }
   if (P->fp_used + fp_need > P->max_fp) return CLAIM_ENOSPC;  // nothing changed
 
-  // the offload digest of every block the batch references (a staged
-  // offload replaces every earlier staging slot); acceptance then copies
-  // each claim's digests into its own offload record
+  // the offload digest of every block the batch references (staged from
+  // slot slot0 of the current generation's buffer; another buffer starts a
+  // new generation); acceptance then copies each claim's digests into its
+  // own offload record
   P->gen += 1;
   if (staging && !append) TRY(fill<uint32_t>(P, P->slot_of, P->nb, kNone));
   const DigestGrid gr = digest_grid(P, b->num_refs);
