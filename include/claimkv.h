@@ -30,7 +30,12 @@
  *                  host;
  *   claim_lookup   the reuse lookup: how many leading token blocks of each
  *                  request hit the identities that offloads registered;
- *   claim_identity_stats  registered and ambiguous identities.
+ *   claim_identity_stats  registered and ambiguous identities;
+ *   claim_staging_reset   start a new generation of the staged bytes (the
+ *                  offload tier), which staged offloads into one buffer
+ *                  otherwise accumulate;
+ *   claim_check_static    claim_check without any allocation, for callers
+ *                  that cannot allocate (graph capture, serving loops).
  *
  * The digest, keys and chain are this library's definitions (the paper
  * leaves the byte-level check open; section 7 path B only requires
