@@ -4,14 +4,14 @@
 bytes changed, registering other prefixes in them; predicates), restores
 of random subsets with reported failures and bit flips, some undoing
 earlier flips (recomputes), checks of random subsets presented as accepted
-or changed, and lookups.  In half of the sequences the offloads stage
-into one staging buffer, which accumulates (some offloads unstaged, which
-drops their blocks' staged copies, and an occasional staging reset), and
-some restores first lose the device copies of staged blocks and copy them
-back from their latest staged bytes.  After every step the pool bytes
-equal the host model; every check's outcomes and events, every lookup and
-the identity counts, and at the end the per-block state, equal the
-oracle's."""
+or changed, and lookups. In half of the sequences the offloads stage into
+one staging buffer (device or page-locked host memory), which accumulates
+(some offloads unstaged, which drops their blocks' staged copies, and an
+occasional staging reset), and some restores first lose the device copies
+of staged blocks and copy them back from their latest staged bytes. After
+every step the pool bytes equal the host model; every check's outcomes and
+events, every lookup and the identity counts, and at the end the per-block
+state, equal the oracle's."""
 
 import numpy as np
 import pytest
@@ -39,7 +39,10 @@ def test_lifecycle_sequence(torch, ck, seed):
     if rng.random() < 0.5:  # one staging buffer for the whole sequence
         slots = sum(well_formed_blocks(st.batch, g.num_blocks).size
                     for st in seq.steps if st.kind == "offload")
-        arena = torch.empty(max(1, slots) * g.block_bytes, dtype=torch.uint8, device="cuda")
+        if rng.random() < 0.5:
+            arena = torch.empty(max(1, slots) * g.block_bytes, dtype=torch.uint8, device="cuda")
+        else:  # page-locked host memory, which the kernels write and read over the link
+            arena = torch.empty(max(1, slots) * g.block_bytes, dtype=torch.uint8, pin_memory=True)
     snap = {}  # block -> its bytes at its latest staged offload
     with ck.Pool(g, w.seed, kv, max_claims=4 * seq.claims + 64, max_footprint=4 * seq.refs + 64,
                  event_capacity=64 * seq.claims + 1024) as pool:
