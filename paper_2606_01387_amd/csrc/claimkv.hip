@@ -11,11 +11,11 @@
 //  * Block digest (the HBM-bound stage).  The pool is plane-major
 //    [plane][block][chunk].  D(b) = sum_i w_i k_i is linear in the words, so
 //    it splits into partial sums over pieces of the canonical block: a piece
-//    is one 64-lane x LPW 8-byte-word segment of a plane's chunk (LPW up
-//    to 32: 16 KiB), and since k_i depends only on the word's canonical
-//    position, a wave pinned to one piece keeps that piece's keys in VGPRs
-//    and streams the same piece of many blocks, with all LPW loads in flight
-//    before any use.  The 4 waves of a workgroup take 4 consecutive pieces
+//    is one 64-lane x LPW 8-byte-word segment of a plane's chunk (LPW up to
+//    24 for whole chunks, 12 KiB; 32 for ragged ones), and since k_i depends
+//    only on the word's canonical position, a wave pinned to one piece keeps
+//    that piece's keys in VGPRs and streams the same piece of many blocks,
+//    with all LPW loads in flight before any use.  The 4 waves of a workgroup take 4 consecutive pieces
 //    of the same blocks and park their per-block sums in an LDS ring, which
 //    the workgroup adds and writes as one contiguous run of partials; the
 //    grid is exactly one resident round, and on the largest pools it reads
@@ -2282,11 +2282,18 @@ int append_events(claim_pool* P, const claim_batch* b, ClaimScratch sc) {
   } while (0)
 
 // Choose words per lane (LPW), segments per chunk and the digest grid.
-// LPW is the largest instantiated width (32, 24, 16, 12, 8, ...) that
-// divides the chunk's words-per-lane, so every segment is full and each wave
-// streams up to 16 KiB per block; chunks that are not a whole number of
-// 512-byte rows, or whose only exact widths are tiny, use the smallest width
-// covering the chunk (at most 32) with a ragged last segment.  The grid is
+// LPW is the largest instantiated width of at most kMaxExactLpw words (24,
+// 16, 12, 8, ...) that divides the chunk's words-per-lane, so every segment
+// is full and each wave streams up to 12 KiB per block; chunks that are not
+// a whole number of 512-byte rows, or whose only exact widths are tiny, use
+// the smallest width covering the chunk (at most 32) with a ragged last
+// segment.  Measured on MI355X in one process over one allocation, two
+// repetitions each: 16 words (8 KiB pieces, 32 KiB in flight per CU)
+// instead of 32 (16 KiB pieces, 64 KiB) read the 8B pool 2.0 % faster
+// (7.32 TB/s), the stress pool 2.6 %, 64 KiB chunks 1.8 %, fp8 and 64-plane
+// 16 KiB pools 1.6-1.7 %, a 160-plane pool 0.8 %; the 70B pool 0.4 % and a
+// 128-plane 16 KiB pool 2.3 % slower.  The 36 KiB MLA chunk keeps 24 words
+// (12 words, 24 KiB in flight, read it 14 % slower).  The grid is
 // persistent and fully resident (no tail of late waves): slots = workgroups
 // per CU x CUs, shared by the piece groups read at a time (digest_grid).
 // Workgroups per CU: enough for about
@@ -2298,6 +2305,7 @@ int append_events(claim_pool* P, const claim_batch* b, ClaimScratch sc) {
 // 2.026 (2 per CU there), 70B unchanged (15.40 -> 15.43); more requests
 // outstanding than the memory needs only queue.
 constexpr int kInflightPerCu = 32 << 10;
+constexpr int kMaxExactLpw = 24;
 
 int choose_digest_shape(claim_pool* P) {
   static const int kLpw[] = {32, 24, 16, 12, 8, 4, 2, 1};  // instantiated widths, descending
@@ -2306,7 +2314,7 @@ int choose_digest_shape(claim_pool* P) {
   int best = 0;
   if (CW % 64 == 0)
     for (int d : kLpw)
-      if (Q % d == 0) {
+      if (d <= kMaxExactLpw && Q % d == 0) {
         best = d;
         break;
       }
@@ -2350,7 +2358,8 @@ int choose_digest_shape(claim_pool* P) {
 // covering at most kPhaseBytes.  Independently, a launch whose
 // one-phase grid would leave more than 15 % of the slots idle (many piece
 // groups, few slots each) reads in phases that fill it (320 planes: 6.05 ->
-// 7.2 TB/s).  refs bounds the launch's unique blocks.
+// 7.2 TB/s).  A phase never has more piece groups than there are slots, so
+// the grid stays one resident round.  refs bounds the launch's unique blocks.
 constexpr uint64_t kOnePhaseBytes = 32ull << 30;
 constexpr uint64_t kPhaseBytes = 4ull << 30;
 constexpr uint32_t kMinFillPct = 85;
@@ -2361,7 +2370,7 @@ DigestGrid digest_grid(const claim_pool* P, uint64_t refs) {
   DigestGrid best{1, 1};
   uint64_t best_fill = 0;
   for (uint32_t d = P->pgs; d >= 1; --d) {
-    if (P->pgs % d) continue;
+    if (P->pgs % d || d > P->slots) continue;  // a phase must fit the resident slots
     const bool one = bytes <= (long double)kOnePhaseBytes;
     if (d > 1 && !one && bytes * d > (long double)kPhaseBytes * P->pgs) continue;
     const uint64_t groups = std::min<uint64_t>(std::max<uint32_t>(1u, P->slots / d), ub);
