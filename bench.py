@@ -283,6 +283,7 @@ def main() -> int:
                              "claim_restore (faults, RESTORE_REQUIRED) on the device-resident pool, "
                              "wall time of one call each, including the offload's host waits"}
     pool.read(max_outcomes=1)
+    grid = pool.digest_grid(batch.num_refs)
 
     for _ in range(warm):
         pool.check(db)
@@ -401,6 +402,14 @@ def main() -> int:
             "avg_launch_ms": round(digest_ms, 4),
             "measured_read_ceiling": round(read_ceiling, 1),
             "frac_of_read_ceiling": round(achieved / read_ceiling, 4),
+            "digest_grid": {
+                "words_per_lane": grid["words_per_lane"],
+                "piece_groups": grid["piece_groups"],
+                "piece_groups_at_a_time": grid["pga"],
+                "workgroups_each": grid["groups"],
+                "phases": grid["piece_groups"] // grid["pga"],
+                "workgroups": grid["pga"] * grid["groups"],
+            },
         },
     }
     line["lookup"] = {

@@ -35,7 +35,8 @@
  *                  offload tier), which staged offloads into one buffer
  *                  otherwise accumulate;
  *   claim_check_static    claim_check without any allocation, for callers
- *                  that cannot allocate (graph capture, serving loops).
+ *                  that cannot allocate (graph capture, serving loops);
+ *   claim_digest_grid     the digest grid a launch takes.
  *
  * The digest, keys and chain are this library's definitions (the paper
  * leaves the byte-level check open; section 7 path B only requires
@@ -335,7 +336,8 @@ int claim_pool_destroy(claim_pool* pool);
  * for the stream to read the acceptance verdict (three times when a block
  * row runs backwards).  ENOSPC if the registry, footprint store or event
  * log could overflow; the footprint store takes num_refs entries, or, when
- * rows share entries, the sum of the well-formed rows' lengths. */
+ * rows share entries, the sum of the well-formed rows' lengths.
+ */
 int claim_offload(claim_pool* pool, const claim_batch* batch, void* staging,
                   uint64_t staging_bytes);
 
@@ -448,6 +450,27 @@ int claim_identity_stats(claim_pool* pool, uint64_t* entries, uint64_t* ambiguou
  * reads the events, and returns ENOSPC. */
 int outcomes_read(claim_pool* pool, claim_outcome* out, uint32_t out_cap, uint32_t* num_out,
                   claim_event* events, uint64_t ev_cap, uint64_t* num_events);
+
+/* The digest grid of a pool.  A digest launch runs slots resident
+ * workgroups of 4 waves; each wave reads one piece (64 lanes x
+ * words_per_lane 8-byte words) of one plane's chunk of each block it
+ * visits, a workgroup 4 consecutive pieces (a piece group), and the launch
+ * reads pga piece groups at a time with groups workgroups on each. */
+typedef struct claim_grid_info {
+  uint32_t words_per_lane;  /* 8-byte words per lane in one piece */
+  uint32_t segments;        /* pieces per plane chunk */
+  uint32_t piece_groups;    /* ceil(planes x segments / 4) */
+  uint32_t slots;           /* workgroups resident at once (per CU x CUs) */
+  uint32_t pga;             /* a launch over `refs` entries: piece groups read at a time */
+  uint32_t groups;          /* ... and workgroups on each */
+} claim_grid_info;
+
+/* Report the digest grid (claim_grid_info) that a launch over a batch of
+ * `refs` block-table entries takes (the piece groups read at a time follow
+ * from an upper bound on the launch's unique blocks, min(refs,
+ * num_blocks)).  Does not wait or queue work.  EINVAL for a NULL pool or
+ * out. */
+int claim_digest_grid(const claim_pool* pool, uint64_t refs, claim_grid_info* out);
 
 /* Wait for the pool's stream and return the summed stage times of the
  * checks queued since the previous call (EINVAL unless the pool was created

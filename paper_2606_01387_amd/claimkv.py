@@ -53,7 +53,7 @@ LOOKUP_DTYPE = np.dtype(
 EXPORTS = ("claim_pool_create", "claim_pool_destroy", "claim_offload", "claim_restore",
            "claim_staging_reset", "claim_check", "claim_check_static", "claim_lookup",
            "claim_identity_stats", "outcomes_read", "claim_timing_read", "claim_block_state_read",
-           "claim_strerror")
+           "claim_digest_grid", "claim_strerror")
 
 
 class PoolDesc(ctypes.Structure):
@@ -87,6 +87,12 @@ class CTiming(ctypes.Structure):
                 ("total_ms", ctypes.c_double), ("digest_ms", ctypes.c_double),
                 ("select_ms", ctypes.c_double), ("finalize_ms", ctypes.c_double),
                 ("claims_ms", ctypes.c_double), ("events_ms", ctypes.c_double)]
+
+
+class CGridInfo(ctypes.Structure):
+    _fields_ = [("words_per_lane", ctypes.c_uint32), ("segments", ctypes.c_uint32),
+                ("piece_groups", ctypes.c_uint32), ("slots", ctypes.c_uint32),
+                ("pga", ctypes.c_uint32), ("groups", ctypes.c_uint32)]
 
 
 assert ctypes.sizeof(PoolDesc) == 96 and ctypes.sizeof(CBatch) == 72
@@ -132,6 +138,7 @@ def lib() -> ctypes.CDLL:
             "outcomes_read": ([vp, vp, u32, ctypes.POINTER(u32), vp, u64, ctypes.POINTER(u64)], i32),
             "claim_timing_read": ([vp, ctypes.POINTER(CTiming)], i32),
             "claim_block_state_read": ([vp, u32, u32, vp, vp, vp, vp], i32),
+            "claim_digest_grid": ([vp, u64, ctypes.POINTER(CGridInfo)], i32),
             "claim_strerror": ([i32], ctypes.c_char_p),
         }
         for name, (args, res) in sig.items():
@@ -385,6 +392,14 @@ class Pool:
                                             failed.ctypes.data), "claim_block_state_read")
         self._inflight = []  # waited for the stream
         return {"d_off": d_off, "d_res": d_res, "valid_off": valid, "load_failed": failed}
+
+    def digest_grid(self, refs: int | None = None) -> dict:
+        """The digest grid of a launch over ``refs`` block-table entries
+        (default: as many as the pool has blocks)."""
+        g = CGridInfo()
+        n = self.geometry.num_blocks if refs is None else refs
+        _check(lib().claim_digest_grid(self._h, n, ctypes.byref(g)), "claim_digest_grid")
+        return {name: getattr(g, name) for name, _ in CGridInfo._fields_}
 
     def timing(self) -> dict:
         t = CTiming()

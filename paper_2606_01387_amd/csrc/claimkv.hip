@@ -2342,26 +2342,36 @@ int choose_digest_shape(claim_pool* P) {
 // the piece-group count, so that every workgroup runs the same number of
 // phases) and how many workgroups share each (groups = slots / pga).
 //
-// Reading every piece group at once suits pools up to a few tens of GB, but
-// not the largest.  Measured on MI355X in one process over one allocation,
-// every block referenced once: with all piece groups at once, pools of 13 to
-// 30 GB read at 6.96-7.20 TB/s, while pools of 84 and 105 GB read at only
-// 6.77-6.84 TB/s.  The same 84 and 105 GB pools read in phases of 2.6-5.2 GB
-// reached 7.07-7.10 TB/s.  The loss is not address translation: the phased
-// launches take more translation misses (about 46 000 and 113 000 per launch
-// against 2 000 on the 105 GB pool).  What separates them is the number of
-// requests outstanding at the memory interface: about 6 000-6 240 on
-// average with phases against 5 500-5 660 without.  A phase costs a key
-// computation and a ring flush, which a pool with few blocks per workgroup
-// feels (a 21 GB pool of 4000 blocks read in 80 phases: -6 %), so phases
-// start only past kOnePhaseBytes of referenced blocks, each phase then
-// covering at most kPhaseBytes.  Independently, a launch whose
-// one-phase grid would leave more than 15 % of the slots idle (many piece
-// groups, few slots each) reads in phases that fill it (320 planes: 6.05 ->
-// 7.2 TB/s).  A phase never has more piece groups than there are slots, so
-// the grid stays one resident round.  refs bounds the launch's unique blocks.
+// Reading every piece group at once suits pools of up to about 13 GB;
+// from kTwoPhaseBytes to kOnePhaseBytes of referenced blocks a launch reads
+// in at least two phases, and past kOnePhaseBytes in phases of at most
+// kPhaseBytes.  Measured on MI355X with 8 KiB pieces, each comparison in one
+// process over one allocation, in several processes: two phases read the
+// 17 GB 8B pool 0.7-1.6 % faster than one (32 piece groups at a time
+// instead of 64; more phases were slower) and the 30 GB stress pool
+// 0.4-0.8 % faster (14 instead of 28), while the 13.5 GB MLA pool read
+// 1.4 % slower in two phases and the 13.1 GB 70B head shard no faster.
+// Over the 105 GB 70B pool (160 piece groups), 2 piece groups at a time
+// (phases of 1.3 GB) read 1.0-1.4 % faster than 5 (3.3 GB phases, the
+// bound of 4 GiB used before), and every other size from 1 to 80 was slower
+// than 2; an 84 GB pool read the same with 1 or 2 at a time.  With 16 KiB
+// pieces, all piece groups at once read the 84 and 105 GB pools at only
+// 6.77-6.84 TB/s against 7.07-7.10 in phases of 2.6-5.2 GB, while pools of
+// 13 to 30 GB read at 6.96-7.20 TB/s in one phase.  That loss is not address
+// translation (the phased launches took more translation misses: about
+// 46 000 and 113 000 per launch against 2 000); the phased launches kept
+// more requests outstanding at the memory interface (about 6 000-6 240 on
+// average against 5 500-5 660).  A phase costs a key computation and a ring
+// flush, which a pool with few blocks per workgroup feels (a 21 GB pool of
+// 4000 blocks read in 80 phases: -6 %), so short phases start only past
+// kOnePhaseBytes.  Independently, a launch whose one-phase grid would leave
+// more than 15 % of the slots idle (many piece groups, few slots each)
+// reads in phases that fill it (320 planes: 6.05 -> 7.2 TB/s).  A phase
+// never has more piece groups than there are slots, so the grid stays one
+// resident round.  refs bounds the launch's unique blocks.
+constexpr uint64_t kTwoPhaseBytes = 14ull << 30;
 constexpr uint64_t kOnePhaseBytes = 32ull << 30;
-constexpr uint64_t kPhaseBytes = 4ull << 30;
+constexpr uint64_t kPhaseBytes = 3ull << 29;  // 1.5 GiB
 constexpr uint32_t kMinFillPct = 85;
 
 DigestGrid digest_grid(const claim_pool* P, uint64_t refs) {
@@ -2373,6 +2383,7 @@ DigestGrid digest_grid(const claim_pool* P, uint64_t refs) {
     if (P->pgs % d || d > P->slots) continue;  // a phase must fit the resident slots
     const bool one = bytes <= (long double)kOnePhaseBytes;
     if (d > 1 && !one && bytes * d > (long double)kPhaseBytes * P->pgs) continue;
+    if (one && bytes >= (long double)kTwoPhaseBytes && P->pgs >= 2 && 2 * d > P->pgs) continue;
     const uint64_t groups = std::min<uint64_t>(std::max<uint32_t>(1u, P->slots / d), ub);
     const uint64_t fill = (uint64_t)d * groups;
     if (fill * 100 >= (uint64_t)kMinFillPct * P->slots) return {d, (uint32_t)groups};
@@ -2457,7 +2468,8 @@ int claim_pool_create(const claim_pool_desc* d, claim_pool** out) {
       d->block_size == 0 || d->block_size > kMaxBlockSize || d->num_kv_heads == 0 ||
       d->head_dim == 0 || d->elem_bytes == 0 || d->num_blocks == 0 || d->num_blocks >= kNone ||
       !d->kv_base || ((uintptr_t)d->kv_base & 15) || d->max_claims == 0 ||
-      d->event_capacity == 0 || (d->flags & ~(CLAIM_POOL_TIMING | CLAIM_POOL_STAGE_TIMING)))
+      d->event_capacity == 0 ||
+      (d->flags & ~(CLAIM_POOL_TIMING | CLAIM_POOL_STAGE_TIMING)))
     return CLAIM_EINVAL;
   const uint64_t planes = (uint64_t)d->num_layers * d->planes_per_layer;
   const uint64_t chunk = (uint64_t)d->block_size * d->num_kv_heads * d->head_dim * d->elem_bytes;
@@ -2830,6 +2842,18 @@ int claim_identity_stats(claim_pool* P, uint64_t* entries, uint64_t* ambiguous) 
   TRY(read_counters(P));
   if (entries) *entries = P->host_ctr->id_entries;
   if (ambiguous) *ambiguous = P->host_ctr->id_ambiguous;
+  return CLAIM_OK;
+}
+
+int claim_digest_grid(const claim_pool* P, uint64_t refs, claim_grid_info* out) {
+  if (!P || !out) return CLAIM_EINVAL;
+  const DigestGrid gr = digest_grid(P, refs);
+  out->words_per_lane = (uint32_t)P->lpw;
+  out->segments = P->segs;
+  out->piece_groups = P->pgs;
+  out->slots = P->slots;
+  out->pga = gr.pga;
+  out->groups = gr.groups;
   return CLAIM_OK;
 }
 

@@ -26,9 +26,9 @@ GEOMETRIES = [
     Geometry(1, 2, 4, 1, 16, 2, 32),  # 4-token blocks, 128-byte chunks
     Geometry(3, 1, 8, 1, 24, 1, 48),  # fp8 latent, 192-byte chunks
     Geometry(2, 2, 16, 1, 64, 2, 40, total_kv_heads=4, first_kv_head=2),  # a head shard
-    # 600 planes of 16 KiB chunks over 4 blocks: 150 piece groups, whose
-    # digest runs in two phases of 75 (one phase would leave 42 % of the
-    # digest grid idle)
+    # 600 planes of 16 KiB chunks over 4 blocks: 300 piece groups of 8 KiB
+    # pieces, whose digest runs in four phases of 75 (fewer phases would
+    # leave a quarter or more of the digest grid idle)
     Geometry(300, 2, 16, 4, 128, 2, 4),
 ]
 

@@ -48,6 +48,7 @@ def test_record_layouts_match_header(tmp_path):
         "claim_batch": [f for f, _ in ck.CBatch._fields_],
         "claim_fault_spec": [f for f, _ in ck.CFaults._fields_],
         "claim_timing": [f for f, _ in ck.CTiming._fields_],
+        "claim_grid_info": [f for f, _ in ck.CGridInfo._fields_],
     }
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "claimkv.h"', "int main(void){"]
     for st, fs in fields.items():
@@ -67,7 +68,8 @@ def test_record_layouts_match_header(tmp_path):
         for f in dt.names:
             assert int(got[f"{st}.{f}"]) == dt.fields[f][1], (st, f)
     for cls, st in ((ck.PoolDesc, "claim_pool_desc"), (ck.CBatch, "claim_batch"),
-                    (ck.CFaults, "claim_fault_spec"), (ck.CTiming, "claim_timing")):
+                    (ck.CFaults, "claim_fault_spec"), (ck.CTiming, "claim_timing"),
+                    (ck.CGridInfo, "claim_grid_info")):
         assert int(got[st]) == ctypes.sizeof(cls)
         for f, _ in cls._fields_:
             assert int(got[f"{st}.{f}"]) == getattr(cls, f).offset, (st, f)
@@ -93,6 +95,7 @@ def _desc(**kw):
     dict(num_kv_heads=0), dict(head_dim=0), dict(elem_bytes=0), dict(num_blocks=0),
     dict(num_blocks=0xFFFFFFFF), dict(kv_base=None), dict(kv_base=0x10008),
     dict(kv_bytes=(1 << 20) - 1), dict(max_claims=0), dict(event_capacity=0), dict(flags=0x80),
+    dict(flags=0x4),
     # head shards: past the full block's heads, or head rows that are not whole words
     dict(total_kv_heads=4, first_kv_head=3), dict(first_kv_head=1), dict(total_kv_heads=1),
     dict(head_dim=2, elem_bytes=1, total_kv_heads=4),
@@ -105,9 +108,10 @@ def test_pool_create_rejects_bad_descriptions(L, bad):
 
 
 @pytest.mark.parametrize("ok", [dict(total_kv_heads=8, first_kv_head=6), dict(total_kv_heads=2),
-                                dict(total_kv_heads=0, first_kv_head=0)])
+                                dict(total_kv_heads=0, first_kv_head=0),
+                                dict(flags=ck.POOL_TIMING | ck.POOL_STAGE_TIMING)])
 def test_pool_create_accepts_head_shards(L, ok):
-    """Valid head-shard descriptions pass validation (without a GPU the
+    """Valid head-shard descriptions and flags pass validation (without a GPU the
     call then fails in the runtime, never with EINVAL)."""
     d = _desc(**ok)
     h = ctypes.c_void_p()
@@ -138,6 +142,8 @@ def test_null_arguments_are_rejected(L):
     assert L.claim_block_state_read(None, 0, 0, None, None, None, None) == ck.EINVAL
     assert L.claim_lookup(None, ctypes.byref(b), None, 0) == ck.EINVAL
     assert L.claim_identity_stats(None, None, None) == ck.EINVAL
+    g = ck.CGridInfo()
+    assert L.claim_digest_grid(None, 0, ctypes.byref(g)) == ck.EINVAL
     assert L.claim_pool_destroy(None) == ck.OK
 
 

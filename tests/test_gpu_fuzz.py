@@ -1,6 +1,6 @@
 """Differential test of the library against the oracle over seeded irregular
 lifecycles (tests/fuzz_cases.py): five pool geometries (one a head shard, one
-whose digest runs in two phases), offload batches with empty, long, missing,
+whose digest runs in four phases), offload batches with empty, long, missing,
 out-of-range, malformed and entry-sharing rows, reserved ids and predicates,
 shared and duplicate-owned identities, faults, a partial restore (in a third
 of the cases from device staging, after the staged blocks' device copies are

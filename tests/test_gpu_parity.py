@@ -122,9 +122,9 @@ MIN_BS = Workload(
 
 # Many planes with few digest workgroups each: the digest reads its piece
 # groups in phases so that the grid stays full.  320 planes of 32 KiB chunks
-# (160 piece groups, two phases of 80) and 122 planes of 36 KiB chunks in
-# three 12 KiB pieces each (92 piece groups, the last with two pieces; two
-# phases of 46).
+# in four 8 KiB pieces each (320 piece groups, four phases of 80) and 122
+# planes of 36 KiB chunks in three 12 KiB pieces each (92 piece groups, the
+# last with two pieces; two phases of 46).
 MANY_PLANES = Workload(
     name="320-planes-phased", geometry=Geometry(160, 2, 16, 8, 128, 2, 24), seed=41, num_claims=30,
     length=("blocks", 1, 6, True), sharing=("fraction", 0.3), corrupt_rate=0.15, num_load_failed=1,
