@@ -2344,8 +2344,9 @@ int choose_digest_shape(claim_pool* P) {
 //
 // Reading every piece group at once suits pools of up to about 13 GB;
 // from kTwoPhaseBytes to kOnePhaseBytes of referenced blocks a launch reads
-// in at least two phases, and past kOnePhaseBytes in phases of at most
-// kPhaseBytes.  Measured on MI355X with 8 KiB pieces, each comparison in one
+// an even number of piece groups in two phases (an odd number, where only
+// more phases would divide it evenly, stays in one), and past
+// kOnePhaseBytes in phases of at most kPhaseBytes.  Measured on MI355X with 8 KiB pieces, each comparison in one
 // process over one allocation, in several processes: two phases read the
 // 17 GB 8B pool 0.7-1.6 % faster than one (32 piece groups at a time
 // instead of 64; more phases were slower) and the 30 GB stress pool
@@ -2383,7 +2384,7 @@ DigestGrid digest_grid(const claim_pool* P, uint64_t refs) {
     if (P->pgs % d || d > P->slots) continue;  // a phase must fit the resident slots
     const bool one = bytes <= (long double)kOnePhaseBytes;
     if (d > 1 && !one && bytes * d > (long double)kPhaseBytes * P->pgs) continue;
-    if (one && bytes >= (long double)kTwoPhaseBytes && P->pgs >= 2 && 2 * d > P->pgs) continue;
+    if (one && bytes >= (long double)kTwoPhaseBytes && P->pgs % 2 == 0 && 2 * d > P->pgs) continue;
     const uint64_t groups = std::min<uint64_t>(std::max<uint32_t>(1u, P->slots / d), ub);
     const uint64_t fill = (uint64_t)d * groups;
     if (fill * 100 >= (uint64_t)kMinFillPct * P->slots) return {d, (uint32_t)groups};
