@@ -2342,16 +2342,21 @@ int choose_digest_shape(claim_pool* P) {
 // the piece-group count, so that every workgroup runs the same number of
 // phases) and how many workgroups share each (groups = slots / pga).
 //
-// Reading every piece group at once suits pools of up to about 13 GB;
-// from kTwoPhaseBytes to kOnePhaseBytes of referenced blocks a launch reads
-// an even number of piece groups in two phases (an odd number, where only
-// more phases would divide it evenly, stays in one), and past
-// kOnePhaseBytes in phases of at most kPhaseBytes.  Measured on MI355X with 8 KiB pieces, each comparison in one
-// process over one allocation, in several processes: two phases read the
-// 17 GB 8B pool 0.7-1.6 % faster than one (32 piece groups at a time
-// instead of 64; more phases were slower) and the 30 GB stress pool
-// 0.4-0.8 % faster (14 instead of 28), while the 13.5 GB MLA pool read
-// 1.4 % slower in two phases and the 13.1 GB 70B head shard no faster.
+// Reading every piece group at once suits pools of up to about 13 GB.
+// From kTwoPhaseBytes to kOnePhaseBytes of referenced blocks a launch reads
+// in two phases when the piece groups split evenly in two at a plane
+// chunk's edge (an even count, half of whose pieces make whole chunks), so
+// that no chunk is read partly in each phase; otherwise in one.  Past
+// kOnePhaseBytes it reads in phases of at most kPhaseBytes.  Measured on
+// MI355X with 8 KiB pieces, each comparison in one process over one
+// allocation, in several processes: two phases read the 17 GB 8B pool
+// 0.7-1.6 % faster than one (32 piece groups at a time instead of 64; more
+// phases were slower), the 30 GB stress pool 0.4-0.8 % faster (14 instead
+// of 28), 128-plane pools of 16 KiB chunks of 17 and 34 GB 1.8 % and 2.3 %
+// faster, and 64-plane pools of 16 KiB chunks within 0.3 %.  MLA pools,
+// whose 36 KiB chunks are three 12 KiB pieces so that half the piece groups
+// end inside a chunk, read 1.1-1.5 % slower in two phases (13.5 and
+// 17.1 GB), and the 13.1 GB 70B head shard no faster.
 // Over the 105 GB 70B pool (160 piece groups), 2 piece groups at a time
 // (phases of 1.3 GB) read 1.0-1.4 % faster than 5 (3.3 GB phases, the
 // bound of 4 GiB used before), and every other size from 1 to 80 was slower
@@ -2380,11 +2385,14 @@ DigestGrid digest_grid(const claim_pool* P, uint64_t refs) {
   const long double bytes = (long double)ub * P->block_bytes;
   DigestGrid best{1, 1};
   uint64_t best_fill = 0;
+  const bool one = bytes <= (long double)kOnePhaseBytes;
+  // two phases where half the piece groups end on a plane chunk's edge
+  const bool two = one && bytes >= (long double)kTwoPhaseBytes && P->pgs % 2 == 0 &&
+                   (2ull * P->pgs) % P->segs == 0;
   for (uint32_t d = P->pgs; d >= 1; --d) {
     if (P->pgs % d || d > P->slots) continue;  // a phase must fit the resident slots
-    const bool one = bytes <= (long double)kOnePhaseBytes;
     if (d > 1 && !one && bytes * d > (long double)kPhaseBytes * P->pgs) continue;
-    if (one && bytes >= (long double)kTwoPhaseBytes && P->pgs % 2 == 0 && 2 * d > P->pgs) continue;
+    if (two && 2 * d > P->pgs) continue;
     const uint64_t groups = std::min<uint64_t>(std::max<uint32_t>(1u, P->slots / d), ub);
     const uint64_t fill = (uint64_t)d * groups;
     if (fill * 100 >= (uint64_t)kMinFillPct * P->slots) return {d, (uint32_t)groups};

@@ -1,7 +1,8 @@
 """The digest grid each workload's launches take (claim_digest_grid) on a
 256-CU MI355X: one phase for the 13 GB MLA and head-shard pools, two for
-the 17 GB 8B and 30 GB stress pools (14 to 32 GiB, an even number of piece
-groups; one for an odd number), and for the 105 GB 70B
+the 17 GB 8B and 30 GB stress pools (14 to 32 GiB, split in two at a plane
+chunk's edge; one for an odd number of piece groups, and one for an MLA pool
+whose halves would end inside a chunk), and for the 105 GB 70B
 pool two piece groups at a time in phases of 1.3 GB; the many-plane pools of the parity and fuzz tests, and a
 launch of the 70B pool over few blocks, in the phases that keep the grid
 full.
@@ -26,6 +27,9 @@ CASES = [
     # the 70B pool under a batch of 300 entries: 1.6 GB, within one phase's
     # bound, read in the two phases that fill the grid
     ("llama3-70b-300-refs", FULL["llama3-70b"].geometry, 300, (16, 4, 160, 256, 80, 3)),
+    # 17.1 GB of 36 KiB chunks in three 12 KiB pieces: half of the 46 piece
+    # groups would end inside a chunk, so one phase
+    ("mla-shaped-17.1GB", Geometry(61, 1, 64, 1, 576, 1, 7600), None, (24, 3, 46, 256, 46, 5)),
     # 15.9 GB in an odd number of piece groups (27): one phase
     ("odd-piece-groups-15.9GB", Geometry(27, 2, 16, 4, 128, 2, 18000), None, (16, 2, 27, 256, 27, 9)),
     (MANY_PLANES.name, MANY_PLANES.geometry, None, (16, 4, 320, 256, 80, 3)),
