@@ -18,8 +18,9 @@
 //    with all LPW loads in flight before any use.  The 4 waves of a workgroup take 4 consecutive pieces
 //    of the same blocks and park their per-block sums in an LDS ring, which
 //    the workgroup adds and writes as one contiguous run of partials; the
-//    grid is exactly one resident round, and on the largest pools it reads
-//    the piece groups a few at a time, in phases.  Each 64-bit word costs one
+//    grid is exactly one resident round, and on larger pools it reads the
+//    piece groups in phases (two from 14 GiB, a few piece groups at a time
+//    past 32 GiB).  Each 64-bit word costs one
 //    32x32->64 multiply-add for lo(w) lo(k) and two 32-bit multiply-adds for
 //    the cross terms (only their low 32 bits reach the result mod 2^64).  A
 //    small kernel adds each block's partials.  No atomics: results are
